@@ -1,0 +1,126 @@
+"""Seeded synthetic masks for the five EDT workloads.
+
+This module only draws inputs: it holds none of the distance-transform
+arithmetic, and both the GPU tests and the CPU oracle's checks take their
+masks from here.  Masks are uint8 arrays shaped (B, C, *spatial) with
+nonzero = foreground, C = 1.
+
+Every sample b of workload k draws from numpy's PCG64 seeded with
+``[260824738, k, b]``.  Voxel centres sit at integer coordinates, ball
+centres are continuous U[0, n_a) per axis, radii continuous U[r_min, r_max],
+and a voxel is inside a ball iff sum_a (i_a - c_a)^2 <= r^2.
+
+The paper's own benchmark masks are not described beyond their sizes, so
+these shapes, densities and structures stand in for them:
+
+  1  2-D  1x1x64x64,        foreground iff U < 0.9                 (dist + idx)
+  2  2-D  32x1x512x512,     background = union of 20 discs,
+                            r ~ U[5, 60]                           (dist)
+  3  3-D  8x1x128^3,        foreground = union of 30 balls,
+                            r ~ U[4, 30]                           (dist, exact d^2)
+  4  3-D  2x1x256^3,        background iff U < 0.01,
+                            sampling (2.5, 0.8, 0.8)               (dist + idx)
+  5  4-D  4x1x32x64x64x64,  background iff U < 1e-4, at least one
+                            background voxel per sample            (dist)
+
+Smaller twins keep the generator and scale ball radii with the smallest
+extent, so parity tests can cover the same structure at sizes the oracle
+finishes in seconds.
+"""
+from __future__ import annotations
+
+import hashlib
+from dataclasses import dataclass, field
+
+import numpy as np
+
+SEED = 260824738
+
+
+@dataclass(frozen=True)
+class Workload:
+    key: int
+    name: str
+    batch: int
+    spatial: tuple
+    kind: str                    # "bernoulli_fg", "discs_bg", "balls_fg", "bernoulli_bg"
+    param: dict = field(default_factory=dict)
+    sampling: tuple | None = None
+    want_idx: bool = False
+
+    @property
+    def ndim(self) -> int:
+        return len(self.spatial)
+
+    @property
+    def voxels(self) -> int:
+        return int(self.batch * np.prod(self.spatial, dtype=np.int64))
+
+
+WORKLOADS = {
+    1: Workload(1, "edt2d_1x64x64_bernoulli", 1, (64, 64), "bernoulli_fg",
+                {"p_fg": 0.9}, None, True),
+    2: Workload(2, "edt2d_32x512x512_discs", 32, (512, 512), "discs_bg",
+                {"count": 20, "r_min": 5.0, "r_max": 60.0}),
+    3: Workload(3, "edt3d_8x128x128x128_balls", 8, (128, 128, 128), "balls_fg",
+                {"count": 30, "r_min": 4.0, "r_max": 30.0}),
+    4: Workload(4, "edt3d_2x256x256x256_aniso", 2, (256, 256, 256), "bernoulli_bg",
+                {"p_bg": 0.01, "at_least_one": False}, (2.5, 0.8, 0.8), True),
+    5: Workload(5, "edt4d_4x32x64x64x64_sparse", 4, (32, 64, 64, 64), "bernoulli_bg",
+                {"p_bg": 1e-4, "at_least_one": True}),
+}
+
+
+def _balls(rng, spatial, count, r_min, r_max, scale):
+    """Boolean union of `count` solid balls with continuous centres and radii."""
+    out = np.zeros(spatial, dtype=bool)
+    nd = len(spatial)
+    for _ in range(count):
+        c = np.array([rng.uniform(0.0, n) for n in spatial])
+        r = rng.uniform(r_min, r_max) * scale
+        lo = [max(0, int(np.floor(c[a] - r))) for a in range(nd)]
+        hi = [min(spatial[a], int(np.ceil(c[a] + r)) + 1) for a in range(nd)]
+        if any(h <= l for l, h in zip(lo, hi)):
+            continue
+        grids = np.ogrid[tuple(slice(l, h) for l, h in zip(lo, hi))]
+        d2 = sum((g - c[a]) ** 2 for a, g in enumerate(grids))
+        region = tuple(slice(l, h) for l, h in zip(lo, hi))
+        out[region] |= d2 <= r * r
+    return out
+
+
+def sample_mask(w: Workload, b: int, spatial=None) -> np.ndarray:
+    """Mask of sample `b` (uint8, nonzero = foreground) at `spatial` (default: full size)."""
+    spatial = tuple(w.spatial if spatial is None else spatial)
+    rng = np.random.default_rng([SEED, w.key, b])
+    scale = min(spatial) / min(w.spatial)
+    if w.kind == "bernoulli_fg":
+        fg = rng.random(spatial) < w.param["p_fg"]
+    elif w.kind == "bernoulli_bg":
+        bg = rng.random(spatial) < w.param["p_bg"]
+        if w.param.get("at_least_one") and not bg.any():
+            pos = tuple(int(rng.integers(0, n)) for n in spatial)
+            bg[pos] = True
+        fg = ~bg
+    elif w.kind == "discs_bg":
+        fg = ~_balls(rng, spatial, w.param["count"], w.param["r_min"], w.param["r_max"], scale)
+    elif w.kind == "balls_fg":
+        fg = _balls(rng, spatial, w.param["count"], w.param["r_min"], w.param["r_max"], scale)
+    else:
+        raise ValueError(w.kind)
+    return fg.astype(np.uint8)
+
+
+def make_mask(key: int, spatial=None, batch=None) -> np.ndarray:
+    """(B, 1, *spatial) uint8 mask of workload `key`, optionally at a smaller size."""
+    w = WORKLOADS[key]
+    spatial = tuple(w.spatial if spatial is None else spatial)
+    batch = w.batch if batch is None else int(batch)
+    out = np.empty((batch, 1) + spatial, dtype=np.uint8)
+    for b in range(batch):
+        out[b, 0] = sample_mask(w, b, spatial)
+    return out
+
+
+def mask_digest(mask: np.ndarray) -> str:
+    return hashlib.sha256(np.ascontiguousarray(mask).tobytes()).hexdigest()
