@@ -1,0 +1,124 @@
+/*
+ * tm_edt.h -- exact Euclidean distance transform on AMD MI355X (gfx950).
+ *
+ * The operation (paper, Section 2.1 "Distance transforms"; kernels in Section
+ * 2.3.2 "Distance-transform kernels"): for each of `batch` independent
+ * samples with spatial extents shape[0..ndim), every element x receives the
+ * distance to the nearest background (zero) element y of its sample,
+ *
+ *     D(x) = sqrt( min over background y of  sum_a s_a^2 (x_a - y_a)^2 ),
+ *
+ * where s is the optional per-axis sampling (paper, Section 2.2.1: the
+ * distance transforms take SciPy's `sampling`, `return_distances` and
+ * `return_indices` arguments), and optionally the coordinates of that y.
+ * Inputs shaped (B, C, spatial...) pass batch = B * C (Section 2.3.2: the
+ * passes run over B*C*n^(d-1) independent lines).
+ *
+ * Conventions shared by every entry point:
+ *   - Layout: C order.  in_u8 is [batch][shape[0]]...[shape[ndim-1]] bytes,
+ *     nonzero = foreground, zero = background.  Distance-like outputs have
+ *     the same layout; out_idx is [batch][ndim][shape...] int32, so each
+ *     sample's block matches SciPy's (ndim, *shape) index array.
+ *   - Memory: in_u8, out_* are DEVICE pointers owned by the caller; shape
+ *     and sampling are HOST pointers read during the call only.  The library
+ *     allocates no device memory; intermediate results live in the output
+ *     buffers, which are overwritten in full.
+ *   - Streams: all work is enqueued on `stream` (0 = the null stream) of the
+ *     current device and the call returns without waiting for it.  Results
+ *     are valid once that stream has been synchronised.  Calls are reentrant;
+ *     calls on different streams must not share output buffers.
+ *   - Ties: the returned element is the nearest background element with the
+ *     smallest row-major flat index (the paper asks only for a genuine
+ *     nearest background element, Section 2.4).
+ *   - No background: a sample with no zero is measured against the virtual
+ *     element (-1, 0, ..., 0), which is also the index reported (paper,
+ *     Section 2.3.2: SciPy's virtual out-of-bounds convention).
+ *   - Errors: every function returns a tm_status.  Arguments are validated on
+ *     the host before any HIP call; a rejected call enqueues nothing.  Nothing
+ *     throws or aborts across this interface.
+ */
+#ifndef TM_EDT_H
+#define TM_EDT_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TM_OK = 0,
+    TM_ERR_NDIM = -1,        /* ndim outside [1, 8] (paper Section 2.2.1 caps the rank at 8) */
+    TM_ERR_SHAPE = -2,       /* shape is NULL or an extent is < 1 */
+    TM_ERR_BATCH = -3,       /* batch < 1 */
+    TM_ERR_NULL = -4,        /* in_u8 is NULL */
+    TM_ERR_NO_OUTPUT = -5,   /* every output pointer is NULL */
+    TM_ERR_SAMPLING = -6,    /* a sampling entry is not finite or not > 0 */
+    TM_ERR_TOO_LARGE = -7,   /* >= 2^31 elements per sample, batch * elements overflows,
+                                or (unit sampling) squared distances may exceed int32 */
+    TM_ERR_ALIAS = -8,       /* two of the buffers overlap */
+    TM_ERR_UNSUPPORTED = -9, /* a line is longer than the envelope kernels hold in LDS */
+    TM_ERR_HIP = -10         /* the HIP runtime reported an error while enqueuing */
+} tm_status;
+
+/*
+ * tm_edt -- distances and/or nearest-background indices.
+ *
+ *   sampling  NULL, or ndim spacings (all finite and > 0).  NULL or all 1.0
+ *             runs the exact integer path (squared distances are exact
+ *             integers; out_dist is the correctly rounded float sqrt).  Other
+ *             spacings run with float32 storage and double breakpoint tests;
+ *             distances then agree with an exact evaluation to ~1e-6 relative.
+ *   out_dist  NULL, or [batch][shape...] float32 distances.
+ *   out_idx   NULL, or [batch][ndim][shape...] int32 coordinates of the
+ *             nearest background element.
+ * At least one of out_dist and out_idx must be non-NULL.
+ */
+int tm_edt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
+           const double *sampling, float *out_dist, int32_t *out_idx,
+           hipStream_t stream);
+
+/*
+ * tm_edt_sq -- exact integer squared distances (unit sampling).
+ *
+ *   out_sq    NULL, or [batch][shape...] int32 squared distances.
+ *   out_idx   NULL, or [batch][ndim][shape...] int32 coordinates.
+ * At least one must be non-NULL.  The sum of squared extents must stay below
+ * 2^31 (TM_ERR_TOO_LARGE otherwise).
+ */
+int tm_edt_sq(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
+              int32_t *out_sq, int32_t *out_idx, hipStream_t stream);
+
+/* Static English text for a tm_status value (never NULL). */
+const char *tm_strerror(int status);
+
+/*
+ * Kernel timing for measurement tools (not needed for computing).
+ *
+ * tm_prof_enable(n) with n > 0 makes subsequent tm_edt / tm_edt_sq calls
+ * from any thread bracket each kernel they launch with a pair of HIP events
+ * on the call's stream, for up to n kernels (later kernels go untimed);
+ * n = 0 disables timing and releases the events.  tm_prof_count() returns
+ * how many kernels were bracketed since enabling; after synchronising the
+ * stream, tm_prof_read(i, &name, &ms) returns kernel i's static name and its
+ * event-to-event time in milliseconds.  Returns TM_OK, TM_ERR_HIP, or
+ * TM_ERR_SHAPE for an index out of range.  Not reentrant with itself.
+ */
+int tm_prof_enable(int max_kernels);
+int tm_prof_count(void);
+int tm_prof_read(int i, const char **name, float *ms);
+
+/*
+ * tm_selftest_host -- checks the host-side planning arithmetic (the
+ * division-by-invariant-integer constants the kernels use to split flat
+ * indices) without touching any GPU.  Returns TM_OK or a negative count of
+ * failures.
+ */
+int tm_selftest_host(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TM_EDT_H */

@@ -1,0 +1,241 @@
+"""Python binding of ``libtm_edt.so``: argument marshalling only.
+
+Every step of the transform runs in the library's HIP kernels; this module
+turns torch tensors into device pointers, shapes and the current HIP stream,
+and turns status codes into exceptions.  There is no fallback: if the library
+is missing, every call raises.
+
+Entry points with the C names (``tm_edt``, ``tm_edt_sq``, ``tm_strerror``)
+plus a ``scipy.ndimage.distance_transform_edt``-style wrapper over
+(B, C, *spatial) tensors (paper, Section 2.2.1).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libtm_edt.so")
+_lock = threading.Lock()
+_lib = None
+
+TM_OK = 0
+
+
+class TMError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s failed: %s (status %d)" % (where, tm_strerror(status), status))
+
+
+def load() -> ctypes.CDLL:
+    """Open the library (once). Raises if it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(
+                    "libtm_edt.so is not built (expected at %s); run "
+                    "`python -m paper_2608_24738_amd.build` or __graft_entry__.build()" % LIB_PATH)
+            lib = ctypes.CDLL(LIB_PATH)
+            vp, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
+            lib.tm_edt.restype = i32
+            lib.tm_edt.argtypes = [vp, i32, vp, i64, vp, vp, vp, vp]
+            lib.tm_edt_sq.restype = i32
+            lib.tm_edt_sq.argtypes = [vp, i32, vp, i64, vp, vp, vp]
+            lib.tm_strerror.restype = ctypes.c_char_p
+            lib.tm_strerror.argtypes = [i32]
+            lib.tm_prof_enable.restype = i32
+            lib.tm_prof_enable.argtypes = [i32]
+            lib.tm_prof_count.restype = i32
+            lib.tm_prof_count.argtypes = []
+            lib.tm_prof_read.restype = i32
+            lib.tm_prof_read.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p),
+                                         ctypes.POINTER(ctypes.c_float)]
+            lib.tm_selftest_host.restype = i32
+            lib.tm_selftest_host.argtypes = []
+            _lib = lib
+    return _lib
+
+
+def tm_strerror(status: int) -> str:
+    return load().tm_strerror(int(status)).decode()
+
+
+def _stream_handle(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def _shape_args(x: torch.Tensor, ndim: int):
+    if x.dim() < ndim:
+        raise ValueError("input has fewer than ndim=%d dimensions" % ndim)
+    spatial = tuple(int(s) for s in x.shape[x.dim() - ndim:])
+    batch = 1
+    for s in x.shape[:x.dim() - ndim]:
+        batch *= int(s)
+    return spatial, batch
+
+
+def _check_mask(in_u8: torch.Tensor):
+    if not in_u8.is_cuda:
+        raise ValueError("input must be a ROCm (cuda) tensor")
+    if in_u8.dtype not in (torch.uint8, torch.bool):
+        raise TypeError("input must be uint8 or bool (nonzero = foreground); got %s" % in_u8.dtype)
+    if not in_u8.is_contiguous():
+        raise ValueError("tm_edt needs a contiguous input")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _check_out(t, dtype, numel, name, dev):
+    if t is None:
+        return
+    if t.dtype != dtype or not t.is_contiguous() or t.numel() != numel or t.device != dev:
+        raise ValueError("%s must be a contiguous %s tensor of %d elements on %s"
+                         % (name, dtype, numel, dev))
+
+
+def tm_edt(in_u8: torch.Tensor, ndim: int, sampling=None, out_dist=None, out_idx=None,
+           stream=None) -> None:
+    """Calls tm_edt on (batch..., *spatial) ``in_u8``; outputs are filled in place."""
+    _check_mask(in_u8)
+    spatial, batch = _shape_args(in_u8, ndim)
+    vox = in_u8.numel() // max(batch, 1)
+    _check_out(out_dist, torch.float32, batch * vox, "out_dist", in_u8.device)
+    _check_out(out_idx, torch.int32, batch * vox * ndim, "out_idx", in_u8.device)
+    shape = (ctypes.c_int64 * ndim)(*spatial)
+    samp = None
+    if sampling is not None:
+        samp = (ctypes.c_double * ndim)(*[float(s) for s in sampling])
+    with torch.cuda.device(in_u8.device):
+        st = _stream_handle(stream)
+        rc = load().tm_edt(_ptr(in_u8), ndim, shape, batch, samp, _ptr(out_dist), _ptr(out_idx),
+                           ctypes.c_void_p(st))
+    if rc != TM_OK:
+        raise TMError(rc, "tm_edt")
+
+
+def tm_edt_sq(in_u8: torch.Tensor, ndim: int, out_sq=None, out_idx=None, stream=None) -> None:
+    """Calls tm_edt_sq (exact int32 squared distances, unit sampling)."""
+    _check_mask(in_u8)
+    spatial, batch = _shape_args(in_u8, ndim)
+    vox = in_u8.numel() // max(batch, 1)
+    _check_out(out_sq, torch.int32, batch * vox, "out_sq", in_u8.device)
+    _check_out(out_idx, torch.int32, batch * vox * ndim, "out_idx", in_u8.device)
+    shape = (ctypes.c_int64 * ndim)(*spatial)
+    with torch.cuda.device(in_u8.device):
+        st = _stream_handle(stream)
+        rc = load().tm_edt_sq(_ptr(in_u8), ndim, shape, batch, _ptr(out_sq), _ptr(out_idx),
+                              ctypes.c_void_p(st))
+    if rc != TM_OK:
+        raise TMError(rc, "tm_edt_sq")
+
+
+def _normalise_sampling(sampling, ndim):
+    if sampling is None:
+        return None
+    if isinstance(sampling, (int, float)):
+        return [float(sampling)] * ndim
+    s = [float(x) for x in sampling]
+    if len(s) != ndim:
+        raise RuntimeError("sequence argument must have length equal to input rank")
+    return s
+
+
+def _as_mask(input: torch.Tensor) -> torch.Tensor:
+    if input.dtype == torch.bool:
+        input = input.view(torch.uint8)
+    elif input.dtype != torch.uint8:
+        raise TypeError("input must be uint8 or bool (nonzero = foreground); convert other "
+                        "dtypes with (x != 0) first; got %s" % input.dtype)
+    return input.contiguous()
+
+
+def distance_transform_edt(input: torch.Tensor, sampling=None, return_distances: bool = True,
+                           return_indices: bool = False, distances=None, indices=None):
+    """``scipy.ndimage.distance_transform_edt`` over a (B, C, *spatial) batch.
+
+    Returns float32 distances (B, C, *S) and/or int32 indices (B, C, len(S), *S),
+    like scipy (a tuple when both are requested).  Pre-allocated ``distances`` /
+    ``indices`` are filled in place and not returned.  Distances are float32.
+    """
+    if input.dim() < 3:
+        raise ValueError("input must be (B, C, *spatial) with 1 to 8 spatial dimensions")
+    ndim = input.dim() - 2
+    if ndim > 8:
+        raise ValueError("at most 8 spatial dimensions are supported")
+    if not (return_distances or return_indices):
+        raise RuntimeError("at least one of return_distances/return_indices must be True")
+    samp = _normalise_sampling(sampling, ndim)
+    mask = _as_mask(input)
+    lead = tuple(mask.shape[:2])
+    spatial = tuple(mask.shape[2:])
+    dev = mask.device
+    dist_out = None
+    if return_distances:
+        if distances is not None:
+            if distances.shape != mask.shape or distances.dtype != torch.float32:
+                raise RuntimeError("distances array has wrong shape or type")
+            dist_out = distances
+        else:
+            dist_out = torch.empty(mask.shape, dtype=torch.float32, device=dev)
+    idx_out = None
+    if return_indices:
+        want = lead + (ndim,) + spatial
+        if indices is not None:
+            if tuple(indices.shape) != want or indices.dtype != torch.int32:
+                raise RuntimeError("indices array has wrong shape or type")
+            idx_out = indices
+        else:
+            idx_out = torch.empty(want, dtype=torch.int32, device=dev)
+    tm_edt(mask, ndim, samp, dist_out, idx_out)
+    result = []
+    if return_distances and distances is None:
+        result.append(dist_out)
+    if return_indices and indices is None:
+        result.append(idx_out)
+    if not result:
+        return None
+    return result[0] if len(result) == 1 else tuple(result)
+
+
+def distance_transform_edt_sq(input: torch.Tensor, return_indices: bool = False):
+    """Exact int32 squared distances (unit sampling) of a (B, C, *spatial) batch."""
+    if input.dim() < 3:
+        raise ValueError("input must be (B, C, *spatial)")
+    ndim = input.dim() - 2
+    mask = _as_mask(input)
+    sq = torch.empty(mask.shape, dtype=torch.int32, device=mask.device)
+    idx = None
+    if return_indices:
+        idx = torch.empty(tuple(mask.shape[:2]) + (ndim,) + tuple(mask.shape[2:]),
+                          dtype=torch.int32, device=mask.device)
+    tm_edt_sq(mask, ndim, sq, idx)
+    return (sq, idx) if return_indices else sq
+
+
+def prof_enable(max_kernels: int) -> None:
+    rc = load().tm_prof_enable(int(max_kernels))
+    if rc != TM_OK:
+        raise TMError(rc, "tm_prof_enable")
+
+
+def prof_read() -> list:
+    """[(kernel name, ms)] for every kernel timed since prof_enable (stream must be synced)."""
+    lib = load()
+    out = []
+    for i in range(lib.tm_prof_count()):
+        name = ctypes.c_char_p()
+        ms = ctypes.c_float()
+        rc = lib.tm_prof_read(i, ctypes.byref(name), ctypes.byref(ms))
+        if rc != TM_OK:
+            raise TMError(rc, "tm_prof_read")
+        out.append((name.value.decode(), float(ms.value)))
+    return out

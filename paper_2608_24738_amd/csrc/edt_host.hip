@@ -1,0 +1,441 @@
+// edt_host.hip -- C-ABI of the MI355X exact Euclidean distance transform:
+// argument validation, pass planning and kernel launches (declared in
+// include/tm_edt.h).
+//
+// Pass order (paper, Section 2.3.2: one 1-D pass per axis): the contiguous
+// last axis first, as a nearest-zero scan of the mask; then every strided
+// axis down to axis 0 as an in-place lower-envelope pass; the axis-0 pass
+// also writes the final outputs (square root, virtual background element,
+// coordinates).  Running axis 0 last makes the reported index the nearest
+// background element with the smallest row-major flat index.
+//
+// Two carriers: without indices the squared distance itself is carried in
+// the distance (or squared-distance) output; with indices the flat index of
+// the nearest background element is carried in slice 0 of the index output
+// and distances are recomputed from it.
+
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cmath>
+#include <mutex>
+#include <vector>
+
+#include "../../include/tm_edt.h"
+#include "edt_common.h"
+#include "edt_fh.h"
+#include "edt_scan.h"
+
+using namespace tmedt;
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Kernel timing (measurement tools only).
+// ---------------------------------------------------------------------------
+struct Prof {
+    std::mutex mu;
+    int cap = 0;
+    std::atomic<int> next{0};
+    std::vector<hipEvent_t> start, stop;
+    std::vector<const char *> names;
+};
+Prof &prof() {
+    static Prof p;
+    return p;
+}
+
+int prof_begin(const char *name, hipStream_t s) {
+    Prof &p = prof();
+    if (p.cap <= 0) return -1;
+    int slot = p.next.fetch_add(1);
+    if (slot >= p.cap) return -1;
+    p.names[slot] = name;
+    (void)hipEventRecord(p.start[slot], s);
+    return slot;
+}
+void prof_end(int slot, hipStream_t s) {
+    if (slot >= 0) (void)hipEventRecord(prof().stop[slot], s);
+}
+
+// ---------------------------------------------------------------------------
+// Launch helpers.
+// ---------------------------------------------------------------------------
+template <typename K>
+hipError_t allow_lds(K kernel, size_t bytes) {
+    if (bytes <= 64 * 1024) return hipSuccess;
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, int(bytes));
+}
+
+template <typename K, typename Args>
+int launch(const char *name, K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+           const Args &args) {
+    if (allow_lds(kernel, lds) != hipSuccess) return TM_ERR_HIP;
+    int slot = prof_begin(name, s);
+    hipLaunchKernelGGL(kernel, grid, block, lds, s, args);
+    hipError_t e = hipGetLastError();
+    prof_end(slot, s);
+    return e == hipSuccess ? TM_OK : TM_ERR_HIP;
+}
+
+int bits_for(uint64_t x) {
+    int b = 0;
+    while (b < 64 && (x >> b) != 0) ++b;
+    return b;
+}
+
+bool overlaps(const void *a, uint64_t na, const void *b, uint64_t nb) {
+    if (!a || !b || na == 0 || nb == 0) return false;
+    uintptr_t a0 = uintptr_t(a), b0 = uintptr_t(b);
+    return a0 < b0 + nb && b0 < a0 + na;
+}
+
+// Lanes per workgroup whose envelope stacks of n entries x eb bytes fit LDS.
+uint32_t lanes_for(uint32_t n, uint32_t eb) {
+    for (uint32_t l = kWave; l >= 1; l >>= 1)
+        if (uint64_t(n) * l * eb <= kLdsBytes) return l;
+    return 0;
+}
+
+// Unit sampling: int32 suffices for every breakpoint product of a pass over
+// lines of length n when the carried squared distance is at most fmax.
+bool int32_safe(uint64_t fmax, uint64_t n) {
+    const uint64_t lim = (uint64_t(1) << 31) - 1;
+    uint64_t key = fmax + (n - 1) * (n - 1);
+    uint64_t den = 2 * (n - 1);
+    if (key >= lim) return false;
+    if (den && key > lim / den) return false;
+    if ((n - 1) * den >= lim) return false;
+    return true;
+}
+
+struct Request {
+    const uint8_t *in;
+    int ndim;
+    uint32_t shape[kMaxDim];
+    uint64_t batch;
+    bool unit;
+    double w[kMaxDim];
+    float *dist;
+    int32_t *sq;
+    int32_t *idx;
+    hipStream_t stream;
+};
+
+int validate(const uint8_t *in, int ndim, const int64_t *shape, int64_t batch,
+             const double *sampling, const void *o1, const void *o2, const void *o3,
+             Request &r) {
+    if (ndim < 1 || ndim > kMaxDim) return TM_ERR_NDIM;
+    if (!shape) return TM_ERR_SHAPE;
+    for (int a = 0; a < ndim; ++a)
+        if (shape[a] < 1) return TM_ERR_SHAPE;
+    if (batch < 1) return TM_ERR_BATCH;
+    if (!in) return TM_ERR_NULL;
+    if (!o1 && !o2 && !o3) return TM_ERR_NO_OUTPUT;
+    r.unit = true;
+    for (int a = 0; a < ndim; ++a) {
+        double s = sampling ? sampling[a] : 1.0;
+        if (!(s > 0.0) || !std::isfinite(s)) return TM_ERR_SAMPLING;
+        if (s != 1.0) r.unit = false;
+        r.w[a] = s * s;
+    }
+    uint64_t vox = 1, sumsq = 0;
+    for (int a = 0; a < ndim; ++a) {
+        if (uint64_t(shape[a]) >= (uint64_t(1) << 31)) return TM_ERR_TOO_LARGE;
+        vox *= uint64_t(shape[a]);
+        if (vox >= (uint64_t(1) << 31)) return TM_ERR_TOO_LARGE;
+        sumsq += uint64_t(shape[a]) * uint64_t(shape[a]);
+        r.shape[a] = uint32_t(shape[a]);
+    }
+    if (uint64_t(batch) >= (uint64_t(1) << 32) / vox) return TM_ERR_TOO_LARGE;
+    if (r.unit && sumsq >= (uint64_t(1) << 31) - 1) return TM_ERR_TOO_LARGE;
+    r.in = in;
+    r.ndim = ndim;
+    r.batch = uint64_t(batch);
+    return TM_OK;
+}
+
+int run(Request &r) {
+    const int nd = r.ndim;
+    uint64_t vox = 1;
+    for (int a = 0; a < nd; ++a) vox *= r.shape[a];
+    const uint64_t total = r.batch * vox;
+
+    // Buffers must not overlap.
+    const uint64_t nin = total, nf = 4 * total, ni = 4 * total * uint64_t(nd);
+    if (overlaps(r.in, nin, r.dist, nf) || overlaps(r.in, nin, r.sq, nf) ||
+        overlaps(r.in, nin, r.idx, ni) || overlaps(r.dist, nf, r.sq, nf) ||
+        overlaps(r.dist, nf, r.idx, ni) || overlaps(r.sq, nf, r.idx, ni))
+        return TM_ERR_ALIAS;
+
+    const bool index_path = r.idx != nullptr;
+
+    // Plan and check every strided pass before launching anything.
+    struct FhPlan {
+        uint32_t lpw;
+        bool pack;
+        int acc;  // 0 int32, 1 int64, 2 double
+        size_t lds;
+    } fh[kMaxDim] = {};
+    for (int a = nd - 2; a >= 0; --a) {
+        const uint32_t n = r.shape[a];
+        uint64_t fmax = 0;
+        for (int b = a + 1; b < nd; ++b) fmax += uint64_t(r.shape[b] - 1) * (r.shape[b] - 1);
+        FhPlan &p = fh[a];
+        p.acc = r.unit ? (int32_safe(fmax, n) ? 0 : 1) : 2;
+        uint32_t eb;
+        if (index_path) {
+            p.pack = false;
+            eb = 4;
+        } else {
+            int vbits = bits_for(n - 1);
+            if (vbits < 1) vbits = 1;
+            p.pack = r.unit && vbits + bits_for(fmax) <= 32;
+            eb = p.pack ? 4 : 8;
+        }
+        p.lpw = lanes_for(n, eb);
+        if (p.lpw == 0) return TM_ERR_UNSUPPORTED;
+        const uint64_t lines = total / n;
+        if ((lines + p.lpw - 1) / p.lpw >= (uint64_t(1) << 31)) return TM_ERR_UNSUPPORTED;
+        p.lds = size_t(n) * p.lpw * eb;
+    }
+    const uint32_t nlast = r.shape[nd - 1];
+    if (nlast > uint32_t(kSpan) &&
+        (uint64_t(nlast + kSpan - 1) / kSpan + 1) * 4 > kLdsBytes)
+        return TM_ERR_UNSUPPORTED;
+
+    int rc;
+    // ---- pass over the last axis: nearest zero in each contiguous line ----
+    {
+        ScanArgs s{};
+        s.in = r.in;
+        s.n = nlast;
+        s.lines = uint32_t(total / nlast);
+        s.lps = uint32_t(vox / nlast);
+        s.div_n = Div32::make(nlast);
+        s.div_lps = Div32::make(s.lps);
+        s.vox = uint32_t(vox);
+        s.ndim = nd;
+        s.w = r.w[nd - 1];
+        int mode;
+        void *out;
+        if (nd == 1) {
+            mode = kScanFinal;
+            s.dist = r.dist;
+            s.sq = r.sq;
+            s.idx = r.idx;
+            out = nullptr;
+        } else if (index_path) {
+            mode = kScanIndex;
+            s.idx = r.idx;
+            out = r.idx;
+        } else if (r.unit) {
+            mode = kScanFieldInt;
+            s.field_i = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
+            out = s.field_i;
+        } else {
+            mode = kScanFieldFlt;
+            s.field_f = r.dist;
+            out = r.dist;
+        }
+        if (nlast <= uint32_t(kSpan)) {
+            s.span_lines = uint32_t(kSpan) / nlast;
+            const uint64_t waves = (uint64_t(s.lines) + s.span_lines - 1) / s.span_lines;
+            const dim3 grid(uint32_t((waves + 3) / 4)), block(256);
+            const bool vec = mode != kScanFinal && nlast % 4 == 0 && kSpan % nlast == 0 &&
+                             uintptr_t(r.in) % 4 == 0 && uintptr_t(out) % 16 == 0;
+            switch (mode * 2 + (vec ? 1 : 0)) {
+                case kScanFieldInt * 2: rc = launch("scan_span", k_scan_span<kScanFieldInt, false>, grid, block, 0, r.stream, s); break;
+                case kScanFieldInt * 2 + 1: rc = launch("scan_span", k_scan_span<kScanFieldInt, true>, grid, block, 0, r.stream, s); break;
+                case kScanFieldFlt * 2: rc = launch("scan_span", k_scan_span<kScanFieldFlt, false>, grid, block, 0, r.stream, s); break;
+                case kScanFieldFlt * 2 + 1: rc = launch("scan_span", k_scan_span<kScanFieldFlt, true>, grid, block, 0, r.stream, s); break;
+                case kScanIndex * 2: rc = launch("scan_span", k_scan_span<kScanIndex, false>, grid, block, 0, r.stream, s); break;
+                case kScanIndex * 2 + 1: rc = launch("scan_span", k_scan_span<kScanIndex, true>, grid, block, 0, r.stream, s); break;
+                default: rc = launch("scan_span", k_scan_span<kScanFinal, false>, grid, block, 0, r.stream, s); break;
+            }
+        } else {
+            s.span_lines = 1;
+            const dim3 grid(s.lines), block(kWave);
+            const size_t lds = size_t(nlast / kSpan + 2) * 4;
+            switch (mode) {
+                case kScanFieldInt: rc = launch("scan_long", k_scan_long<kScanFieldInt>, grid, block, lds, r.stream, s); break;
+                case kScanFieldFlt: rc = launch("scan_long", k_scan_long<kScanFieldFlt>, grid, block, lds, r.stream, s); break;
+                case kScanIndex: rc = launch("scan_long", k_scan_long<kScanIndex>, grid, block, lds, r.stream, s); break;
+                default: rc = launch("scan_long", k_scan_long<kScanFinal>, grid, block, lds, r.stream, s); break;
+            }
+        }
+        if (rc != TM_OK) return rc;
+    }
+
+    // ---- strided lower-envelope passes, axis nd-2 down to 0 ----------------
+    for (int a = nd - 2; a >= 0; --a) {
+        const FhPlan &p = fh[a];
+        const uint32_t n = r.shape[a];
+        uint64_t inner = 1;
+        for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
+        const uint64_t lines = total / n;
+        const dim3 grid(uint32_t((lines + p.lpw - 1) / p.lpw)), block(kWave);
+        const bool fin = a == 0;
+        if (!index_path) {
+            FieldArgs f{};
+            f.buf = r.dist ? static_cast<void *>(r.dist) : static_cast<void *>(r.sq);
+            f.lines = lines;
+            f.n = n;
+            f.inner = uint32_t(inner);
+            f.lpw = p.lpw;
+            int vbits = bits_for(n - 1);
+            f.vbits = uint32_t(vbits < 1 ? 1 : vbits);
+            f.w = r.w[a];
+            f.dist = r.dist;
+            f.sq = r.sq;
+            f.ndim = nd;
+            for (int b = 0; b < nd; ++b) {
+                f.shape[b] = r.shape[b];
+                f.wall[b] = r.w[b];
+            }
+            const char *nm = fin ? "fh_field_final" : "fh_field";
+#define TM_FIELD(A, PK, FN) launch(nm, k_fh_field<A, PK, FN>, grid, block, p.lds, r.stream, f)
+            if (p.acc == 2) rc = fin ? TM_FIELD(double, false, true) : TM_FIELD(double, false, false);
+            else if (p.acc == 0 && p.pack) rc = fin ? TM_FIELD(int32_t, true, true) : TM_FIELD(int32_t, true, false);
+            else if (p.acc == 0) rc = fin ? TM_FIELD(int32_t, false, true) : TM_FIELD(int32_t, false, false);
+            else if (p.pack) rc = fin ? TM_FIELD(int64_t, true, true) : TM_FIELD(int64_t, true, false);
+            else rc = fin ? TM_FIELD(int64_t, false, true) : TM_FIELD(int64_t, false, false);
+#undef TM_FIELD
+        } else {
+            IndexArgs x{};
+            x.idx = r.idx;
+            x.lines = lines;
+            x.lps = uint32_t(vox / n);
+            x.n = n;
+            x.inner = uint32_t(inner);
+            x.lpw = p.lpw;
+            x.vox = uint32_t(vox);
+            x.ndim = nd;
+            x.axis = a;
+            x.div_inner = Div32::make(uint32_t(inner));
+            for (int b = 0; b < nd; ++b) {
+                x.div_shape[b] = Div32::make(r.shape[b]);
+                x.wall[b] = r.w[b];
+            }
+            x.dist = fin ? r.dist : nullptr;
+            x.sq = fin ? r.sq : nullptr;
+            const char *nm = fin ? "fh_index_final" : "fh_index";
+#define TM_INDEX(A, FN) launch(nm, k_fh_index<A, FN>, grid, block, p.lds, r.stream, x)
+            if (p.acc == 2) rc = fin ? TM_INDEX(double, true) : TM_INDEX(double, false);
+            else if (p.acc == 0) rc = fin ? TM_INDEX(int32_t, true) : TM_INDEX(int32_t, false);
+            else rc = fin ? TM_INDEX(int64_t, true) : TM_INDEX(int64_t, false);
+#undef TM_INDEX
+        }
+        if (rc != TM_OK) return rc;
+    }
+    return TM_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C-ABI
+// ---------------------------------------------------------------------------
+extern "C" int tm_edt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
+                      const double *sampling, float *out_dist, int32_t *out_idx,
+                      hipStream_t stream) {
+    Request r{};
+    int rc = validate(in_u8, ndim, shape, batch, sampling, out_dist, out_idx, nullptr, r);
+    if (rc != TM_OK) return rc;
+    r.dist = out_dist;
+    r.sq = nullptr;
+    r.idx = out_idx;
+    r.stream = stream;
+    return run(r);
+}
+
+extern "C" int tm_edt_sq(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
+                         int32_t *out_sq, int32_t *out_idx, hipStream_t stream) {
+    Request r{};
+    int rc = validate(in_u8, ndim, shape, batch, nullptr, out_sq, out_idx, nullptr, r);
+    if (rc != TM_OK) return rc;
+    r.dist = nullptr;
+    r.sq = out_sq;
+    r.idx = out_idx;
+    r.stream = stream;
+    return run(r);
+}
+
+extern "C" const char *tm_strerror(int status) {
+    switch (status) {
+        case TM_OK: return "success";
+        case TM_ERR_NDIM: return "spatial rank must be between 1 and 8";
+        case TM_ERR_SHAPE: return "shape is missing or has an extent below 1";
+        case TM_ERR_BATCH: return "batch must be at least 1";
+        case TM_ERR_NULL: return "input pointer is null";
+        case TM_ERR_NO_OUTPUT: return "at least one output must be requested";
+        case TM_ERR_SAMPLING: return "sampling entries must be finite and positive";
+        case TM_ERR_TOO_LARGE: return "input too large for 32-bit indices or int32 squared distances";
+        case TM_ERR_ALIAS: return "input and output buffers overlap";
+        case TM_ERR_UNSUPPORTED: return "a line is longer than the envelope stack held in LDS";
+        case TM_ERR_HIP: return "HIP runtime error while enqueuing kernels";
+        default: return "unknown status";
+    }
+}
+
+extern "C" int tm_prof_enable(int max_kernels) {
+    Prof &p = prof();
+    std::lock_guard<std::mutex> g(p.mu);
+    for (size_t k = 0; k < p.start.size(); ++k) {
+        (void)hipEventDestroy(p.start[k]);
+        (void)hipEventDestroy(p.stop[k]);
+    }
+    p.start.clear();
+    p.stop.clear();
+    p.names.clear();
+    p.cap = 0;
+    p.next = 0;
+    if (max_kernels <= 0) return TM_OK;
+    p.start.resize(max_kernels);
+    p.stop.resize(max_kernels);
+    p.names.assign(max_kernels, nullptr);
+    for (int k = 0; k < max_kernels; ++k) {
+        if (hipEventCreate(&p.start[k]) != hipSuccess || hipEventCreate(&p.stop[k]) != hipSuccess) {
+            p.start.resize(k);
+            p.stop.resize(k);
+            return TM_ERR_HIP;
+        }
+    }
+    p.cap = max_kernels;
+    return TM_OK;
+}
+
+extern "C" int tm_prof_count(void) {
+    Prof &p = prof();
+    int c = p.next.load();
+    return c < p.cap ? c : p.cap;
+}
+
+extern "C" int tm_prof_read(int i, const char **name, float *ms) {
+    Prof &p = prof();
+    if (i < 0 || i >= tm_prof_count()) return TM_ERR_SHAPE;
+    if (name) *name = p.names[i];
+    if (ms && hipEventElapsedTime(ms, p.start[i], p.stop[i]) != hipSuccess) return TM_ERR_HIP;
+    return TM_OK;
+}
+
+extern "C" int tm_selftest_host(void) {
+    int bad = 0;
+    const uint32_t divs[] = {1u, 2u, 3u, 5u, 7u, 64u, 100u, 127u, 128u, 255u, 256u, 1000u,
+                             4096u, 65535u, 65536u, 1u << 20, 16777215u, 2147483647u,
+                             2147483648u, 4294967295u};
+    uint64_t state = 0x9e3779b97f4a7c15ull;
+    for (uint32_t d : divs) {
+        Div32 q = Div32::make(d);
+        for (int t = 0; t < 20000; ++t) {
+            state = state * 6364136223846793005ull + 1442695040888963407ull;
+            uint32_t x = uint32_t(state >> 32);
+            if (t < 8) x = (t < 4) ? uint32_t(t) : 0xffffffffu - uint32_t(t - 4);
+            if (t == 8) x = d;
+            if (t == 9) x = d - 1;
+            if (q.div(x) != x / d) ++bad;
+        }
+    }
+    return bad ? -bad : TM_OK;
+}

@@ -1,0 +1,295 @@
+// edt_scan.h -- first pass of the separable EDT, along the contiguous last
+// axis (paper, Section 2.3.2: one 1-D pass per axis; this one starts from a
+// binary mask, so the lower envelope degenerates to "nearest zero in the
+// line").
+//
+// Each wavefront owns a span of up to 1024 consecutive mask bytes.  Lane l
+// holds the 16 positions 256k + 4l + j (k, j < 4), so every load instruction
+// of the wave reads 256 contiguous bytes and every store writes 1 KiB
+// contiguous.  The nearest zero on each side comes from per-lane 4-bit zero
+// masks, a wave-wide inclusive prefix-max (last zero so far) and suffix-min
+// (first zero from here), and carries across the four groups.  Ties between
+// an equally distant left and right zero go to the left (smaller) one.
+#pragma once
+
+#include "edt_common.h"
+
+namespace tmedt {
+
+enum ScanMode : int {
+    kScanFieldInt = 0,   // int32 squared distance, kInfI if the line has no zero
+    kScanFieldFlt = 1,   // float w * squared distance, +inf if none
+    kScanIndex = 2,      // int32 in-sample flat index of the zero, -1 if none
+    kScanFinal = 3       // rank-1 input: the line is the sample; final outputs
+};
+
+struct ScanArgs {
+    const uint8_t *in;
+    uint32_t n;            // line length
+    uint32_t lines;        // lines in the batch (batch * voxels / n)
+    uint32_t span_lines;   // whole lines per wavefront span (n <= 1024)
+    uint32_t lps;          // lines per sample
+    Div32 div_n;           // span-relative position -> line
+    Div32 div_lps;         // line -> sample
+    uint32_t vox;          // elements per sample
+    int32_t ndim;
+    double w;              // squared sampling of the last axis
+    int32_t *field_i;      // kScanFieldInt output (batch-flat)
+    float *field_f;        // kScanFieldFlt output (batch-flat)
+    int32_t *idx;          // kScanIndex: [batch][ndim][vox] (slice 0 written); kScanFinal: coords
+    float *dist;           // kScanFinal outputs (each may be null)
+    int32_t *sq;
+};
+
+constexpr int kBig = 0x3fffffff;
+
+// Left/right zero candidates for the 16 positions a lane holds in one 1024-
+// position chunk.  zb[k] bit j marks a zero at chunk position 256k + 4l + j.
+// cl / cr: last zero before / first zero after the chunk (chunk-relative,
+// -kBig / kBig when none).  Outputs chunk-relative candidates (-kBig / kBig
+// when none).
+__device__ inline void chunk_candidates(const uint32_t zb[4], int cl, int cr, int lane,
+                                        int left[4][4], int right[4][4]) {
+    int pl[4], sf[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        int base = 256 * k + 4 * lane;
+        pl[k] = zb[k] ? base + 31 - __clz(zb[k]) : -kBig;
+        sf[k] = zb[k] ? base + __ffs(zb[k]) - 1 : kBig;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+#pragma unroll
+        for (int d = 1; d < kWave; d <<= 1) {
+            int t = __shfl_up(pl[k], d, kWave);
+            if (lane >= d) pl[k] = max(pl[k], t);
+            int u = __shfl_down(sf[k], d, kWave);
+            if (lane + d < kWave) sf[k] = min(sf[k], u);
+        }
+    }
+    int exl[4], exr[4];
+    int carry = cl;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        int t = __shfl_up(pl[k], 1, kWave);
+        exl[k] = max(lane == 0 ? -kBig : t, carry);
+        carry = max(carry, __shfl(pl[k], kWave - 1, kWave));
+    }
+    carry = cr;
+#pragma unroll
+    for (int k = 3; k >= 0; --k) {
+        int t = __shfl_down(sf[k], 1, kWave);
+        exr[k] = min(lane == kWave - 1 ? kBig : t, carry);
+        carry = min(carry, __shfl(sf[k], 0, kWave));
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        int base = 256 * k + 4 * lane;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            uint32_t lo = zb[k] & ((2u << j) - 1u);
+            left[k][j] = lo ? base + 31 - __clz(lo) : exl[k];
+            uint32_t hi = zb[k] >> j;
+            right[k][j] = hi ? base + j + __ffs(hi) - 1 : exr[k];
+        }
+    }
+}
+
+// Zero masks of one chunk: positions >= valid read as foreground.
+template <bool VEC>
+__device__ inline void load_zero_bits(const uint8_t *p, int valid, int lane, uint32_t zb[4]) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        int base = 256 * k + 4 * lane;
+        uint32_t bits = 0;
+        if (VEC) {
+            uint32_t word = *reinterpret_cast<const uint32_t *>(p + base);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) bits |= ((word >> (8 * j)) & 0xffu) == 0 ? (1u << j) : 0u;
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (base + j < valid && p[base + j] == 0) bits |= 1u << j;
+        }
+        zb[k] = bits;
+    }
+}
+
+// Writes the results of four consecutive positions (x0 .. x0+3 of one line,
+// line-relative; y[j] = line-relative zero or -1) for line `gline`.
+template <int MODE, bool VEC>
+__device__ inline void scan_store4(const ScanArgs &a, uint32_t gline, int x0, const int y[4],
+                                   int count) {
+    const uint64_t lbase = uint64_t(gline) * a.n;  // batch-flat start of the line
+    if (MODE == kScanFieldInt) {
+        int32_t v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            int d = x0 + j - y[j];
+            v[j] = y[j] >= 0 ? d * d : kInfI;
+        }
+        int32_t *o = a.field_i + lbase + x0;
+        if (VEC) {
+            *reinterpret_cast<int4 *>(o) = make_int4(v[0], v[1], v[2], v[3]);
+        } else {
+            for (int j = 0; j < count; ++j) o[j] = v[j];
+        }
+    } else if (MODE == kScanFieldFlt) {
+        float v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            double d = double(x0 + j - y[j]);
+            v[j] = y[j] >= 0 ? float(a.w * (d * d)) : __builtin_inff();
+        }
+        float *o = a.field_f + lbase + x0;
+        if (VEC) {
+            *reinterpret_cast<float4 *>(o) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+            for (int j = 0; j < count; ++j) o[j] = v[j];
+        }
+    } else if (MODE == kScanIndex) {
+        uint32_t s = a.div_lps.div(gline);
+        uint32_t lline = gline - s * a.lps;
+        uint64_t local = uint64_t(lline) * a.n;
+        int32_t v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = y[j] >= 0 ? int32_t(local + y[j]) : kNoIdx;
+        int32_t *o = a.idx + uint64_t(s) * a.ndim * a.vox + local + x0;
+        if (VEC) {
+            *reinterpret_cast<int4 *>(o) = make_int4(v[0], v[1], v[2], v[3]);
+        } else {
+            for (int j = 0; j < count; ++j) o[j] = v[j];
+        }
+    } else {  // kScanFinal: rank 1, the line is the whole sample
+        for (int j = 0; j < count; ++j) {
+            int x = x0 + j;
+            double d = y[j] >= 0 ? double(x - y[j]) : double(x + 1);  // virtual zero at -1
+            if (a.dist) a.dist[lbase + x] = float(sqrt(a.w * (d * d)));
+            if (a.sq) {
+                int64_t di = y[j] >= 0 ? int64_t(x - y[j]) : int64_t(x + 1);
+                a.sq[lbase + x] = int32_t(di * di);
+            }
+            if (a.idx) a.idx[lbase + x] = y[j] >= 0 ? y[j] : -1;
+        }
+    }
+}
+
+// Lines of length n <= 1024: each wavefront scans `span_lines` whole lines.
+template <int MODE, bool VEC>
+__global__ void __launch_bounds__(256) k_scan_span(ScanArgs a) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const uint32_t wave = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    const uint64_t line0 = uint64_t(wave) * a.span_lines;
+    if (line0 >= a.lines) return;  // whole wavefront exits together
+    const uint32_t nl = uint32_t(min<uint64_t>(a.span_lines, a.lines - line0));
+    const int valid = int(nl * a.n);
+    const uint8_t *src = a.in + line0 * a.n;
+    const bool full = VEC && valid == kSpan;
+
+    uint32_t zb[4];
+    if (full) load_zero_bits<true>(src, valid, lane, zb);
+    else load_zero_bits<false>(src, valid, lane, zb);
+    int left[4][4], right[4][4];
+    chunk_candidates(zb, -kBig, kBig, lane, left, right);
+
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int p0 = 256 * k + 4 * lane;  // span position of the group's first element
+        if (p0 >= valid) continue;
+        // With n % 4 == 0 (vector path) the four positions share one line.
+        int y[4];
+        uint32_t line_of[4];
+        int xs[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            int p = p0 + j;
+            uint32_t l = a.div_n.div(uint32_t(p));
+            int ls = int(l * a.n);
+            int le = ls + int(a.n);
+            bool hl = left[k][j] >= ls;
+            bool hr = right[k][j] < le && right[k][j] < valid;
+            int yy = -1;
+            if (hl && (!hr || p - left[k][j] <= right[k][j] - p)) yy = left[k][j] - ls;
+            else if (hr) yy = right[k][j] - ls;
+            y[j] = yy;
+            line_of[j] = l;
+            xs[j] = p - ls;
+        }
+        if (full) {
+            scan_store4<MODE, true>(a, uint32_t(line0) + line_of[0], xs[0], y, 4);
+        } else {
+            for (int j = 0; j < 4; ++j) {
+                if (p0 + j >= valid) break;
+                int yy[4] = {y[j], -1, -1, -1};
+                scan_store4<MODE, false>(a, uint32_t(line0) + line_of[j], xs[j], yy, 1);
+            }
+        }
+    }
+}
+
+// Lines longer than 1024: one wavefront per line, two sweeps over 1024-
+// position chunks.  The first (right to left) stores, per chunk, the first
+// zero at or after the chunk start in LDS; the second (left to right) carries
+// the last zero seen and reads the right carry from LDS.
+template <int MODE>
+__global__ void __launch_bounds__(64) k_scan_long(ScanArgs a) {
+    extern __shared__ int first_from[];  // [chunks + 1]
+    const int lane = threadIdx.x;
+    const uint32_t gline = blockIdx.x;
+    const uint8_t *src = a.in + uint64_t(gline) * a.n;
+    const int n = int(a.n);
+    const int chunks = (n + kSpan - 1) / kSpan;
+    if (lane == 0) first_from[chunks] = kBig;
+    int carry = kBig;
+    for (int c = chunks - 1; c >= 0; --c) {
+        const int valid = min(kSpan, n - c * kSpan);
+        uint32_t zb[4];
+        load_zero_bits<false>(src + c * kSpan, valid, lane, zb);
+        int m = kBig;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (zb[k]) m = min(m, c * kSpan + 256 * k + 4 * lane + __ffs(zb[k]) - 1);
+#pragma unroll
+        for (int d = 32; d >= 1; d >>= 1) m = min(m, __shfl_xor(m, d, kWave));
+        carry = min(carry, m);
+        if (lane == 0) first_from[c] = carry;
+    }
+    __syncthreads();
+    int last = -kBig;  // last zero before the current chunk (line-relative)
+    for (int c = 0; c < chunks; ++c) {
+        const int valid = min(kSpan, n - c * kSpan);
+        const int off = c * kSpan;
+        uint32_t zb[4];
+        load_zero_bits<false>(src + off, valid, lane, zb);
+        const int cl = last == -kBig ? -kBig : last - off;
+        const int nxt = first_from[c + 1];
+        const int cr = nxt == kBig ? kBig : nxt - off;
+        int left[4][4], right[4][4];
+        chunk_candidates(zb, cl, cr, lane, left, right);
+        int m = -kBig;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (zb[k]) m = max(m, off + 256 * k + 4 * lane + 31 - __clz(zb[k]));
+#pragma unroll
+        for (int d = 32; d >= 1; d >>= 1) m = max(m, __shfl_xor(m, d, kWave));
+        last = max(last, m);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int p0 = 256 * k + 4 * lane;
+            for (int j = 0; j < 4; ++j) {
+                const int p = p0 + j;
+                if (p >= valid) break;
+                const int l = left[k][j], r = right[k][j];
+                const bool hl = l > -kBig;
+                const bool hr = r < kBig;
+                int yy = -1;
+                if (hl && (!hr || p - l <= r - p)) yy = l + off;
+                else if (hr) yy = r + off;
+                int ys[4] = {yy, -1, -1, -1};
+                scan_store4<MODE, false>(a, gline, p + off, ys, 1);
+            }
+        }
+    }
+}
+
+}  // namespace tmedt

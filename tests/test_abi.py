@@ -1,0 +1,123 @@
+"""The C-ABI library: exported symbols, host-side checks and argument
+validation.  Every call here is rejected on the host before any HIP call, so
+these run without a GPU."""
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+from paper_2608_24738_amd import binding, build as hip_build
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+TM_OK, TM_ERR_NDIM, TM_ERR_SHAPE, TM_ERR_BATCH, TM_ERR_NULL = 0, -1, -2, -3, -4
+TM_ERR_NO_OUTPUT, TM_ERR_SAMPLING, TM_ERR_TOO_LARGE, TM_ERR_ALIAS = -5, -6, -7, -8
+TM_ERR_UNSUPPORTED, TM_ERR_HIP = -9, -10
+
+FAKE_IN = 0x100000           # never dereferenced: every call below fails validation
+FAKE_OUT = 0x40000000
+FAKE_IDX = 0x80000000
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if hip_build.is_stale():
+        hip_build.build()
+    return binding.load()
+
+
+def declared_functions():
+    names = []
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        names += re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(tm_\w+)\s*\(", text, re.M)
+    return sorted(set(names))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert {"tm_edt", "tm_edt_sq", "tm_strerror"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_host_division_constants(lib):
+    assert lib.tm_selftest_host() == 0
+
+
+def test_strerror_covers_every_status(lib):
+    for s in range(0, -11, -1):
+        msg = binding.tm_strerror(s)
+        assert msg and msg != "unknown status", s
+    assert binding.tm_strerror(-99) == "unknown status"
+
+
+def call_edt(lib, shape, batch=1, sampling=None, inp=FAKE_IN, dist=FAKE_OUT, idx=None, ndim=None):
+    nd = len(shape) if ndim is None else ndim
+    sh = (ctypes.c_int64 * max(len(shape), 1))(*shape) if shape is not None else None
+    samp = (ctypes.c_double * len(sampling))(*sampling) if sampling is not None else None
+    return lib.tm_edt(inp and ctypes.c_void_p(inp), nd, sh, batch, samp,
+                      dist and ctypes.c_void_p(dist), idx and ctypes.c_void_p(idx), None)
+
+
+def call_sq(lib, shape, batch=1, inp=FAKE_IN, sq=FAKE_OUT, idx=None):
+    sh = (ctypes.c_int64 * len(shape))(*shape)
+    return lib.tm_edt_sq(ctypes.c_void_p(inp), len(shape), sh, batch,
+                         sq and ctypes.c_void_p(sq), idx and ctypes.c_void_p(idx), None)
+
+
+def test_rank_limits(lib):
+    assert call_edt(lib, [4] * 9) == TM_ERR_NDIM
+    assert call_edt(lib, [4], ndim=0) == TM_ERR_NDIM
+
+
+def test_shape_and_batch(lib):
+    assert call_edt(lib, None, ndim=2) == TM_ERR_SHAPE
+    assert call_edt(lib, [4, 0]) == TM_ERR_SHAPE
+    assert call_edt(lib, [4, -3]) == TM_ERR_SHAPE
+    assert call_edt(lib, [4, 4], batch=0) == TM_ERR_BATCH
+
+
+def test_null_input_and_no_output(lib):
+    assert call_edt(lib, [4, 4], inp=0) == TM_ERR_NULL
+    assert call_edt(lib, [4, 4], dist=0, idx=0) == TM_ERR_NO_OUTPUT
+    assert call_sq(lib, [4, 4], sq=0, idx=0) == TM_ERR_NO_OUTPUT
+
+
+@pytest.mark.parametrize("bad", [0.0, -1.0, float("inf"), float("nan")])
+def test_sampling_must_be_positive_and_finite(lib, bad):
+    assert call_edt(lib, [4, 4], sampling=[1.0, bad]) == TM_ERR_SAMPLING
+
+
+def test_too_large(lib):
+    assert call_edt(lib, [1 << 16, 1 << 15]) == TM_ERR_TOO_LARGE          # 2^31 per sample
+    assert call_edt(lib, [1 << 10, 1 << 10], batch=1 << 12) == TM_ERR_TOO_LARGE  # 2^32 total
+    assert call_sq(lib, [50000, 2]) == TM_ERR_TOO_LARGE                    # sum of n^2 >= 2^31
+
+
+def test_overlapping_buffers(lib):
+    assert call_edt(lib, [16, 16], dist=FAKE_IN + 100) == TM_ERR_ALIAS
+    assert call_edt(lib, [16, 16], dist=FAKE_OUT, idx=FAKE_OUT + 4) == TM_ERR_ALIAS
+    assert call_sq(lib, [16, 16], sq=FAKE_OUT, idx=FAKE_OUT + 512) == TM_ERR_ALIAS
+
+
+def test_unsupported_long_strided_line(lib):
+    # 60000-long lines along axis 0 with float stacks exceed the LDS budget
+    assert call_edt(lib, [60000, 2], sampling=[1.5, 1.0]) == TM_ERR_UNSUPPORTED
+
+
+def test_binding_rejects_bad_python_arguments():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros((1, 1, 4, 4), dtype=torch.uint8)
+    with pytest.raises(ValueError):
+        binding.tm_edt(x, 2, out_dist=torch.empty(16))                    # not a GPU tensor
+    with pytest.raises(RuntimeError):
+        binding.distance_transform_edt(x, return_distances=False, return_indices=False)
+    with pytest.raises(RuntimeError):
+        binding.distance_transform_edt(x, sampling=[1.0, 2.0, 3.0])
+    with pytest.raises(TypeError):
+        binding.distance_transform_edt(x.float())
+    with pytest.raises(ValueError):
+        binding.distance_transform_edt(torch.zeros((4, 4), dtype=torch.uint8))

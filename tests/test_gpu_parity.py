@@ -1,0 +1,177 @@
+"""GPU parity: the HIP library against the CPU oracle, element by element.
+
+Unit sampling: int32 squared distances and float distances bit-exact, indices
+equal to the canonical ones.  Sampled: distances within 1e-5 relative or
+1e-6 absolute, indices checked to be nearest background elements.
+"""
+import numpy as np
+import pytest
+
+from gpu_util import announce, check_against_oracle, run_gpu
+from oracle import edt_oracle
+from paper_2608_24738_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+NTHREADS = 16
+
+
+def oracle(mask, ndim, sampling=None):
+    return edt_oracle.edt(mask, ndim, sampling, nthreads=NTHREADS)
+
+
+def parity(mask, ndim, sampling=None, dist=True, idx=False, sq=None, tag=""):
+    unit = sampling is None
+    if sq is None:
+        sq = unit
+    announce("%s shape=%s ndim=%d sampling=%s dist=%s idx=%s sq=%s"
+             % (tag, mask.shape, ndim, sampling, dist, idx, sq))
+    res = run_gpu(mask, ndim, sampling, dist=dist, idx=idx, sq=sq)
+    ora = oracle(mask, ndim, sampling)
+    check_against_oracle(mask, ndim, sampling, res, ora)
+    return res, ora
+
+
+# ---- the five workloads at smaller sizes (several tiles, ragged tails) -------
+TWINS = [
+    (1, (64, 64), 1, True),
+    (2, (100, 72), 3, False),        # last axis 72 does not divide the 1024-byte span
+    (2, (128, 256), 2, False),
+    (3, (40, 37, 64), 3, False),
+    (3, (33, 48, 96), 2, True),
+    (4, (30, 33, 64), 2, True),
+    (4, (17, 40, 52), 1, False),
+    (5, (5, 9, 10, 64), 2, False),
+    (5, (3, 7, 11, 13), 3, True),
+]
+
+
+@pytest.mark.parametrize("key,spatial,batch,want_idx", TWINS,
+                         ids=["cfg%d-%s-b%d%s" % (k, "x".join(map(str, s)), b, "-idx" if i else "")
+                              for k, s, b, i in TWINS])
+def test_workload_twins(key, spatial, batch, want_idx):
+    w = workloads.WORKLOADS[key]
+    mask = workloads.make_mask(key, spatial, batch)
+    samp = w.sampling
+    parity(mask, len(spatial), samp, dist=True, idx=want_idx, tag="twin cfg%d" % key)
+    if want_idx:
+        # indices alone (no distance output) take the same path
+        parity(mask, len(spatial), samp, dist=False, idx=True, sq=False, tag="idx-only cfg%d" % key)
+
+
+# ---- the five workloads at full size, in the configuration the bench times ---
+FULL = [(1, True), (2, False), (3, False), (4, True), (5, False)]
+
+
+@pytest.mark.parametrize("key,want_idx", FULL, ids=["cfg%d" % k for k, _ in FULL])
+def test_workload_full_size(key, want_idx):
+    w = workloads.WORKLOADS[key]
+    mask = workloads.make_mask(key)
+    parity(mask, w.ndim, w.sampling, dist=True, idx=want_idx, tag="full cfg%d" % key)
+
+
+# ---- edge cases -------------------------------------------------------------
+def rand_mask(shape, p_bg, seed):
+    rng = np.random.default_rng(seed)
+    return (rng.random(shape) >= p_bg).astype(np.uint8)
+
+
+@pytest.mark.parametrize("ndim", [1, 2, 3, 4, 5, 6, 7, 8])
+def test_every_rank(ndim):
+    rng = np.random.default_rng(100 + ndim)
+    spatial = tuple(int(rng.integers(1, 6 if ndim > 4 else 12)) for _ in range(ndim))
+    mask = rand_mask((3,) + spatial, 0.15, ndim)
+    parity(mask, ndim, None, dist=True, idx=True, tag="rank")
+    parity(mask, ndim, [1.5] * ndim, dist=True, idx=True, tag="rank sampled")
+    parity(mask, ndim, [0.5 + 0.25 * a for a in range(ndim)], dist=True, idx=False, tag="rank sampled")
+
+
+@pytest.mark.parametrize("case", ["all_background", "all_foreground", "single_zero", "unit_extent"])
+def test_degenerate_inputs(case):
+    shape = (2, 9, 17, 33)
+    if case == "all_background":
+        mask = np.zeros(shape, np.uint8)
+    elif case == "all_foreground":
+        mask = np.ones(shape, np.uint8)
+    elif case == "single_zero":
+        mask = np.ones(shape, np.uint8)
+        mask[0, 4, 3, 30] = 0
+        mask[1, 8, 16, 0] = 0
+    else:
+        shape = (4, 1, 7, 1)
+        mask = rand_mask(shape, 0.3, 9)
+    parity(mask, 3, None, dist=True, idx=True, tag=case)
+    parity(mask, 3, (2.5, 0.8, 0.8), dist=True, idx=True, tag=case + " sampled")
+    parity(mask, 3, (2.5, 0.8, 0.8), dist=True, idx=False, tag=case + " sampled")
+
+
+def test_mixed_batch_with_and_without_background():
+    mask = rand_mask((5, 21, 30), 0.02, 3)
+    mask[1] = 1
+    mask[3] = 1
+    parity(mask, 2, None, dist=True, idx=True, tag="mixed batch")
+    parity(mask, 2, (0.7, 1.3), dist=True, idx=True, tag="mixed batch sampled")
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 63, 65, 1000, 1024, 1025, 3000])
+def test_scan_line_lengths(n):
+    """Rank-1 lines and 2-D last axes of every scan variant (span, generic, long)."""
+    mask = rand_mask((3, n), 0.05, n)
+    parity(mask, 1, None, dist=True, idx=True, tag="1-D n=%d" % n)
+    parity(mask, 1, (1.7,), dist=True, idx=True, tag="1-D sampled n=%d" % n)
+    m2 = rand_mask((2, 3, n), 0.02, n + 1)
+    parity(m2, 2, None, dist=True, idx=True, tag="2-D n=%d" % n)
+    parity(m2, 2, None, dist=True, idx=False, tag="2-D n=%d" % n)
+
+
+@pytest.mark.parametrize("n", [700, 1500, 3000])
+def test_long_strided_lines(n):
+    """Strided lines long enough that fewer than 64 lanes share a workgroup's LDS,
+    and (n = 3000) products that need the int64 comparison path."""
+    mask = rand_mask((n, 40), 0.003, n)
+    parity(mask[None], 2, None, dist=True, idx=True, tag="long strided n=%d" % n)
+    parity(mask[None], 2, None, dist=True, idx=False, tag="long strided n=%d" % n)
+    parity(mask[None], 2, (1.25, 0.5), dist=True, idx=False, tag="long strided sampled n=%d" % n)
+
+
+def test_sparse_long_envelopes():
+    """Few background seeds in a 4-D volume: most first-pass lines are empty."""
+    mask = np.ones((2, 12, 20, 24, 28), np.uint8)
+    mask[0, 3, 7, 11, 13] = 0
+    mask[0, 11, 19, 0, 27] = 0
+    mask[1, 0, 0, 0, 0] = 0
+    parity(mask, 4, None, dist=True, idx=True, tag="sparse 4-D")
+    parity(mask, 4, (1.0, 2.0, 0.5, 1.5), dist=True, idx=True, tag="sparse 4-D sampled")
+
+
+def test_batch_equals_per_sample():
+    mask = workloads.make_mask(3, (24, 20, 36), 4)[:, 0]
+    announce("batch vs per-sample")
+    whole = run_gpu(mask, 3, None, dist=True, idx=True, sq=True)
+    for b in range(mask.shape[0]):
+        one = run_gpu(mask[b:b + 1], 3, None, dist=True, idx=True, sq=True)
+        for k in ("dist", "idx", "sq"):
+            assert np.array_equal(whole[k][b:b + 1], one[k]), (b, k)
+
+
+def test_deterministic():
+    mask = workloads.make_mask(4, (40, 48, 64), 2)
+    announce("determinism")
+    a = run_gpu(mask, 3, (2.5, 0.8, 0.8), dist=True, idx=True)
+    b = run_gpu(mask, 3, (2.5, 0.8, 0.8), dist=True, idx=True)
+    assert np.array_equal(a["dist"], b["dist"]) and np.array_equal(a["idx"], b["idx"])
+
+
+def test_sqrt_is_correctly_rounded():
+    """Distances are the correctly rounded float sqrt of the exact squared distance.
+    A single zero at the corner of a 1024^2 image gives every sum of two squares up
+    to 2 * 1023^2; one at the corner of a 100^3 volume gives every sum of three."""
+    for shape in [(1024, 1024), (100, 100, 100)]:
+        mask = np.ones((1,) + shape, np.uint8)
+        mask[(0,) * (len(shape) + 1)] = 0
+        announce("sqrt rounding %s" % (shape,))
+        res = run_gpu(mask, len(shape), None, dist=True, sq=True)
+        grid = np.indices(shape, dtype=np.int64)
+        d2 = sum(g * g for g in grid)
+        assert np.array_equal(res["sq"][0], d2)
+        assert np.array_equal(res["dist"][0], np.sqrt(d2.astype(np.float64)).astype(np.float32))
