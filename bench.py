@@ -1,0 +1,238 @@
+#!/usr/bin/env python3
+"""Throughput of the exact EDT on one MI355X.
+
+Default workload: 3-D EDT of 8 x 1 x 128^3 uint8 masks whose foreground is the
+union of 30 random solid balls (radius 4-30 voxels) per volume, unit
+sampling, float32 distances.  One step = one tm_edt call over the whole batch
+(the last-axis scan, the axis-1 envelope pass and the fused axis-0 pass), with
+the mask already resident in HBM and the output preallocated.
+
+Prints one JSON line: voxels/s, per-step time, the dominant kernel's
+achieved HBM bandwidth against the MI355X peak (algorithmic bytes over its
+HIP-event-timed average duration), and the CPU oracle's throughput on a
+bounded sample on this host.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E peak, GB/s
+SOURCES = ["paper_2608_24738_amd/csrc/edt_common.h", "paper_2608_24738_amd/csrc/edt_fh.h",
+           "paper_2608_24738_amd/csrc/edt_scan.h", "paper_2608_24738_amd/csrc/edt_host.hip"]
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def source_digest():
+    h = hashlib.sha256()
+    for s in SOURCES:
+        with open(os.path.join(ROOT, s), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
+    """Bytes one launch of kernel `name` must move (separable-pass model):
+    the last-axis scan reads the 1-byte mask and writes the 4-byte field,
+    every envelope pass reads and writes the 4-byte field, and the final
+    pass reads the field and writes the outputs."""
+    if name.startswith("scan"):
+        return total * (1 + 4)
+    if name == "fh_field":
+        return total * (4 + 4)
+    if name == "fh_field_final":
+        return total * (4 + out_bytes)
+    if name == "fh_index":
+        return total * (4 + 4)
+    if name == "fh_index_final":
+        return total * (4 + 4 * ndim + (out_bytes if want_idx else 0))
+    raise KeyError(name)
+
+
+def read_counters(kernel, workload_name):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
+    was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", "%s__%s.md" % (kernel, workload_name))
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    start = text.find("```json")
+    if start < 0:
+        return None
+    end = text.find("```", start + 7)
+    try:
+        data = json.loads(text[start + 7:end])
+    except ValueError:
+        return None
+    if data.get("source_digest") != source_digest():
+        return None
+    return data.get("traffic_bytes_per_launch")
+
+
+def cpu_baseline(mask_np, ndim, sampling, budget_s=10.0):
+    from oracle import edt_oracle
+    nthreads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or min(16, os.cpu_count() or 1)
+    used = edt_oracle.threads_used(nthreads)
+    batch = mask_np.shape[0]
+    vox_per = int(mask_np[0].size)
+    done_vox, reps = 0, 0
+    t0 = time.perf_counter()
+    while True:
+        edt_oracle.edt(mask_np, ndim, sampling, want_sq=False, want_dist=True, want_idx=False,
+                       nthreads=nthreads)
+        reps += 1
+        done_vox += batch * vox_per
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    # single-thread figure on one volume, for the paper's one-core comparison
+    t1 = time.perf_counter()
+    edt_oracle.edt(mask_np[:1], ndim, sampling, want_sq=False, want_dist=True, want_idx=False,
+                   nthreads=1)
+    dt1 = time.perf_counter() - t1
+    return {"value": done_vox / dt, "unit": "voxels/s", "cores": used, "kind": "oracle",
+            "sample": "%d x the whole %d-volume batch (%.1f s wall, %d OpenMP threads)"
+                      % (reps, batch, dt, used),
+            "single_thread_value": vox_per / dt1}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=3, help="workload key 1-5 (3 = headline)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="run only a plain 256 MiB device copy (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only; --gpus %d is not supported (the EDT shards "
+              "by batch with no exchange, see DESIGN.md)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_24738_amd import binding, build as hip_build, workloads
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+
+    if args.copy_calib:
+        n = 64 * 1024 * 1024                       # 256 MiB of float32 each way
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calib": True, "read_bytes": 4 * n, "write_bytes": 4 * n}))
+        return
+
+    if not os.path.exists(binding.LIB_PATH):
+        hip_build.build()
+    binding.load()
+
+    w = workloads.WORKLOADS[args.workload]
+    log("generating %s" % w.name)
+    mask_np = workloads.make_mask(args.workload)
+    ndim = w.ndim
+    total = int(mask_np.size)
+    x = torch.from_numpy(mask_np).to(dev)
+    dist = torch.empty(mask_np.shape, dtype=torch.float32, device=dev)
+    idx = None
+    if w.want_idx:
+        idx = torch.empty((w.batch, 1, ndim) + tuple(w.spatial), dtype=torch.int32, device=dev)
+    samp = list(w.sampling) if w.sampling else None
+
+    def step():
+        binding.tm_edt(x, ndim, samp, dist, idx, stream=stream)
+
+    log("warmup %d" % args.warmup)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    log("timing %d steps" % args.steps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+
+    # per-kernel durations: HIP events recorded by the library around each of
+    # its launches, on the launch stream, over the same number of steps
+    log("timing kernels over %d steps" % args.steps)
+    binding.prof_enable(8 * args.steps)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    per = {}
+    for name, t in binding.prof_read():
+        per.setdefault(name, []).append(t)
+    binding.prof_enable(0)
+    kernels = {k: {"avg_ms": sum(v) / len(v), "launches": len(v)} for k, v in per.items()}
+    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
+    dom_launches_per_step = kernels[dom]["launches"] / args.steps
+    algo = algorithmic_bytes(dom, total, ndim, w.want_idx)
+    achieved = algo / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
+    for k, v in kernels.items():
+        b = algorithmic_bytes(k, total, ndim, w.want_idx)
+        v["algorithmic_bytes"] = b
+        v["achieved_GBs"] = round(b / (v["avg_ms"] * 1e-3) / 1e9, 1)
+        v["avg_ms"] = round(v["avg_ms"], 5)
+        v["launches"] = int(v["launches"] / args.steps)
+
+    traffic = read_counters(dom, w.name)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": dom, "launches_per_step": dom_launches_per_step}
+
+    cpu = None
+    if not args.no_cpu:
+        log("timing the CPU oracle")
+        cpu = cpu_baseline(mask_np.reshape((w.batch,) + tuple(w.spatial)), ndim, w.sampling)
+
+    vox_s = total / (ms * 1e-3)
+    out = {
+        "metric": "EDT voxels/sec and achieved HBM GB/s (% of peak), batch 8x1x128^3",
+        "value": vox_s,
+        "unit": "voxels/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32" if samp is None else "f64",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "channels": 1,
+                   "spatial": list(w.spatial), "sampling": samp or "unit",
+                   "outputs": "float32 distances" + (" + int32 indices" if w.want_idx else ""),
+                   "mask_sha256": workloads.mask_digest(mask_np)[:16]},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+        "model_GBs_per_step": round(sum(v["algorithmic_bytes"] * v["launches"]
+                                        for v in kernels.values()) / (ms * 1e-3) / 1e9, 1),
+        "source_digest": source_digest(),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
