@@ -27,7 +27,30 @@
 
 #include "edt_common.h"
 
+// Rows of each line kept in flight ahead of the envelope build.
+#ifndef TM_FH_PREFETCH
+#define TM_FH_PREFETCH 16
+#endif
+
 namespace tmedt {
+
+// Arithmetic of one pass.  Unit sampling runs in int32 with full-rate 24-bit
+// multiplies when the host proves every operand fits in 24 bits and every
+// product in 31, in plain int32 when only the products fit, else in int64;
+// sampled passes run in double.  All four give the exact (unit) or the same
+// double-rounded (sampled) breakpoint comparisons.
+template <typename T, bool M24>
+struct Ar {
+    using A = T;
+    __device__ static inline A mul(A x, A y) {
+        if constexpr (M24) return A(__mul24(int(x), int(y)));
+        else return x * y;
+    }
+};
+using ArI24 = Ar<int32_t, true>;
+using ArI32 = Ar<int32_t, false>;
+using ArI64 = Ar<int64_t, false>;
+using ArF64 = Ar<double, false>;
 
 // ---------------------------------------------------------------------------
 // Field path: the working value (int32 squared distance, or float for
@@ -67,8 +90,9 @@ __device__ inline A virtual_sq(int q, uint32_t i, int ndim, const uint32_t *shap
     return acc;
 }
 
-template <typename A, bool PACK, bool FINAL>
+template <class M, bool PACK, bool FINAL>
 __global__ void __launch_bounds__(64) k_fh_field(FieldArgs a) {
+    using A = typename M::A;
     constexpr bool SAMP = std::is_same<A, double>::value;
     using S = typename std::conditional<SAMP, float, int32_t>::type;
     extern __shared__ uint32_t lds[];
@@ -95,14 +119,18 @@ __global__ void __launch_bounds__(64) k_fh_field(FieldArgs a) {
             sf[j * stride] = __builtin_bit_cast(uint32_t, f);
         }
     };
-    auto get = [&](int j, int &v, A &f) {
-        uint32_t e = sv[j * stride];
+    // Raw stack words of entry j (the second word is unused when packed).
+    auto raw = [&](int j, uint32_t &e, uint32_t &g) {
+        e = sv[j * stride];
+        if (!PACK) g = sf[j * stride];
+    };
+    auto decode = [&](uint32_t e, uint32_t g, int &v, A &f) {
         if (PACK) {
             v = int(e & vmask);
             f = A(e >> a.vbits);
         } else {
             v = int(e);
-            f = A(__builtin_bit_cast(S, sf[j * stride]));
+            f = A(__builtin_bit_cast(S, g));
         }
     };
     auto is_site = [](S f) {
@@ -111,42 +139,55 @@ __global__ void __launch_bounds__(64) k_fh_field(FieldArgs a) {
     };
 
     // ---- build the lower envelope -------------------------------------
-    int top = 0;          // stack size
-    int vt = 0, vb = 0;   // apexes of the top two entries
-    A kt = 0, kb = 0;     // g + w v^2 of the top two entries
-    A zn = 0, zd = 1;     // breakpoint between them (top >= 2)
-    constexpr int PF = 8;
-    S cur[PF], nxt[PF];
+    // Registers cache the top entries: (v0, k0) the top, (v1, k1) the one
+    // below, (v2, f2) the third; k = g + w v^2.  (zn, zd) is the breakpoint of
+    // the top against the entry below.  After a pop the new third entry is
+    // fetched from LDS into (e2, g2) and decoded only at the next pop, so a
+    // single pop never waits for LDS.  Line values are prefetched PF rows
+    // ahead into a rotating register buffer with clamped (always in-bounds)
+    // addresses, so each load is waited for only when it is consumed.
+    int top = 0;
+    int v0 = 0, v1 = 0, v2 = 0;
+    A f0 = 0, f1 = 0, f2 = 0;
+    A k0 = 0, k1 = 0;
+    A zn = 0, zd = 1;
+    uint32_t e2 = 0, g2 = 0;
+    bool third_raw = false;  // entry top-3 sits in (e2, g2) rather than (v2, f2)
+    constexpr int PF = TM_FH_PREFETCH;
+    const int last = n - 1;
+    S buf[PF];
 #pragma unroll
-    for (int j = 0; j < PF; ++j) cur[j] = j < n ? line[uint64_t(j) * inner] : S(0);
+    for (int j = 0; j < PF; ++j) buf[j] = line[uint64_t(min(j, last)) * inner];
     for (int q0 = 0; q0 < n; q0 += PF) {
 #pragma unroll
         for (int j = 0; j < PF; ++j) {
-            int q = q0 + PF + j;
-            nxt[j] = q < n ? line[uint64_t(q) * inner] : S(0);
-        }
-#pragma unroll
-        for (int j = 0; j < PF; ++j) {
             const int q = q0 + j;
-            if (q >= n) break;
-            const S fq = cur[j];
-            if (!is_site(fq)) continue;
-            const A kq = A(fq) + W * A(q) * A(q);
+            const S fq = buf[j];
+            buf[j] = line[uint64_t(min(q + PF, last)) * inner];
+            if (q >= n || !is_site(fq)) continue;
+            const A kq = A(fq) + W * M::mul(A(q), A(q));
             A num = 0, den = 1;
             while (top > 0) {
-                num = kq - kt;
-                den = A(2) * W * A(q - vt);
-                if (top >= 2 && num * zd <= zn * den) {
+                num = kq - k0;
+                den = A(2) * W * A(q - v0);
+                if (top >= 2 && M::mul(num, zd) <= M::mul(zn, den)) {
                     // the top parabola is nowhere strictly lowest: drop it
                     --top;
-                    vt = vb;
-                    kt = kb;
+                    v0 = v1;
+                    f0 = f1;
+                    k0 = k1;
                     if (top >= 2) {
-                        A fb;
-                        get(top - 2, vb, fb);
-                        kb = fb + W * A(vb) * A(vb);
-                        zn = kt - kb;
-                        zd = A(2) * W * A(vt - vb);
+                        if (third_raw) {
+                            decode(e2, g2, v1, f1);
+                        } else {
+                            v1 = v2;
+                            f1 = f2;
+                        }
+                        k1 = f1 + W * M::mul(A(v1), A(v1));
+                        zn = k0 - k1;
+                        zd = A(2) * W * A(v0 - v1);
+                        third_raw = top >= 3;
+                        if (third_raw) raw(top - 3, e2, g2);
                     }
                     continue;
                 }
@@ -154,17 +195,20 @@ __global__ void __launch_bounds__(64) k_fh_field(FieldArgs a) {
             }
             put(top, q, fq);
             if (top >= 1) {
-                vb = vt;
-                kb = kt;
+                v2 = v1;
+                f2 = f1;
+                third_raw = false;
+                v1 = v0;
+                f1 = f0;
+                k1 = k0;
                 zn = num;
                 zd = den;
             }
-            vt = q;
-            kt = kq;
+            v0 = q;
+            f0 = A(fq);
+            k0 = kq;
             ++top;
         }
-#pragma unroll
-        for (int j = 0; j < PF; ++j) cur[j] = nxt[j];
     }
 
     // ---- query every position ------------------------------------------
@@ -188,33 +232,40 @@ __global__ void __launch_bounds__(64) k_fh_field(FieldArgs a) {
         }
         return;
     }
+    // Entry k is current, k + 1 is decoded in registers, k + 2 is in flight.
     int k = 0;
     int vc, vn = 0;
     A fc, fn = 0;
-    get(0, vc, fc);
-    A kc = fc + W * A(vc) * A(vc), kn = 0;
+    uint32_t e, g = 0;
+    raw(0, e, g);
+    decode(e, g, vc, fc);
+    A kc = fc + W * M::mul(A(vc), A(vc)), kn = 0;
     A bn = 0, bd = 1;  // breakpoint between entries k and k + 1
+    uint32_t ep = 0, gp = 0;
     if (top > 1) {
-        get(1, vn, fn);
-        kn = fn + W * A(vn) * A(vn);
+        raw(1, e, g);
+        decode(e, g, vn, fn);
+        kn = fn + W * M::mul(A(vn), A(vn));
         bn = kn - kc;
         bd = A(2) * W * A(vn - vc);
+        if (top > 2) raw(2, ep, gp);
     }
     for (int q = 0; q < n; ++q) {
-        while (k + 1 < top && bn < A(q) * bd) {
+        while (k + 1 < top && bn < M::mul(A(q), bd)) {
             ++k;
             vc = vn;
             fc = fn;
             kc = kn;
             if (k + 1 < top) {
-                get(k + 1, vn, fn);
-                kn = fn + W * A(vn) * A(vn);
+                decode(ep, gp, vn, fn);
+                kn = fn + W * M::mul(A(vn), A(vn));
                 bn = kn - kc;
                 bd = A(2) * W * A(vn - vc);
+                if (k + 2 < top) raw(k + 2, ep, gp);
             }
         }
         const A d = A(q - vc);
-        emit(q, fc + W * d * d);
+        emit(q, fc + W * M::mul(d, d));
     }
 }
 
@@ -240,8 +291,9 @@ struct IndexArgs {
     int32_t *sq;
 };
 
-template <typename A, bool FINAL>
+template <class M, bool FINAL>
 __global__ void __launch_bounds__(64) k_fh_index(IndexArgs a) {
+    using A = typename M::A;
     constexpr bool SAMP = std::is_same<A, double>::value;
     extern __shared__ uint32_t lds[];
 
@@ -294,7 +346,7 @@ __global__ void __launch_bounds__(64) k_fh_index(IndexArgs a) {
                 if (yc) yc[b] = yb;
                 int d = xc[b] - yb;
                 if (SAMP) acc += a.wall[b] * double(d) * double(d);
-                else acc += A(d) * A(d);
+                else acc += M::mul(A(d), A(d));
             }
         }
         f = acc;
@@ -323,19 +375,19 @@ __global__ void __launch_bounds__(64) k_fh_index(IndexArgs a) {
             int vq;
             A fq;
             decode(yq, vq, fq, nullptr);
-            const A kq = fq + W * A(q) * A(q);
+            const A kq = fq + W * M::mul(A(q), A(q));
             A num = 0, den = 1;
             while (top > 0) {
                 num = kq - kt;
                 den = A(2) * W * A(q - vt);
-                if (top >= 2 && num * zd <= zn * den) {
+                if (top >= 2 && M::mul(num, zd) <= M::mul(zn, den)) {
                     --top;
                     vt = vb;
                     kt = kb;
                     if (top >= 2) {
                         A fb;
                         decode(int32_t(st[(top - 2) * stride]), vb, fb, nullptr);
-                        kb = fb + W * A(vb) * A(vb);
+                        kb = fb + W * M::mul(A(vb), A(vb));
                         zn = kt - kb;
                         zd = A(2) * W * A(vt - vb);
                     }
@@ -394,16 +446,16 @@ __global__ void __launch_bounds__(64) k_fh_index(IndexArgs a) {
 #pragma unroll
     for (int b = 0; b < kMaxDim; ++b) cc[b] = cn[b] = 0;
     decode(yc, vc, fc, cc);
-    A kc = fc + W * A(vc) * A(vc), kn = 0, bn = 0, bd = 1;
+    A kc = fc + W * M::mul(A(vc), A(vc)), kn = 0, bn = 0, bd = 1;
     if (top > 1) {
         yn = int32_t(st[stride]);
         decode(yn, vn, fn, cn);
-        kn = fn + W * A(vn) * A(vn);
+        kn = fn + W * M::mul(A(vn), A(vn));
         bn = kn - kc;
         bd = A(2) * W * A(vn - vc);
     }
     for (int q = 0; q < n; ++q) {
-        while (k + 1 < top && bn < A(q) * bd) {
+        while (k + 1 < top && bn < M::mul(A(q), bd)) {
             ++k;
             vc = vn;
             fc = fn;
@@ -414,7 +466,7 @@ __global__ void __launch_bounds__(64) k_fh_index(IndexArgs a) {
             if (k + 1 < top) {
                 yn = int32_t(st[(k + 1) * stride]);
                 decode(yn, vn, fn, cn);
-                kn = fn + W * A(vn) * A(vn);
+                kn = fn + W * M::mul(A(vn), A(vn));
                 bn = kn - kc;
                 bd = A(2) * W * A(vn - vc);
             }
@@ -424,7 +476,7 @@ __global__ void __launch_bounds__(64) k_fh_index(IndexArgs a) {
             line[e] = yc;
         } else {
             const A d = A(q - vc);
-            const A d2 = fc + W * d * d;
+            const A d2 = fc + W * M::mul(d, d);
             const uint64_t loc = base + i + e;
             if (a.dist) a.dist[s * vox + loc] = float(sqrt(double(d2)));
             if (a.sq) a.sq[s * vox + loc] = int32_t(d2);
@@ -433,6 +485,211 @@ __global__ void __launch_bounds__(64) k_fh_index(IndexArgs a) {
             for (int b = 1; b < kMaxDim; ++b)
                 if (b < nd) slice0[uint64_t(b) * vox + loc] = cc[b];
         }
+    }
+}
+
+}  // namespace tmedt
+
+namespace tmedt {
+
+// ---------------------------------------------------------------------------
+// Tiled pass (unit sampling, field carrier): a workgroup stages the whole of
+// 64 adjacent lines in LDS as tile[q][lane] (coalesced 256-byte rows), then
+// every element q searches outwards, d = 1, 2, ..., for
+//     min over |p - q| <= d of g(p) + (q - p)^2,
+// stopping at the first d with d^2 greater than the best value so far (no
+// site farther away can do better).  The result is the exact minimum of the
+// envelope pass.  Elements are independent, so the four waves of the
+// workgroup split the rows and no per-line sequential chain remains.
+//
+// A search that has not stopped after `cap` steps marks the tile as hard;
+// the workgroup then recomputes every line of the tile with the sequential
+// lower-envelope build from the LDS copy (one lane per line), keeping the
+// envelope stack in the high bits of the tile words.  The tile's global
+// outputs are simply written again with the same exact values.
+// ---------------------------------------------------------------------------
+struct TileArgs {
+    int32_t *buf;         // int32 squared distances, batch-flat, updated in place
+    uint64_t lines;       // batch * voxels / n
+    uint32_t n;           // line length
+    uint32_t inner;       // element stride of the line
+    uint32_t cap;         // search steps before falling back
+    uint32_t fbits;       // tile words: value in the low fbits, stack apex above
+    // final pass only (axis 0)
+    float *dist;
+    int32_t *sq;
+    int32_t ndim;
+    uint32_t shape[kMaxDim];
+    double wall[kMaxDim];
+};
+
+constexpr int kTileWaves = 4;
+
+template <bool FINAL>
+__global__ void __launch_bounds__(kWave * kTileWaves) k_tile_field(TileArgs a) {
+    extern __shared__ int32_t tile[];  // [n][kWave]
+    __shared__ int hard;
+    __shared__ uint32_t any_site[kTileWaves][kWave];
+    const int t = threadIdx.x;
+    const int lane = t & (kWave - 1);
+    const int wv = __builtin_amdgcn_readfirstlane(t / kWave);  // wave-uniform
+    const int n = int(a.n);
+    const uint64_t L = uint64_t(blockIdx.x) * kWave + lane;
+    const bool live = L < a.lines;
+    const uint64_t inner = a.inner;
+    uint64_t o = 0, i = 0;
+    if (live) {
+        o = L / inner;
+        i = L - o * inner;
+    }
+    const uint64_t base = o * uint64_t(n) * inner + i;
+    // lanes past the last line read line 0 (always valid) and discard it
+    const int32_t *src = a.buf + (live ? base : 0);
+    const int32_t fmask = int32_t((1u << a.fbits) - 1u);  // also the "no site" code
+    const int cap = int(a.cap);
+
+    if (t == 0) hard = 0;
+    // Stage: each wave reads rows wv, wv + 4, ...; SB loads are issued before
+    // the first is consumed (row indices clamped so every load is in bounds).
+    uint32_t seen = 0;
+    constexpr int SB = 8;
+    for (int q0 = wv; q0 < n; q0 += kTileWaves * SB) {
+        int32_t v[SB];
+#pragma unroll
+        for (int j = 0; j < SB; ++j) {
+            const int q = min(q0 + j * kTileWaves, n - 1);
+            v[j] = src[uint64_t(q) * inner];
+        }
+#pragma unroll
+        for (int j = 0; j < SB; ++j) {
+            const int q = q0 + j * kTileWaves;
+            if (q < n) {
+                const int32_t f = (!live || v[j] == kInfI) ? fmask : v[j];
+                seen |= f != fmask;
+                tile[q * kWave + lane] = f;
+            }
+        }
+    }
+    any_site[wv][lane] = seen;
+    __syncthreads();
+    bool has_site = false;
+#pragma unroll
+    for (int w = 0; w < kTileWaves; ++w) has_site |= any_site[w][lane] != 0;
+
+    int32_t *out_i = a.buf + base;
+    auto emit = [&](int q, int32_t d2, bool none) {
+        const uint64_t off = uint64_t(q) * inner;  // uniform across the wave
+        const uint64_t g = base + off;
+        if (!FINAL) {
+            out_i[off] = none ? kInfI : d2;
+        } else {
+            int64_t v = none ? virtual_sq<int64_t>(q, uint32_t(i), a.ndim, a.shape, a.wall) : d2;
+            if (a.dist) a.dist[g] = float(sqrt(double(v)));
+            if (a.sq) a.sq[g] = int32_t(v);
+        }
+    };
+
+    // ---- windowed exact search ----------------------------------------
+    // The step loop is uniform across the wave: a lane whose search has
+    // stopped keeps taking minima, which cannot change its value (every
+    // farther candidate is at least d^2 > best).  One wave-wide vote per
+    // two steps ends the loop.
+    bool mine_hard = false;
+    const int32_t *col = tile + lane;
+    for (int q = wv; q < n; q += kTileWaves) {
+        if (!live) break;
+        int32_t best = col[q * kWave];
+        if (!has_site) {
+            emit(q, 0, true);
+            continue;
+        }
+        int d = 1;
+        while (d <= cap) {
+            if (__all(best < d * d)) break;
+            const int lo = q - d, hi = q + d;
+            const int32_t a0 = lo >= 0 ? col[lo * kWave] : fmask;
+            const int32_t a1 = hi < n ? col[hi * kWave] : fmask;
+            const int32_t b0 = lo >= 1 ? col[(lo - 1) * kWave] : fmask;
+            const int32_t b1 = hi + 1 < n ? col[(hi + 1) * kWave] : fmask;
+            best = min(best, min(a0, a1) + d * d);
+            best = min(best, min(b0, b1) + (d + 1) * (d + 1));
+            d += 2;
+        }
+        if (best >= d * d) {
+            mine_hard = true;
+        } else {
+            emit(q, best, false);
+        }
+    }
+    if (mine_hard) hard = 1;
+    __syncthreads();
+    if (!hard || wv != 0 || !live || !has_site) return;
+
+    // ---- fallback: sequential lower envelope from the LDS copy ----------
+    const int fb = int(a.fbits);
+    auto val = [&](int p) { return tile[p * kWave + lane] & fmask; };
+    auto apex = [&](int j) { return int(uint32_t(tile[j * kWave + lane]) >> fb); };
+    auto push = [&](int j, int v) {
+        int32_t &w = tile[j * kWave + lane];
+        w = (w & fmask) | int32_t(uint32_t(v) << fb);
+    };
+    int top = 0, vt = 0, vb = 0;
+    int32_t kt = 0, kb = 0, zn = 0, zd = 1;
+    for (int q = 0; q < n; ++q) {
+        const int32_t fq = val(q);
+        if (fq == fmask) continue;
+        const int32_t kq = fq + q * q;
+        int32_t num = 0, den = 1;
+        while (top > 0) {
+            num = kq - kt;
+            den = 2 * (q - vt);
+            if (top >= 2 && int64_t(num) * zd <= int64_t(zn) * den) {
+                --top;
+                vt = vb;
+                kt = kb;
+                if (top >= 2) {
+                    vb = apex(top - 2);
+                    kb = val(vb) + vb * vb;
+                    zn = kt - kb;
+                    zd = 2 * (vt - vb);
+                }
+                continue;
+            }
+            break;
+        }
+        push(top, q);
+        if (top >= 1) {
+            vb = vt;
+            kb = kt;
+            zn = num;
+            zd = den;
+        }
+        vt = q;
+        kt = kq;
+        ++top;
+    }
+    int k = 0;
+    int vc = apex(0), vn = 0;
+    int32_t kc = val(vc) + vc * vc, kn = 0, bn = 0, bd = 1;
+    if (top > 1) {
+        vn = apex(1);
+        kn = val(vn) + vn * vn;
+        bn = kn - kc;
+        bd = 2 * (vn - vc);
+    }
+    for (int q = 0; q < n; ++q) {
+        while (k + 1 < top && int64_t(bn) < int64_t(q) * bd) {
+            ++k;
+            vc = vn;
+            kc = kn;
+            if (k + 1 < top) {
+                vn = apex(k + 1);
+                kn = val(vn) + vn * vn;
+                bn = kn - kc;
+                bd = 2 * (vn - vc);
+            }
+        }
+        emit(q, kc - vc * vc + (q - vc) * (q - vc), false);
     }
 }
 

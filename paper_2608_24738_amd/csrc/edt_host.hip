@@ -110,6 +110,12 @@ bool int32_safe(uint64_t fmax, uint64_t n) {
     return true;
 }
 
+// ... and every operand also fits in a signed 24-bit multiply.
+bool int24_safe(uint64_t fmax, uint64_t n) {
+    const uint64_t lim24 = (uint64_t(1) << 23) - 1;
+    return int32_safe(fmax, n) && fmax + (n - 1) * (n - 1) < lim24 && 2 * (n - 1) < lim24;
+}
+
 struct Request {
     const uint8_t *in;
     int ndim;
@@ -175,15 +181,18 @@ int run(Request &r) {
     struct FhPlan {
         uint32_t lpw;
         bool pack;
-        int acc;  // 0 int32, 1 int64, 2 double
+        int acc;  // 0 int32 with 24-bit multiplies, 1 int32, 2 int64, 3 double
         size_t lds;
+        bool tiled;      // staged tile + windowed search (k_tile_field)
+        uint32_t fbits;  // tiled: value bits of a tile word
+        uint32_t cap;    // tiled: search steps before the envelope fallback
     } fh[kMaxDim] = {};
     for (int a = nd - 2; a >= 0; --a) {
         const uint32_t n = r.shape[a];
         uint64_t fmax = 0;
         for (int b = a + 1; b < nd; ++b) fmax += uint64_t(r.shape[b] - 1) * (r.shape[b] - 1);
         FhPlan &p = fh[a];
-        p.acc = r.unit ? (int32_safe(fmax, n) ? 0 : 1) : 2;
+        p.acc = !r.unit ? 3 : int24_safe(fmax, n) ? 0 : int32_safe(fmax, n) ? 1 : 2;
         uint32_t eb;
         if (index_path) {
             p.pack = false;
@@ -195,6 +204,26 @@ int run(Request &r) {
             eb = p.pack ? 4 : 8;
         }
         p.lpw = lanes_for(n, eb);
+        // Tiled pass: 64 lines x n int32 words in LDS, each word holding the
+        // value in its low fbits bits and (during a fallback) an envelope
+        // apex above them.  "No site" is coded as the all-ones value, which
+        // must exceed every real value plus cap^2.
+        if (!index_path && r.unit) {
+            const uint32_t cap = n - 1 < 64 ? n - 1 : 64;
+            int vbits = bits_for(n - 1);
+            if (vbits < 1) vbits = 1;
+            const int fbits = 32 - vbits < 30 ? 32 - vbits : 30;
+            const uint64_t fmask = (uint64_t(1) << fbits) - 1;
+            const size_t tile = size_t(n) * kWave * 4;
+            if (tile + 2048 <= kLdsBytes && fmax + uint64_t(n - 1) * (n - 1) < (uint64_t(1) << 30) &&
+                fmask > fmax + uint64_t(cap) * cap) {
+                p.tiled = true;
+                p.fbits = uint32_t(fbits);
+                p.cap = cap;
+                p.lds = tile;
+                continue;
+            }
+        }
         if (p.lpw == 0) return TM_ERR_UNSUPPORTED;
         const uint64_t lines = total / n;
         if ((lines + p.lpw - 1) / p.lpw >= (uint64_t(1) << 31)) return TM_ERR_UNSUPPORTED;
@@ -277,7 +306,25 @@ int run(Request &r) {
         const uint64_t lines = total / n;
         const dim3 grid(uint32_t((lines + p.lpw - 1) / p.lpw)), block(kWave);
         const bool fin = a == 0;
-        if (!index_path) {
+        if (p.tiled) {
+            TileArgs tg{};
+            tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
+            tg.lines = lines;
+            tg.n = n;
+            tg.inner = uint32_t(inner);
+            tg.cap = p.cap;
+            tg.fbits = p.fbits;
+            tg.dist = r.dist;
+            tg.sq = r.sq;
+            tg.ndim = nd;
+            for (int b = 0; b < nd; ++b) {
+                tg.shape[b] = r.shape[b];
+                tg.wall[b] = r.w[b];
+            }
+            const dim3 tgrid(uint32_t((lines + kWave - 1) / kWave)), tblock(kWave * kTileWaves);
+            rc = fin ? launch("tile_field_final", k_tile_field<true>, tgrid, tblock, p.lds, r.stream, tg)
+                     : launch("tile_field", k_tile_field<false>, tgrid, tblock, p.lds, r.stream, tg);
+        } else if (!index_path) {
             FieldArgs f{};
             f.buf = r.dist ? static_cast<void *>(r.dist) : static_cast<void *>(r.sq);
             f.lines = lines;
@@ -295,12 +342,14 @@ int run(Request &r) {
                 f.wall[b] = r.w[b];
             }
             const char *nm = fin ? "fh_field_final" : "fh_field";
-#define TM_FIELD(A, PK, FN) launch(nm, k_fh_field<A, PK, FN>, grid, block, p.lds, r.stream, f)
-            if (p.acc == 2) rc = fin ? TM_FIELD(double, false, true) : TM_FIELD(double, false, false);
-            else if (p.acc == 0 && p.pack) rc = fin ? TM_FIELD(int32_t, true, true) : TM_FIELD(int32_t, true, false);
-            else if (p.acc == 0) rc = fin ? TM_FIELD(int32_t, false, true) : TM_FIELD(int32_t, false, false);
-            else if (p.pack) rc = fin ? TM_FIELD(int64_t, true, true) : TM_FIELD(int64_t, true, false);
-            else rc = fin ? TM_FIELD(int64_t, false, true) : TM_FIELD(int64_t, false, false);
+#define TM_FIELD(M, PK, FN) launch(nm, k_fh_field<M, PK, FN>, grid, block, p.lds, r.stream, f)
+            if (p.acc == 3) rc = fin ? TM_FIELD(ArF64, false, true) : TM_FIELD(ArF64, false, false);
+            else if (p.acc == 0 && p.pack) rc = fin ? TM_FIELD(ArI24, true, true) : TM_FIELD(ArI24, true, false);
+            else if (p.acc == 0) rc = fin ? TM_FIELD(ArI24, false, true) : TM_FIELD(ArI24, false, false);
+            else if (p.acc == 1 && p.pack) rc = fin ? TM_FIELD(ArI32, true, true) : TM_FIELD(ArI32, true, false);
+            else if (p.acc == 1) rc = fin ? TM_FIELD(ArI32, false, true) : TM_FIELD(ArI32, false, false);
+            else if (p.pack) rc = fin ? TM_FIELD(ArI64, true, true) : TM_FIELD(ArI64, true, false);
+            else rc = fin ? TM_FIELD(ArI64, false, true) : TM_FIELD(ArI64, false, false);
 #undef TM_FIELD
         } else {
             IndexArgs x{};
@@ -321,10 +370,11 @@ int run(Request &r) {
             x.dist = fin ? r.dist : nullptr;
             x.sq = fin ? r.sq : nullptr;
             const char *nm = fin ? "fh_index_final" : "fh_index";
-#define TM_INDEX(A, FN) launch(nm, k_fh_index<A, FN>, grid, block, p.lds, r.stream, x)
-            if (p.acc == 2) rc = fin ? TM_INDEX(double, true) : TM_INDEX(double, false);
-            else if (p.acc == 0) rc = fin ? TM_INDEX(int32_t, true) : TM_INDEX(int32_t, false);
-            else rc = fin ? TM_INDEX(int64_t, true) : TM_INDEX(int64_t, false);
+#define TM_INDEX(M, FN) launch(nm, k_fh_index<M, FN>, grid, block, p.lds, r.stream, x)
+            if (p.acc == 3) rc = fin ? TM_INDEX(ArF64, true) : TM_INDEX(ArF64, false);
+            else if (p.acc == 0) rc = fin ? TM_INDEX(ArI24, true) : TM_INDEX(ArI24, false);
+            else if (p.acc == 1) rc = fin ? TM_INDEX(ArI32, true) : TM_INDEX(ArI32, false);
+            else rc = fin ? TM_INDEX(ArI64, true) : TM_INDEX(ArI64, false);
 #undef TM_INDEX
         }
         if (rc != TM_OK) return rc;
