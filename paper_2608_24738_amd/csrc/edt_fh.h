@@ -603,17 +603,31 @@ __global__ void __launch_bounds__(kWave * kTileWaves) k_tile_field(TileArgs a) {
             emit(q, 0, true);
             continue;
         }
+        // Blocks of four steps per vote; a block whose rows all lie inside
+        // the line (the common case) reads without bound checks.
         int d = 1;
         while (d <= cap) {
             if (__all(best < d * d)) break;
-            const int lo = q - d, hi = q + d;
-            const int32_t a0 = lo >= 0 ? col[lo * kWave] : fmask;
-            const int32_t a1 = hi < n ? col[hi * kWave] : fmask;
-            const int32_t b0 = lo >= 1 ? col[(lo - 1) * kWave] : fmask;
-            const int32_t b1 = hi + 1 < n ? col[(hi + 1) * kWave] : fmask;
-            best = min(best, min(a0, a1) + d * d);
-            best = min(best, min(b0, b1) + (d + 1) * (d + 1));
-            d += 2;
+            if (q - d - 3 >= 0 && q + d + 3 < n) {
+                const int32_t *up = col + (q - d) * kWave;
+                const int32_t *dn = col + (q + d) * kWave;
+                const int32_t u0 = up[0], u1 = up[-kWave], u2 = up[-2 * kWave], u3 = up[-3 * kWave];
+                const int32_t w0 = dn[0], w1 = dn[kWave], w2 = dn[2 * kWave], w3 = dn[3 * kWave];
+                const int32_t c0 = min(u0, w0) + d * d;
+                const int32_t c1 = min(u1, w1) + (d + 1) * (d + 1);
+                const int32_t c2 = min(u2, w2) + (d + 2) * (d + 2);
+                const int32_t c3 = min(u3, w3) + (d + 3) * (d + 3);
+                best = min(min(best, min(c0, c1)), min(c2, c3));
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int lo = q - d - j, hi = q + d + j;
+                    const int32_t x0 = lo >= 0 ? col[lo * kWave] : fmask;
+                    const int32_t x1 = hi < n ? col[hi * kWave] : fmask;
+                    best = min(best, min(x0, x1) + (d + j) * (d + j));
+                }
+            }
+            d += 4;
         }
         if (best >= d * d) {
             mine_hard = true;
@@ -684,6 +698,217 @@ __global__ void __launch_bounds__(kWave * kTileWaves) k_tile_field(TileArgs a) {
             kc = kn;
             if (k + 1 < top) {
                 vn = apex(k + 1);
+                kn = val(vn) + vn * vn;
+                bn = kn - kc;
+                bd = 2 * (vn - vc);
+            }
+        }
+        emit(q, kc - vc * vc + (q - vc) * (q - vc), false);
+    }
+}
+
+}  // namespace tmedt
+
+namespace tmedt {
+
+// ---------------------------------------------------------------------------
+// 16-bit tiled pass: as k_tile_field, for passes whose values (plus the
+// squared search reach) fit in 16 bits.  The tile holds u16 values with G
+// guard rows of "no site" (0xffff) above and below the line, so every read of
+// the search is in bounds without a test; the search is unrolled in blocks of
+// four steps, which makes every squared distance a literal and every LDS
+// offset an immediate.  The fallback keeps its envelope stack (apex per
+// level) in the guard rows, which the search no longer needs.
+// ---------------------------------------------------------------------------
+constexpr int kCap16 = 64;                 // search steps before the fallback
+constexpr int kGuard16 = kCap16 + 4;       // minimum guard rows per side
+constexpr int32_t kNone16 = 0xffff;
+
+struct Tile16Args {
+    int32_t *buf;         // int32 squared distances, batch-flat, in place
+    uint64_t lines;
+    uint32_t n;
+    uint32_t inner;
+    uint32_t guard;       // guard rows per side: >= kGuard16 and 2 * guard >= n
+    float *dist;          // final pass outputs
+    int32_t *sq;
+    int32_t ndim;
+    uint32_t shape[kMaxDim];
+    double wall[kMaxDim];
+};
+
+template <bool FINAL>
+__global__ void __launch_bounds__(kWave * kTileWaves) k_tile16(Tile16Args a) {
+    extern __shared__ uint16_t t16[];      // rows [-guard, n + guard) x kWave
+    __shared__ int hard;
+    __shared__ uint32_t any_site[kTileWaves][kWave];
+    const int t = threadIdx.x;
+    const int lane = t & (kWave - 1);
+    const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
+    const int n = int(a.n);
+    const int G = int(a.guard);
+    const uint64_t L = uint64_t(blockIdx.x) * kWave + lane;
+    const bool live = L < a.lines;
+    const uint64_t inner = a.inner;
+    uint64_t o = 0, i = 0;
+    if (live) {
+        o = L / inner;
+        i = L - o * inner;
+    }
+    const uint64_t base = o * uint64_t(n) * inner + i;
+    const int32_t *src = a.buf + (live ? base : 0);
+    uint16_t *row0 = t16 + G * kWave;      // row 0 of the line
+
+    if (t == 0) hard = 0;
+    // guard rows: "no site", written as 32-bit pairs
+    {
+        uint32_t *g32 = reinterpret_cast<uint32_t *>(t16);
+        const int half = G * kWave / 2;    // u32 words per guard block
+        uint32_t *g2 = reinterpret_cast<uint32_t *>(t16 + (G + n) * kWave);
+        for (int k = t; k < half; k += kWave * kTileWaves) {
+            g32[k] = 0xffffffffu;
+            g2[k] = 0xffffffffu;
+        }
+    }
+    uint32_t seen = 0;
+    constexpr int SB = 8;
+    for (int q0 = wv; q0 < n; q0 += kTileWaves * SB) {
+        int32_t v[SB];
+#pragma unroll
+        for (int j = 0; j < SB; ++j) {
+            const int q = min(q0 + j * kTileWaves, n - 1);
+            v[j] = src[uint64_t(q) * inner];
+        }
+#pragma unroll
+        for (int j = 0; j < SB; ++j) {
+            const int q = q0 + j * kTileWaves;
+            if (q < n) {
+                const int32_t f = (!live || v[j] == kInfI) ? kNone16 : v[j];
+                seen |= f != kNone16;
+                row0[q * kWave + lane] = uint16_t(f);
+            }
+        }
+    }
+    any_site[wv][lane] = seen;
+    __syncthreads();
+    bool has_site = false;
+#pragma unroll
+    for (int w = 0; w < kTileWaves; ++w) has_site |= any_site[w][lane] != 0;
+
+    int32_t *out_i = a.buf + base;
+    auto emit = [&](int q, int32_t d2, bool none) {
+        const uint64_t off = uint64_t(q) * inner;
+        if (!FINAL) {
+            out_i[off] = none ? kInfI : d2;
+        } else {
+            const uint64_t g = base + off;
+            if (none) {
+                const int64_t v = virtual_sq<int64_t>(q, uint32_t(i), a.ndim, a.shape, a.wall);
+                if (a.dist) a.dist[g] = float(sqrt(double(v)));
+                if (a.sq) a.sq[g] = int32_t(v);
+            } else {
+                // d2 < 2^24 converts exactly; sqrtf is correctly rounded
+                if (a.dist) a.dist[g] = sqrtf(float(d2));
+                if (a.sq) a.sq[g] = d2;
+            }
+        }
+    };
+
+    // ---- windowed exact search, unrolled -----------------------------------
+    bool mine_hard = false;
+    for (int q = wv; q < n; q += kTileWaves) {
+        if (!live) break;
+        if (!has_site) {
+            emit(q, 0, true);
+            continue;
+        }
+        const uint16_t *dn = row0 + q * kWave + lane;        // rows q + d at +d*kWave
+        const uint16_t *up = dn - kGuard16 * kWave;          // rows q - d at (kGuard16 - d)*kWave
+        int32_t best = dn[0];
+        int dnext = 1;
+#pragma unroll
+        for (int blk = 0; blk < kCap16 / 4; ++blk) {
+            const int d = 1 + 4 * blk;
+            if (__all(best < d * d)) break;
+            const int32_t u0 = up[(kGuard16 - d) * kWave], u1 = up[(kGuard16 - d - 1) * kWave];
+            const int32_t u2 = up[(kGuard16 - d - 2) * kWave], u3 = up[(kGuard16 - d - 3) * kWave];
+            const int32_t w0 = dn[d * kWave], w1 = dn[(d + 1) * kWave];
+            const int32_t w2 = dn[(d + 2) * kWave], w3 = dn[(d + 3) * kWave];
+            const int32_t c0 = min(u0, w0) + d * d;
+            const int32_t c1 = min(u1, w1) + (d + 1) * (d + 1);
+            const int32_t c2 = min(u2, w2) + (d + 2) * (d + 2);
+            const int32_t c3 = min(u3, w3) + (d + 3) * (d + 3);
+            best = min(min(best, min(c0, c1)), min(c2, c3));
+            dnext = d + 4;
+        }
+        if (best >= dnext * dnext) {
+            mine_hard = true;
+        } else {
+            emit(q, best, false);
+        }
+    }
+    if (mine_hard) hard = 1;
+    __syncthreads();
+    if (!hard || wv != 0 || !live || !has_site) return;
+
+    // ---- fallback: sequential lower envelope from the LDS copy --------------
+    // Stack level j keeps its apex in guard row j (top guard block first, then
+    // the bottom one); 2 * guard >= n levels are available.
+    auto val = [&](int p) { return int32_t(row0[p * kWave + lane]); };
+    auto slot = [&](int j) -> uint16_t & {
+        return j < G ? t16[j * kWave + lane] : t16[(n + j) * kWave + lane];
+    };
+    int top = 0, vt = 0, vb = 0;
+    int32_t kt = 0, kb = 0, zn = 0, zd = 1;
+    for (int q = 0; q < n; ++q) {
+        const int32_t fq = val(q);
+        if (fq == kNone16) continue;
+        const int32_t kq = fq + q * q;
+        int32_t num = 0, den = 1;
+        while (top > 0) {
+            num = kq - kt;
+            den = 2 * (q - vt);
+            if (top >= 2 && int64_t(num) * zd <= int64_t(zn) * den) {
+                --top;
+                vt = vb;
+                kt = kb;
+                if (top >= 2) {
+                    vb = slot(top - 2);
+                    kb = val(vb) + vb * vb;
+                    zn = kt - kb;
+                    zd = 2 * (vt - vb);
+                }
+                continue;
+            }
+            break;
+        }
+        slot(top) = uint16_t(q);
+        if (top >= 1) {
+            vb = vt;
+            kb = kt;
+            zn = num;
+            zd = den;
+        }
+        vt = q;
+        kt = kq;
+        ++top;
+    }
+    int k = 0;
+    int vc = slot(0), vn = 0;
+    int32_t kc = val(vc) + vc * vc, kn = 0, bn = 0, bd = 1;
+    if (top > 1) {
+        vn = slot(1);
+        kn = val(vn) + vn * vn;
+        bn = kn - kc;
+        bd = 2 * (vn - vc);
+    }
+    for (int q = 0; q < n; ++q) {
+        while (k + 1 < top && int64_t(bn) < int64_t(q) * bd) {
+            ++k;
+            vc = vn;
+            kc = kn;
+            if (k + 1 < top) {
+                vn = slot(k + 1);
                 kn = val(vn) + vn * vn;
                 bn = kn - kc;
                 bd = 2 * (vn - vc);

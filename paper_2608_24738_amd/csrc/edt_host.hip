@@ -184,8 +184,10 @@ int run(Request &r) {
         int acc;  // 0 int32 with 24-bit multiplies, 1 int32, 2 int64, 3 double
         size_t lds;
         bool tiled;      // staged tile + windowed search (k_tile_field)
+        bool tiled16;    // 16-bit tile with guard rows (k_tile16)
         uint32_t fbits;  // tiled: value bits of a tile word
         uint32_t cap;    // tiled: search steps before the envelope fallback
+        uint32_t guard;  // tiled16: guard rows per side
     } fh[kMaxDim] = {};
     for (int a = nd - 2; a >= 0; --a) {
         const uint32_t n = r.shape[a];
@@ -207,8 +209,21 @@ int run(Request &r) {
         // Tiled pass: 64 lines x n int32 words in LDS, each word holding the
         // value in its low fbits bits and (during a fallback) an envelope
         // apex above them.  "No site" is coded as the all-ones value, which
-        // must exceed every real value plus cap^2.
+        // must exceed every real value plus the square of the farthest step
+        // a search takes (cap + 3).
         if (!index_path && r.unit) {
+            // 16-bit tile: values and the search reach below the "no site" code
+            const uint32_t g16 = uint32_t(kGuard16) > (n + 1) / 2 ? uint32_t(kGuard16) : (n + 1) / 2;
+            const size_t t16 = size_t(n + 2 * g16) * kWave * 2;
+            if (fmax + uint64_t(kCap16 + 3) * (kCap16 + 3) < uint64_t(kNone16) &&
+                fmax + uint64_t(n - 1) * (n - 1) < (uint64_t(1) << 30) && t16 + 2048 <= kLdsBytes) {
+                p.tiled16 = true;
+                p.guard = g16;
+                p.lds = t16;
+                continue;
+            }
+        }
+        if (!index_path && r.unit && n <= 256) {
             const uint32_t cap = n - 1 < 64 ? n - 1 : 64;
             int vbits = bits_for(n - 1);
             if (vbits < 1) vbits = 1;
@@ -216,7 +231,7 @@ int run(Request &r) {
             const uint64_t fmask = (uint64_t(1) << fbits) - 1;
             const size_t tile = size_t(n) * kWave * 4;
             if (tile + 2048 <= kLdsBytes && fmax + uint64_t(n - 1) * (n - 1) < (uint64_t(1) << 30) &&
-                fmask > fmax + uint64_t(cap) * cap) {
+                fmask > fmax + uint64_t(cap + 4) * (cap + 4)) {
                 p.tiled = true;
                 p.fbits = uint32_t(fbits);
                 p.cap = cap;
@@ -306,7 +321,24 @@ int run(Request &r) {
         const uint64_t lines = total / n;
         const dim3 grid(uint32_t((lines + p.lpw - 1) / p.lpw)), block(kWave);
         const bool fin = a == 0;
-        if (p.tiled) {
+        if (p.tiled16) {
+            Tile16Args tg{};
+            tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
+            tg.lines = lines;
+            tg.n = n;
+            tg.inner = uint32_t(inner);
+            tg.guard = p.guard;
+            tg.dist = r.dist;
+            tg.sq = r.sq;
+            tg.ndim = nd;
+            for (int b = 0; b < nd; ++b) {
+                tg.shape[b] = r.shape[b];
+                tg.wall[b] = r.w[b];
+            }
+            const dim3 tgrid(uint32_t((lines + kWave - 1) / kWave)), tblock(kWave * kTileWaves);
+            rc = fin ? launch("tile16_final", k_tile16<true>, tgrid, tblock, p.lds, r.stream, tg)
+                     : launch("tile16", k_tile16<false>, tgrid, tblock, p.lds, r.stream, tg);
+        } else if (p.tiled) {
             TileArgs tg{};
             tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
             tg.lines = lines;
