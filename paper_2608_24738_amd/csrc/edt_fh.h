@@ -27,10 +27,6 @@
 
 #include "edt_common.h"
 
-// Rows of each line kept in flight ahead of the envelope build.
-#ifndef TM_FH_PREFETCH
-#define TM_FH_PREFETCH 16
-#endif
 
 namespace tmedt {
 
@@ -119,18 +115,14 @@ __global__ void __launch_bounds__(64) k_fh_field(FieldArgs a) {
             sf[j * stride] = __builtin_bit_cast(uint32_t, f);
         }
     };
-    // Raw stack words of entry j (the second word is unused when packed).
-    auto raw = [&](int j, uint32_t &e, uint32_t &g) {
-        e = sv[j * stride];
-        if (!PACK) g = sf[j * stride];
-    };
-    auto decode = [&](uint32_t e, uint32_t g, int &v, A &f) {
+    auto get = [&](int j, int &v, A &f) {
+        uint32_t e = sv[j * stride];
         if (PACK) {
             v = int(e & vmask);
             f = A(e >> a.vbits);
         } else {
             v = int(e);
-            f = A(__builtin_bit_cast(S, g));
+            f = A(__builtin_bit_cast(S, sf[j * stride]));
         }
     };
     auto is_site = [](S f) {
@@ -139,55 +131,44 @@ __global__ void __launch_bounds__(64) k_fh_field(FieldArgs a) {
     };
 
     // ---- build the lower envelope -------------------------------------
-    // Registers cache the top entries: (v0, k0) the top, (v1, k1) the one
-    // below, (v2, f2) the third; k = g + w v^2.  (zn, zd) is the breakpoint of
-    // the top against the entry below.  After a pop the new third entry is
-    // fetched from LDS into (e2, g2) and decoded only at the next pop, so a
-    // single pop never waits for LDS.  Line values are prefetched PF rows
-    // ahead into a rotating register buffer with clamped (always in-bounds)
-    // addresses, so each load is waited for only when it is consumed.
+    // (vt, kt) is the top entry, (vb, kb) the one below, k = g + w v^2;
+    // (zn, zd) is the breakpoint between them.  Rows are read PF at a time.
     int top = 0;
-    int v0 = 0, v1 = 0, v2 = 0;
-    A f0 = 0, f1 = 0, f2 = 0;
-    A k0 = 0, k1 = 0;
+    int vt = 0, vb = 0;
+    A kt = 0, kb = 0;
     A zn = 0, zd = 1;
-    uint32_t e2 = 0, g2 = 0;
-    bool third_raw = false;  // entry top-3 sits in (e2, g2) rather than (v2, f2)
-    constexpr int PF = TM_FH_PREFETCH;
-    const int last = n - 1;
-    S buf[PF];
+    constexpr int PF = 8;
+    S cur[PF], nxt[PF];
 #pragma unroll
-    for (int j = 0; j < PF; ++j) buf[j] = line[uint64_t(min(j, last)) * inner];
+    for (int j = 0; j < PF; ++j) cur[j] = j < n ? line[uint64_t(j) * inner] : S(0);
     for (int q0 = 0; q0 < n; q0 += PF) {
 #pragma unroll
         for (int j = 0; j < PF; ++j) {
+            int q = q0 + PF + j;
+            nxt[j] = q < n ? line[uint64_t(q) * inner] : S(0);
+        }
+#pragma unroll
+        for (int j = 0; j < PF; ++j) {
             const int q = q0 + j;
-            const S fq = buf[j];
-            buf[j] = line[uint64_t(min(q + PF, last)) * inner];
-            if (q >= n || !is_site(fq)) continue;
+            if (q >= n) break;
+            const S fq = cur[j];
+            if (!is_site(fq)) continue;
             const A kq = A(fq) + W * M::mul(A(q), A(q));
             A num = 0, den = 1;
             while (top > 0) {
-                num = kq - k0;
-                den = A(2) * W * A(q - v0);
+                num = kq - kt;
+                den = A(2) * W * A(q - vt);
                 if (top >= 2 && M::mul(num, zd) <= M::mul(zn, den)) {
                     // the top parabola is nowhere strictly lowest: drop it
                     --top;
-                    v0 = v1;
-                    f0 = f1;
-                    k0 = k1;
+                    vt = vb;
+                    kt = kb;
                     if (top >= 2) {
-                        if (third_raw) {
-                            decode(e2, g2, v1, f1);
-                        } else {
-                            v1 = v2;
-                            f1 = f2;
-                        }
-                        k1 = f1 + W * M::mul(A(v1), A(v1));
-                        zn = k0 - k1;
-                        zd = A(2) * W * A(v0 - v1);
-                        third_raw = top >= 3;
-                        if (third_raw) raw(top - 3, e2, g2);
+                        A fb;
+                        get(top - 2, vb, fb);
+                        kb = fb + W * M::mul(A(vb), A(vb));
+                        zn = kt - kb;
+                        zd = A(2) * W * A(vt - vb);
                     }
                     continue;
                 }
@@ -195,20 +176,17 @@ __global__ void __launch_bounds__(64) k_fh_field(FieldArgs a) {
             }
             put(top, q, fq);
             if (top >= 1) {
-                v2 = v1;
-                f2 = f1;
-                third_raw = false;
-                v1 = v0;
-                f1 = f0;
-                k1 = k0;
+                vb = vt;
+                kb = kt;
                 zn = num;
                 zd = den;
             }
-            v0 = q;
-            f0 = A(fq);
-            k0 = kq;
+            vt = q;
+            kt = kq;
             ++top;
         }
+#pragma unroll
+        for (int j = 0; j < PF; ++j) cur[j] = nxt[j];
     }
 
     // ---- query every position ------------------------------------------
@@ -232,23 +210,17 @@ __global__ void __launch_bounds__(64) k_fh_field(FieldArgs a) {
         }
         return;
     }
-    // Entry k is current, k + 1 is decoded in registers, k + 2 is in flight.
     int k = 0;
     int vc, vn = 0;
     A fc, fn = 0;
-    uint32_t e, g = 0;
-    raw(0, e, g);
-    decode(e, g, vc, fc);
+    get(0, vc, fc);
     A kc = fc + W * M::mul(A(vc), A(vc)), kn = 0;
     A bn = 0, bd = 1;  // breakpoint between entries k and k + 1
-    uint32_t ep = 0, gp = 0;
     if (top > 1) {
-        raw(1, e, g);
-        decode(e, g, vn, fn);
+        get(1, vn, fn);
         kn = fn + W * M::mul(A(vn), A(vn));
         bn = kn - kc;
         bd = A(2) * W * A(vn - vc);
-        if (top > 2) raw(2, ep, gp);
     }
     for (int q = 0; q < n; ++q) {
         while (k + 1 < top && bn < M::mul(A(q), bd)) {
@@ -257,11 +229,10 @@ __global__ void __launch_bounds__(64) k_fh_field(FieldArgs a) {
             fc = fn;
             kc = kn;
             if (k + 1 < top) {
-                decode(ep, gp, vn, fn);
+                get(k + 1, vn, fn);
                 kn = fn + W * M::mul(A(vn), A(vn));
                 bn = kn - kc;
                 bd = A(2) * W * A(vn - vc);
-                if (k + 2 < top) raw(k + 2, ep, gp);
             }
         }
         const A d = A(q - vc);
@@ -720,12 +691,45 @@ namespace tmedt {
 // offset an immediate.  The fallback keeps its envelope stack (apex per
 // level) in the guard rows, which the search no longer needs.
 // ---------------------------------------------------------------------------
+// Buffer resource over `bytes` bytes from `p` (gfx9 raw-buffer descriptor):
+// loads past the end read 0 and stores past it are dropped.
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void *p, uint64_t bytes) {
+    const int32_t n = bytes >= 0xffffffffull ? int32_t(0xffffffff) : int32_t(bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, n, 0x00020000);
+}
+
 constexpr int kCap16 = 64;                 // search steps before the fallback
 constexpr int kGuard16 = kCap16 + 4;       // minimum guard rows per side
 constexpr int32_t kNone16 = 0xffff;
 
+// Search blocks BLK .. NBLK-1 (four steps each) of one element of a u16
+// tile, unrolled at compile time: dn points at the element's row, up at the
+// row kGuard16 above it, both with a row stride of kWave.  Returns with
+// `dnext` = the first distance not examined.  Ends early once every lane of
+// the wave has stopped (best below the next squared distance).
+template <int BLK, int NBLK>
+__device__ __forceinline__ void search16(const uint16_t *up, const uint16_t *dn, int32_t &best,
+                                         int &dnext) {
+    if constexpr (BLK < NBLK) {
+        constexpr int d = 1 + 4 * BLK;
+        if (__all(best < d * d)) return;
+        const int32_t u0 = up[(kGuard16 - d) * kWave], u1 = up[(kGuard16 - d - 1) * kWave];
+        const int32_t u2 = up[(kGuard16 - d - 2) * kWave], u3 = up[(kGuard16 - d - 3) * kWave];
+        const int32_t w0 = dn[d * kWave], w1 = dn[(d + 1) * kWave];
+        const int32_t w2 = dn[(d + 2) * kWave], w3 = dn[(d + 3) * kWave];
+        const int32_t c0 = min(u0, w0) + d * d;
+        const int32_t c1 = min(u1, w1) + (d + 1) * (d + 1);
+        const int32_t c2 = min(u2, w2) + (d + 2) * (d + 2);
+        const int32_t c3 = min(u3, w3) + (d + 3) * (d + 3);
+        best = min(min(best, min(c0, c1)), min(c2, c3));
+        dnext = d + 4;
+        search16<BLK + 1, NBLK>(up, dn, best, dnext);
+    }
+}
+
 struct Tile16Args {
     int32_t *buf;         // int32 squared distances, batch-flat, in place
+    uint64_t total;       // elements of buf
     uint64_t lines;
     uint32_t n;
     uint32_t inner;
@@ -756,7 +760,16 @@ __global__ void __launch_bounds__(kWave * kTileWaves) k_tile16(Tile16Args a) {
         i = L - o * inner;
     }
     const uint64_t base = o * uint64_t(n) * inner + i;
-    const int32_t *src = a.buf + (live ? base : 0);
+    // Global accesses go through buffer resources based at the workgroup's
+    // first line: a per-lane byte offset that never changes plus a scalar
+    // row offset (the host keeps both below 2^32).
+    const uint64_t L0 = uint64_t(blockIdx.x) * kWave;
+    const uint64_t o0 = L0 / inner;
+    const uint64_t wg_base = o0 * uint64_t(n) * inner + (L0 - o0 * inner);
+    const uint64_t span = (a.total - wg_base) * 4;
+    const uint32_t voff = live ? uint32_t((base - wg_base) * 4) : 0u;
+    const uint32_t row_bytes = uint32_t(inner * 4);
+    const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.buf + wg_base, span);
     uint16_t *row0 = t16 + G * kWave;      // row 0 of the line
 
     if (t == 0) hard = 0;
@@ -777,7 +790,7 @@ __global__ void __launch_bounds__(kWave * kTileWaves) k_tile16(Tile16Args a) {
 #pragma unroll
         for (int j = 0; j < SB; ++j) {
             const int q = min(q0 + j * kTileWaves, n - 1);
-            v[j] = src[uint64_t(q) * inner];
+            v[j] = int32_t(__builtin_amdgcn_raw_buffer_load_b32(rb, voff, uint32_t(q) * row_bytes, 0));
         }
 #pragma unroll
         for (int j = 0; j < SB; ++j) {
@@ -795,56 +808,65 @@ __global__ void __launch_bounds__(kWave * kTileWaves) k_tile16(Tile16Args a) {
 #pragma unroll
     for (int w = 0; w < kTileWaves; ++w) has_site |= any_site[w][lane] != 0;
 
-    int32_t *out_i = a.buf + base;
+    __amdgpu_buffer_rsrc_t rd = rb, rs = rb;
+    if (FINAL) {
+        rd = make_rsrc(a.dist ? reinterpret_cast<const int32_t *>(a.dist) + wg_base : nullptr,
+                       a.dist ? span : 0);
+        rs = make_rsrc(a.sq ? a.sq + wg_base : nullptr, a.sq ? span : 0);
+    }
     auto emit = [&](int q, int32_t d2, bool none) {
-        const uint64_t off = uint64_t(q) * inner;
+        const uint32_t soff = uint32_t(q) * row_bytes;
         if (!FINAL) {
-            out_i[off] = none ? kInfI : d2;
+            __builtin_amdgcn_raw_buffer_store_b32(uint32_t(none ? kInfI : d2), rb, voff, soff, 0);
         } else {
-            const uint64_t g = base + off;
+            float df;
+            int32_t dq;
             if (none) {
                 const int64_t v = virtual_sq<int64_t>(q, uint32_t(i), a.ndim, a.shape, a.wall);
-                if (a.dist) a.dist[g] = float(sqrt(double(v)));
-                if (a.sq) a.sq[g] = int32_t(v);
+                df = float(sqrt(double(v)));
+                dq = int32_t(v);
             } else {
                 // d2 < 2^24 converts exactly; sqrtf is correctly rounded
-                if (a.dist) a.dist[g] = sqrtf(float(d2));
-                if (a.sq) a.sq[g] = d2;
+                df = sqrtf(float(d2));
+                dq = d2;
             }
+            if (a.dist) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, df), rd, voff, soff, 0);
+            if (a.sq) __builtin_amdgcn_raw_buffer_store_b32(uint32_t(dq), rs, voff, soff, 0);
         }
     };
 
     // ---- windowed exact search, unrolled -----------------------------------
+    // Rows are taken RB at a time and their results stored together after the
+    // searches, so no search waits on the store of the row before it.
     bool mine_hard = false;
-    for (int q = wv; q < n; q += kTileWaves) {
+    constexpr int RB = 4;
+    for (int q0 = wv; q0 < n; q0 += kTileWaves * RB) {
         if (!live) break;
         if (!has_site) {
-            emit(q, 0, true);
+            for (int j = 0; j < RB; ++j)
+                if (q0 + kTileWaves * j < n) emit(q0 + kTileWaves * j, 0, true);
             continue;
         }
-        const uint16_t *dn = row0 + q * kWave + lane;        // rows q + d at +d*kWave
-        const uint16_t *up = dn - kGuard16 * kWave;          // rows q - d at (kGuard16 - d)*kWave
-        int32_t best = dn[0];
-        int dnext = 1;
+        int32_t res[RB];
+        bool ok[RB];
 #pragma unroll
-        for (int blk = 0; blk < kCap16 / 4; ++blk) {
-            const int d = 1 + 4 * blk;
-            if (__all(best < d * d)) break;
-            const int32_t u0 = up[(kGuard16 - d) * kWave], u1 = up[(kGuard16 - d - 1) * kWave];
-            const int32_t u2 = up[(kGuard16 - d - 2) * kWave], u3 = up[(kGuard16 - d - 3) * kWave];
-            const int32_t w0 = dn[d * kWave], w1 = dn[(d + 1) * kWave];
-            const int32_t w2 = dn[(d + 2) * kWave], w3 = dn[(d + 3) * kWave];
-            const int32_t c0 = min(u0, w0) + d * d;
-            const int32_t c1 = min(u1, w1) + (d + 1) * (d + 1);
-            const int32_t c2 = min(u2, w2) + (d + 2) * (d + 2);
-            const int32_t c3 = min(u3, w3) + (d + 3) * (d + 3);
-            best = min(min(best, min(c0, c1)), min(c2, c3));
-            dnext = d + 4;
+        for (int j = 0; j < RB; ++j) {
+            const int q = min(q0 + kTileWaves * j, n - 1);         // uniform
+            const uint16_t *dn = row0 + q * kWave + lane;        // rows q + d at +d*kWave
+            const uint16_t *up = dn - kGuard16 * kWave;          // rows q - d at (kGuard16 - d)*kWave
+            int32_t best = dn[0];
+            int dnext = 1;
+            search16<0, kCap16 / 4>(up, dn, best, dnext);
+            res[j] = best;
+            ok[j] = best < dnext * dnext;
         }
-        if (best >= dnext * dnext) {
-            mine_hard = true;
-        } else {
-            emit(q, best, false);
+#pragma unroll
+        for (int j = 0; j < RB; ++j) {
+            const int q = q0 + kTileWaves * j;
+            if (q < n) {
+                if (ok[j]) emit(q, res[j], false);
+                else mine_hard = true;
+            }
         }
     }
     if (mine_hard) hard = 1;

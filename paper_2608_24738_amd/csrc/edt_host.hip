@@ -215,8 +215,13 @@ int run(Request &r) {
             // 16-bit tile: values and the search reach below the "no site" code
             const uint32_t g16 = uint32_t(kGuard16) > (n + 1) / 2 ? uint32_t(kGuard16) : (n + 1) / 2;
             const size_t t16 = size_t(n + 2 * g16) * kWave * 2;
+            uint64_t inner = 1;
+            for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
+            // byte offsets within a workgroup's buffer view stay below 2^31
+            const bool offsets_fit = (uint64_t(n) * inner * 2 + uint64_t(n) * kWave) * 4 < (uint64_t(1) << 31);
             if (fmax + uint64_t(kCap16 + 3) * (kCap16 + 3) < uint64_t(kNone16) &&
-                fmax + uint64_t(n - 1) * (n - 1) < (uint64_t(1) << 30) && t16 + 2048 <= kLdsBytes) {
+                fmax + uint64_t(n - 1) * (n - 1) < (uint64_t(1) << 30) && t16 + 2048 <= kLdsBytes &&
+                offsets_fit) {
                 p.tiled16 = true;
                 p.guard = g16;
                 p.lds = t16;
@@ -324,6 +329,7 @@ int run(Request &r) {
         if (p.tiled16) {
             Tile16Args tg{};
             tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
+            tg.total = total;
             tg.lines = lines;
             tg.n = n;
             tg.inner = uint32_t(inner);
