@@ -46,9 +46,9 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
     pass reads the field and writes the outputs."""
     if name.startswith("scan"):
         return total * (1 + 4)
-    if name in ("fh_field", "tile_field", "tile16"):
+    if name in ("fh_field", "tile_field", "tile_pair"):
         return total * (4 + 4)
-    if name in ("fh_field_final", "tile_field_final", "tile16_final"):
+    if name in ("fh_field_final", "tile_field_final", "tile_pair_final"):
         return total * (4 + out_bytes)
     if name == "fh_index":
         return total * (4 + 4)

@@ -683,14 +683,27 @@ __global__ void __launch_bounds__(kWave * kTileWaves) k_tile_field(TileArgs a) {
 namespace tmedt {
 
 // ---------------------------------------------------------------------------
-// 16-bit tiled pass: as k_tile_field, for passes whose values (plus the
-// squared search reach) fit in 16 bits.  The tile holds u16 values with G
-// guard rows of "no site" (0xffff) above and below the line, so every read of
-// the search is in bounds without a test; the search is unrolled in blocks of
-// four steps, which makes every squared distance a literal and every LDS
-// offset an immediate.  The fallback keeps its envelope stack (apex per
-// level) in the guard rows, which the search no longer needs.
+// Paired 16-bit tiled pass: for passes whose values plus the squared search
+// reach fit in 16 bits.  A workgroup owns 128 adjacent lines; lane l of each
+// wave holds lines 2l and 2l+1 packed in one 32-bit tile word, so one LDS
+// read fetches a row for both lines and packed 16-bit min / saturating add
+// (v_pk_min_u16, v_pk_add_u16 clamp) process both at once.  kGuard16 rows of
+// "no site" (0xffff) above and below the line make the first kCap16 steps
+// of every search read in bounds without a test, unrolled in blocks of four
+// with literal squared distances and immediate LDS offsets.  Searches that
+// need more steps continue with the row index clamped into the guard rows
+// (every row beyond the line is "no site" anyway), so the result is exact for
+// any input; only sparse inputs pay for the longer searches.
 // ---------------------------------------------------------------------------
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kCap16 = 16;                 // unrolled search steps
+constexpr int kReach16 = kCap16 + 3;       // farthest row the unrolled part reads
+constexpr int kGuard16 = kCap16 + 4;       // guard rows per side
+constexpr int32_t kNone16 = 0xffff;
+constexpr int kPairWaves = 8;              // waves per workgroup
+constexpr int kPairLines = 2 * kWave;      // lines per workgroup
+
 // Buffer resource over `bytes` bytes from `p` (gfx9 raw-buffer descriptor):
 // loads past the end read 0 and stores past it are dropped.
 __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void *p, uint64_t bytes) {
@@ -698,42 +711,50 @@ __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void *p, uint64_t bytes
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, n, 0x00020000);
 }
 
-constexpr int kCap16 = 64;                 // search steps before the fallback
-constexpr int kGuard16 = kCap16 + 4;       // minimum guard rows per side
-constexpr int32_t kNone16 = 0xffff;
+__device__ __forceinline__ u16x2 as_pair(uint32_t v) { return __builtin_bit_cast(u16x2, v); }
+__device__ __forceinline__ uint32_t as_word(u16x2 v) { return __builtin_bit_cast(uint32_t, v); }
+__device__ __forceinline__ u16x2 splat(int v) { return u16x2{uint16_t(v), uint16_t(v)}; }
+// true when both halves are below d^2 (the search of both lines has stopped)
+__device__ __forceinline__ bool stopped(u16x2 best, int d) {
+    const int lim = d * d - 1 < kNone16 ? d * d - 1 : kNone16;
+    return as_word(__builtin_elementwise_sub_sat(best, splat(lim))) == 0;
+}
 
-// Search blocks BLK .. NBLK-1 (four steps each) of one element of a u16
-// tile, unrolled at compile time: dn points at the element's row, up at the
-// row kGuard16 above it, both with a row stride of kWave.  Returns with
-// `dnext` = the first distance not examined.  Ends early once every lane of
-// the wave has stopped (best below the next squared distance).
+// Search blocks BLK .. NBLK-1 (four steps each) for both lines of a lane,
+// unrolled at compile time.  `b` points at the word of row (element row -
+// kReach16), row stride kWave words.  Leaves `dnext` = the first distance not
+// examined; ends early once both lines of every lane have stopped.
 template <int BLK, int NBLK>
-__device__ __forceinline__ void search16(const uint16_t *up, const uint16_t *dn, int32_t &best,
-                                         int &dnext) {
+__device__ __forceinline__ void search_pair(const uint32_t *b, u16x2 &best, int &dnext) {
     if constexpr (BLK < NBLK) {
         constexpr int d = 1 + 4 * BLK;
-        if (__all(best < d * d)) return;
-        const int32_t u0 = up[(kGuard16 - d) * kWave], u1 = up[(kGuard16 - d - 1) * kWave];
-        const int32_t u2 = up[(kGuard16 - d - 2) * kWave], u3 = up[(kGuard16 - d - 3) * kWave];
-        const int32_t w0 = dn[d * kWave], w1 = dn[(d + 1) * kWave];
-        const int32_t w2 = dn[(d + 2) * kWave], w3 = dn[(d + 3) * kWave];
-        const int32_t c0 = min(u0, w0) + d * d;
-        const int32_t c1 = min(u1, w1) + (d + 1) * (d + 1);
-        const int32_t c2 = min(u2, w2) + (d + 2) * (d + 2);
-        const int32_t c3 = min(u3, w3) + (d + 3) * (d + 3);
-        best = min(min(best, min(c0, c1)), min(c2, c3));
+        constexpr int R = kReach16;
+        if (__all(stopped(best, d))) return;
+        const u16x2 u0 = as_pair(b[(R - d) * kWave]), u1 = as_pair(b[(R - d - 1) * kWave]);
+        const u16x2 u2 = as_pair(b[(R - d - 2) * kWave]), u3 = as_pair(b[(R - d - 3) * kWave]);
+        const u16x2 w0 = as_pair(b[(R + d) * kWave]), w1 = as_pair(b[(R + d + 1) * kWave]);
+        const u16x2 w2 = as_pair(b[(R + d + 2) * kWave]), w3 = as_pair(b[(R + d + 3) * kWave]);
+        const u16x2 c0 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u0, w0), splat(d * d));
+        const u16x2 c1 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u1, w1),
+                                                       splat((d + 1) * (d + 1)));
+        const u16x2 c2 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u2, w2),
+                                                       splat((d + 2) * (d + 2)));
+        const u16x2 c3 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u3, w3),
+                                                       splat((d + 3) * (d + 3)));
+        best = __builtin_elementwise_min(
+            best, __builtin_elementwise_min(__builtin_elementwise_min(c0, c1),
+                                            __builtin_elementwise_min(c2, c3)));
         dnext = d + 4;
-        search16<BLK + 1, NBLK>(up, dn, best, dnext);
+        search_pair<BLK + 1, NBLK>(b, best, dnext);
     }
 }
 
-struct Tile16Args {
+struct PairArgs {
     int32_t *buf;         // int32 squared distances, batch-flat, in place
     uint64_t total;       // elements of buf
     uint64_t lines;
     uint32_t n;
     uint32_t inner;
-    uint32_t guard;       // guard rows per side: >= kGuard16 and 2 * guard >= n
     float *dist;          // final pass outputs
     int32_t *sq;
     int32_t ndim;
@@ -742,79 +763,79 @@ struct Tile16Args {
 };
 
 template <bool FINAL>
-__global__ void __launch_bounds__(kWave * kTileWaves) k_tile16(Tile16Args a) {
-    extern __shared__ uint16_t t16[];      // rows [-guard, n + guard) x kWave
-    __shared__ int hard;
-    __shared__ uint32_t any_site[kTileWaves][kWave];
+__global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
+    extern __shared__ uint32_t tw[];       // rows [-kGuard16, n + kGuard16) x kWave words
+    __shared__ uint8_t any_site[kPairWaves][kWave];
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
     const int n = int(a.n);
-    const int G = int(a.guard);
-    const uint64_t L = uint64_t(blockIdx.x) * kWave + lane;
-    const bool live = L < a.lines;
     const uint64_t inner = a.inner;
-    uint64_t o = 0, i = 0;
-    if (live) {
-        o = L / inner;
-        i = L - o * inner;
-    }
-    const uint64_t base = o * uint64_t(n) * inner + i;
-    // Global accesses go through buffer resources based at the workgroup's
-    // first line: a per-lane byte offset that never changes plus a scalar
-    // row offset (the host keeps both below 2^32).
-    const uint64_t L0 = uint64_t(blockIdx.x) * kWave;
+    const uint64_t L0 = uint64_t(blockIdx.x) * kPairLines;
     const uint64_t o0 = L0 / inner;
     const uint64_t wg_base = o0 * uint64_t(n) * inner + (L0 - o0 * inner);
     const uint64_t span = (a.total - wg_base) * 4;
-    const uint32_t voff = live ? uint32_t((base - wg_base) * 4) : 0u;
     const uint32_t row_bytes = uint32_t(inner * 4);
     const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.buf + wg_base, span);
-    uint16_t *row0 = t16 + G * kWave;      // row 0 of the line
-
-    if (t == 0) hard = 0;
-    // guard rows: "no site", written as 32-bit pairs
-    {
-        uint32_t *g32 = reinterpret_cast<uint32_t *>(t16);
-        const int half = G * kWave / 2;    // u32 words per guard block
-        uint32_t *g2 = reinterpret_cast<uint32_t *>(t16 + (G + n) * kWave);
-        for (int k = t; k < half; k += kWave * kTileWaves) {
-            g32[k] = 0xffffffffu;
-            g2[k] = 0xffffffffu;
-        }
-    }
-    uint32_t seen = 0;
-    constexpr int SB = 8;
-    for (int q0 = wv; q0 < n; q0 += kTileWaves * SB) {
-        int32_t v[SB];
-#pragma unroll
-        for (int j = 0; j < SB; ++j) {
-            const int q = min(q0 + j * kTileWaves, n - 1);
-            v[j] = int32_t(__builtin_amdgcn_raw_buffer_load_b32(rb, voff, uint32_t(q) * row_bytes, 0));
-        }
-#pragma unroll
-        for (int j = 0; j < SB; ++j) {
-            const int q = q0 + j * kTileWaves;
-            if (q < n) {
-                const int32_t f = (!live || v[j] == kInfI) ? kNone16 : v[j];
-                seen |= f != kNone16;
-                row0[q * kWave + lane] = uint16_t(f);
-            }
-        }
-    }
-    any_site[wv][lane] = seen;
-    __syncthreads();
-    bool has_site = false;
-#pragma unroll
-    for (int w = 0; w < kTileWaves; ++w) has_site |= any_site[w][lane] != 0;
-
     __amdgpu_buffer_rsrc_t rd = rb, rs = rb;
     if (FINAL) {
         rd = make_rsrc(a.dist ? reinterpret_cast<const int32_t *>(a.dist) + wg_base : nullptr,
                        a.dist ? span : 0);
         rs = make_rsrc(a.sq ? a.sq + wg_base : nullptr, a.sq ? span : 0);
     }
-    auto emit = [&](int q, int32_t d2, bool none) {
+    // Line j of the workgroup: liveness, position along the later axes, and
+    // byte offset of its row 0 in the workgroup's buffer view.
+    auto locate = [&](int j, bool &live, uint32_t &ipos, uint32_t &voff) {
+        const uint64_t L = L0 + j;
+        live = L < a.lines;
+        const uint64_t o = live ? L / inner : o0;
+        const uint64_t i = live ? L - o * inner : 0;
+        ipos = uint32_t(i);
+        voff = live ? uint32_t((o * uint64_t(n) * inner + i - wg_base) * 4) : 0u;
+    };
+    bool live_a, live_b;
+    uint32_t i_a, i_b, voff_a, voff_b;
+    locate(2 * lane, live_a, i_a, voff_a);
+    locate(2 * lane + 1, live_b, i_b, voff_b);
+    uint32_t *row0 = tw + kGuard16 * kWave;   // row 0 of the lines
+
+    for (int k = t; k < kGuard16 * kWave; k += kWave * kPairWaves) {
+        tw[k] = 0xffffffffu;
+        row0[(n * kWave) + k] = 0xffffffffu;
+    }
+    // Stage: wave wv reads rows wv, wv + 8, ...; SB rows are in flight at once.
+    uint32_t seen = 0;
+    constexpr int SB = 8;
+    for (int q0 = wv; q0 < n; q0 += kPairWaves * SB) {
+        uint32_t va[SB], vb[SB];
+#pragma unroll
+        for (int j = 0; j < SB; ++j) {
+            const uint32_t so = uint32_t(min(q0 + j * kPairWaves, n - 1)) * row_bytes;
+            va[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_a, so, 0);
+            vb[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_b, so, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < SB; ++j) {
+            const int q = q0 + j * kPairWaves;
+            if (q < n) {
+                const uint32_t fa = (!live_a || va[j] == uint32_t(kInfI)) ? kNone16 : va[j];
+                const uint32_t fb = (!live_b || vb[j] == uint32_t(kInfI)) ? kNone16 : vb[j];
+                seen |= (fa != kNone16 ? 1u : 0u) | (fb != kNone16 ? 2u : 0u);
+                row0[q * kWave + lane] = fa | (fb << 16);
+            }
+        }
+    }
+    any_site[wv][lane] = uint8_t(seen);
+    __syncthreads();
+    uint32_t has = 0;
+#pragma unroll
+    for (int w = 0; w < kPairWaves; ++w) has |= any_site[w][lane];
+    // Halves whose line is absent or has no site need no search: clearing
+    // them keeps them from holding the wave's stop vote open.
+    const uint32_t searched = ((live_a && (has & 1u)) ? 0xffffu : 0u) |
+                              ((live_b && (has & 2u)) ? 0xffff0000u : 0u);
+
+    auto emit = [&](uint32_t voff, uint32_t ipos, int q, int32_t d2, bool none) {
         const uint32_t soff = uint32_t(q) * row_bytes;
         if (!FINAL) {
             __builtin_amdgcn_raw_buffer_store_b32(uint32_t(none ? kInfI : d2), rb, voff, soff, 0);
@@ -822,7 +843,7 @@ __global__ void __launch_bounds__(kWave * kTileWaves) k_tile16(Tile16Args a) {
             float df;
             int32_t dq;
             if (none) {
-                const int64_t v = virtual_sq<int64_t>(q, uint32_t(i), a.ndim, a.shape, a.wall);
+                const int64_t v = virtual_sq<int64_t>(q, ipos, a.ndim, a.shape, a.wall);
                 df = float(sqrt(double(v)));
                 dq = int32_t(v);
             } else {
@@ -835,108 +856,43 @@ __global__ void __launch_bounds__(kWave * kTileWaves) k_tile16(Tile16Args a) {
         }
     };
 
-    // ---- windowed exact search, unrolled -----------------------------------
-    // Rows are taken RB at a time and their results stored together after the
-    // searches, so no search waits on the store of the row before it.
-    bool mine_hard = false;
+    // ---- windowed exact search -------------------------------------------
+    // Rows are taken RB at a time and stored together after their searches.
     constexpr int RB = 4;
-    for (int q0 = wv; q0 < n; q0 += kTileWaves * RB) {
-        if (!live) break;
-        if (!has_site) {
-            for (int j = 0; j < RB; ++j)
-                if (q0 + kTileWaves * j < n) emit(q0 + kTileWaves * j, 0, true);
-            continue;
-        }
-        int32_t res[RB];
-        bool ok[RB];
+    for (int q0 = wv; q0 < n; q0 += kPairWaves * RB) {
+        u16x2 res[RB];
 #pragma unroll
         for (int j = 0; j < RB; ++j) {
-            const int q = min(q0 + kTileWaves * j, n - 1);         // uniform
-            const uint16_t *dn = row0 + q * kWave + lane;        // rows q + d at +d*kWave
-            const uint16_t *up = dn - kGuard16 * kWave;          // rows q - d at (kGuard16 - d)*kWave
-            int32_t best = dn[0];
-            int dnext = 1;
-            search16<0, kCap16 / 4>(up, dn, best, dnext);
-            res[j] = best;
-            ok[j] = best < dnext * dnext;
-        }
+            const int q = min(q0 + kPairWaves * j, n - 1);
+            // base row q - kReach16 (inside the guard rows)
+            const uint32_t *bp = row0 + (q - kReach16) * kWave + lane;
+            u16x2 best = as_pair(bp[kReach16 * kWave] & searched);
+            int d = 1;
+            search_pair<0, kCap16 / 4>(bp, best, d);
+            // Longer searches: row indices clamp into the guard rows.
+            while (!__all(stopped(best, d))) {
 #pragma unroll
-        for (int j = 0; j < RB; ++j) {
-            const int q = q0 + kTileWaves * j;
-            if (q < n) {
-                if (ok[j]) emit(q, res[j], false);
-                else mine_hard = true;
-            }
-        }
-    }
-    if (mine_hard) hard = 1;
-    __syncthreads();
-    if (!hard || wv != 0 || !live || !has_site) return;
-
-    // ---- fallback: sequential lower envelope from the LDS copy --------------
-    // Stack level j keeps its apex in guard row j (top guard block first, then
-    // the bottom one); 2 * guard >= n levels are available.
-    auto val = [&](int p) { return int32_t(row0[p * kWave + lane]); };
-    auto slot = [&](int j) -> uint16_t & {
-        return j < G ? t16[j * kWave + lane] : t16[(n + j) * kWave + lane];
-    };
-    int top = 0, vt = 0, vb = 0;
-    int32_t kt = 0, kb = 0, zn = 0, zd = 1;
-    for (int q = 0; q < n; ++q) {
-        const int32_t fq = val(q);
-        if (fq == kNone16) continue;
-        const int32_t kq = fq + q * q;
-        int32_t num = 0, den = 1;
-        while (top > 0) {
-            num = kq - kt;
-            den = 2 * (q - vt);
-            if (top >= 2 && int64_t(num) * zd <= int64_t(zn) * den) {
-                --top;
-                vt = vb;
-                kt = kb;
-                if (top >= 2) {
-                    vb = slot(top - 2);
-                    kb = val(vb) + vb * vb;
-                    zn = kt - kb;
-                    zd = 2 * (vt - vb);
+                for (int s = 0; s < 4; ++s) {
+                    const int dd = d + s;
+                    const int lo = max(q - dd, -kGuard16), hi = min(q + dd, n + kGuard16 - 1);
+                    const u16x2 u = as_pair(row0[lo * kWave + lane]);
+                    const u16x2 w = as_pair(row0[hi * kWave + lane]);
+                    best = __builtin_elementwise_min(
+                        best, __builtin_elementwise_add_sat(__builtin_elementwise_min(u, w),
+                                                            splat(dd * dd >= kNone16 ? kNone16 : dd * dd)));
                 }
-                continue;
+                d += 4;
+                if (d > n + 4) break;   // every row has been examined
             }
-            break;
+            res[j] = best;
         }
-        slot(top) = uint16_t(q);
-        if (top >= 1) {
-            vb = vt;
-            kb = kt;
-            zn = num;
-            zd = den;
+#pragma unroll
+        for (int j = 0; j < RB; ++j) {
+            const int q = q0 + kPairWaves * j;
+            if (q >= n) continue;
+            if (live_a) emit(voff_a, i_a, q, int32_t(res[j].x), !(has & 1u));
+            if (live_b) emit(voff_b, i_b, q, int32_t(res[j].y), !(has & 2u));
         }
-        vt = q;
-        kt = kq;
-        ++top;
-    }
-    int k = 0;
-    int vc = slot(0), vn = 0;
-    int32_t kc = val(vc) + vc * vc, kn = 0, bn = 0, bd = 1;
-    if (top > 1) {
-        vn = slot(1);
-        kn = val(vn) + vn * vn;
-        bn = kn - kc;
-        bd = 2 * (vn - vc);
-    }
-    for (int q = 0; q < n; ++q) {
-        while (k + 1 < top && int64_t(bn) < int64_t(q) * bd) {
-            ++k;
-            vc = vn;
-            kc = kn;
-            if (k + 1 < top) {
-                vn = slot(k + 1);
-                kn = val(vn) + vn * vn;
-                bn = kn - kc;
-                bd = 2 * (vn - vc);
-            }
-        }
-        emit(q, kc - vc * vc + (q - vc) * (q - vc), false);
     }
 }
 

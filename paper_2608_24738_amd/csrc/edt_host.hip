@@ -184,10 +184,9 @@ int run(Request &r) {
         int acc;  // 0 int32 with 24-bit multiplies, 1 int32, 2 int64, 3 double
         size_t lds;
         bool tiled;      // staged tile + windowed search (k_tile_field)
-        bool tiled16;    // 16-bit tile with guard rows (k_tile16)
+        bool tiled16;    // paired 16-bit tile with guard rows (k_tile_pair)
         uint32_t fbits;  // tiled: value bits of a tile word
         uint32_t cap;    // tiled: search steps before the envelope fallback
-        uint32_t guard;  // tiled16: guard rows per side
     } fh[kMaxDim] = {};
     for (int a = nd - 2; a >= 0; --a) {
         const uint32_t n = r.shape[a];
@@ -212,19 +211,19 @@ int run(Request &r) {
         // must exceed every real value plus the square of the farthest step
         // a search takes (cap + 3).
         if (!index_path && r.unit) {
-            // 16-bit tile: values and the search reach below the "no site" code
-            const uint32_t g16 = uint32_t(kGuard16) > (n + 1) / 2 ? uint32_t(kGuard16) : (n + 1) / 2;
-            const size_t t16 = size_t(n + 2 * g16) * kWave * 2;
+            // Paired 16-bit tile: every value plus the square of any distance
+            // within the line stays below the "no site" code, the tile (with
+            // guard rows) fits LDS, and byte offsets within a workgroup's
+            // buffer view stay below 2^31.
+            const size_t tp = size_t(n + 2 * kGuard16) * kWave * 4;
             uint64_t inner = 1;
             for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
-            // byte offsets within a workgroup's buffer view stay below 2^31
-            const bool offsets_fit = (uint64_t(n) * inner * 2 + uint64_t(n) * kWave) * 4 < (uint64_t(1) << 31);
-            if (fmax + uint64_t(kCap16 + 3) * (kCap16 + 3) < uint64_t(kNone16) &&
-                fmax + uint64_t(n - 1) * (n - 1) < (uint64_t(1) << 30) && t16 + 2048 <= kLdsBytes &&
+            const bool offsets_fit =
+                (uint64_t(n) * inner * 2 + uint64_t(n) * kPairLines) * 4 < (uint64_t(1) << 31);
+            if (fmax + uint64_t(n + 4) * (n + 4) < uint64_t(kNone16) && tp + 1024 <= kLdsBytes &&
                 offsets_fit) {
                 p.tiled16 = true;
-                p.guard = g16;
-                p.lds = t16;
+                p.lds = tp;
                 continue;
             }
         }
@@ -327,13 +326,12 @@ int run(Request &r) {
         const dim3 grid(uint32_t((lines + p.lpw - 1) / p.lpw)), block(kWave);
         const bool fin = a == 0;
         if (p.tiled16) {
-            Tile16Args tg{};
+            PairArgs tg{};
             tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
             tg.total = total;
             tg.lines = lines;
             tg.n = n;
             tg.inner = uint32_t(inner);
-            tg.guard = p.guard;
             tg.dist = r.dist;
             tg.sq = r.sq;
             tg.ndim = nd;
@@ -341,9 +339,9 @@ int run(Request &r) {
                 tg.shape[b] = r.shape[b];
                 tg.wall[b] = r.w[b];
             }
-            const dim3 tgrid(uint32_t((lines + kWave - 1) / kWave)), tblock(kWave * kTileWaves);
-            rc = fin ? launch("tile16_final", k_tile16<true>, tgrid, tblock, p.lds, r.stream, tg)
-                     : launch("tile16", k_tile16<false>, tgrid, tblock, p.lds, r.stream, tg);
+            const dim3 tgrid(uint32_t((lines + kPairLines - 1) / kPairLines)), tblock(kWave * kPairWaves);
+            rc = fin ? launch("tile_pair_final", k_tile_pair<true>, tgrid, tblock, p.lds, r.stream, tg)
+                     : launch("tile_pair", k_tile_pair<false>, tgrid, tblock, p.lds, r.stream, tg);
         } else if (p.tiled) {
             TileArgs tg{};
             tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
