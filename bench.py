@@ -46,6 +46,10 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
     pass reads the field and writes the outputs."""
     if name.startswith("scan"):
         return total * (1 + 4)
+    if name == "plane_pair":          # reads the mask, writes the field
+        return total * (1 + 4)
+    if name == "plane_pair_final":
+        return total * (1 + out_bytes)
     if name in ("fh_field", "tile_field", "tile_pair"):
         return total * (4 + 4)
     if name in ("fh_field_final", "tile_field_final", "tile_pair_final"):

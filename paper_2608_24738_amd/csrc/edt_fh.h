@@ -751,6 +751,8 @@ __device__ __forceinline__ void search_pair(const uint32_t *b, u16x2 &best, int 
 
 struct PairArgs {
     int32_t *buf;         // int32 squared distances, batch-flat, in place
+    const uint8_t *mask;  // FROM_MASK: the input mask; this pass runs along axis ndim-2
+    uint32_t n2;          // FROM_MASK: extent of the last axis (a multiple of 64)
     uint64_t total;       // elements of buf
     uint64_t lines;
     uint32_t n;
@@ -762,9 +764,18 @@ struct PairArgs {
     double wall[kMaxDim];
 };
 
-template <bool FINAL>
+// FROM_MASK: the pass along axis ndim-2 computes its own input, the
+// last-axis pass, from the mask.  The workgroup's 128 lines are columns of
+// one or more mask planes (the last two axes); it loads those planes with
+// 16-byte loads, turns every 16 bytes into a 16-bit zero mask in LDS (so each
+// mask row is a run of 64-bit words), notes per row and word the nearest zero
+// in the words before and after it, and gives each column its squared
+// distance to the nearest zero of its row from one shift and a leading- or
+// trailing-zero count.  This removes the last-axis kernel's write and this
+// pass's read of the intermediate.
+template <bool FINAL, bool FROM_MASK>
 __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
-    extern __shared__ uint32_t tw[];       // rows [-kGuard16, n + kGuard16) x kWave words
+    extern __shared__ __attribute__((aligned(16))) uint32_t tw[];  // rows [-kGuard16, n + kGuard16) x kWave words, then FROM_MASK data
     __shared__ uint8_t any_site[kPairWaves][kWave];
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
@@ -803,8 +814,83 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
         tw[k] = 0xffffffffu;
         row0[(n * kWave) + k] = 0xffffffffu;
     }
-    // Stage: wave wv reads rows wv, wv + 8, ...; SB rows are in flight at once.
     uint32_t seen = 0;
+    if constexpr (FROM_MASK) {
+        const uint32_t n2 = a.n2;
+        const int nw = int(n2 / 64);
+        const uint64_t p_first = L0 / n2;
+        const uint64_t last_line = min(L0 + kPairLines, a.lines) - 1;
+        const int planes = int(last_line / n2 - p_first) + 1;
+        const int rows = planes * n;                                  // mask rows held
+        uint16_t *zm16 = reinterpret_cast<uint16_t *>(tw + (n + 2 * kGuard16) * kWave);
+        const uint64_t *zm = reinterpret_cast<const uint64_t *>(zm16);  // [row][word]
+        int16_t *before = reinterpret_cast<int16_t *>(zm16 + rows * nw * 4);  // last zero before word, or -1
+        int16_t *after = before + rows * nw;                                  // first zero after word, or -1
+        // zero masks: 16 bytes -> 16 bits
+        const uint4 *src = reinterpret_cast<const uint4 *>(a.mask + p_first * uint64_t(n) * n2);
+        const int chunks = rows * int(n2 / 16);
+        constexpr int MB = 4;
+        for (int k0 = t; k0 < chunks; k0 += kWave * kPairWaves * MB) {
+            uint4 v[MB];
+#pragma unroll
+            for (int j = 0; j < MB; ++j) v[j] = src[min(k0 + j * kWave * kPairWaves, chunks - 1)];
+#pragma unroll
+            for (int j = 0; j < MB; ++j) {
+                const int k = k0 + j * kWave * kPairWaves;
+                if (k >= chunks) break;
+                const uint32_t d4[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+                uint32_t bits = 0;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const uint32_t x = d4[c];
+                    const uint32_t zb = ~(((x & 0x7f7f7f7fu) + 0x7f7f7f7fu) | x | 0x7f7f7f7fu);
+                    bits |= (((zb >> 7) & 1u) | ((zb >> 14) & 2u) | ((zb >> 21) & 4u) | ((zb >> 28) & 8u)) << (4 * c);
+                }
+                zm16[k] = uint16_t(bits);
+            }
+        }
+        __syncthreads();
+        // nearest zero in the words before / after each word of each row
+        for (int r = t; r < rows; r += kWave * kPairWaves) {
+            int last = -1;
+            for (int w = 0; w < nw; ++w) {
+                before[r * nw + w] = int16_t(last);
+                const uint64_t m = zm[r * nw + w];
+                if (m) last = w * 64 + 63 - __clzll(m);
+            }
+            int first = -1;
+            for (int w = nw - 1; w >= 0; --w) {
+                after[r * nw + w] = int16_t(first);
+                const uint64_t m = zm[r * nw + w];
+                if (m) first = w * 64 + __ffsll((unsigned long long)m) - 1;
+            }
+        }
+        __syncthreads();
+        // row distances of this lane's two columns, straight into the tile
+        const uint64_t La = min(L0 + 2 * lane, last_line), Lb = min(L0 + 2 * lane + 1, last_line);
+        const int pa = int(La / n2 - p_first), pb = int(Lb / n2 - p_first);
+        const int ca = int(La % n2), cb = int(Lb % n2);
+        auto rowdist = [&](int pl, int c, int q) -> uint32_t {
+            const int r = pl * n + q;
+            const int w = c >> 6, b = c & 63;
+            const uint64_t m = zm[r * nw + w];
+            const uint64_t ml = m << (63 - b);     // zeros at or before c, top bit = c
+            const uint64_t mr = m >> b;            // zeros at or after c, bit 0 = c
+            const int yl = ml ? c - int(__clzll(ml)) : int(before[r * nw + w]);
+            const int yr = mr ? c + __ffsll((unsigned long long)mr) - 1 : int(after[r * nw + w]);
+            int d = kNone16;
+            if (yl >= 0) d = c - yl;
+            if (yr >= 0 && yr - c < d) d = yr - c;
+            return d == kNone16 ? uint32_t(kNone16) : uint32_t(d * d);
+        };
+        for (int q = wv; q < n; q += kPairWaves) {
+            const uint32_t fa = live_a ? rowdist(pa, ca, q) : kNone16;
+            const uint32_t fb = live_b ? rowdist(pb, cb, q) : kNone16;
+            seen |= (fa != kNone16 ? 1u : 0u) | (fb != kNone16 ? 2u : 0u);
+            row0[q * kWave + lane] = fa | (fb << 16);
+        }
+    } else {
+    // Stage: wave wv reads rows wv, wv + 8, ...; SB rows are in flight at once.
     constexpr int SB = 8;
     for (int q0 = wv; q0 < n; q0 += kPairWaves * SB) {
         uint32_t va[SB], vb[SB];
@@ -824,6 +910,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
                 row0[q * kWave + lane] = fa | (fb << 16);
             }
         }
+    }
     }
     any_site[wv][lane] = uint8_t(seen);
     __syncthreads();

@@ -185,6 +185,7 @@ int run(Request &r) {
         size_t lds;
         bool tiled;      // staged tile + windowed search (k_tile_field)
         bool tiled16;    // paired 16-bit tile with guard rows (k_tile_pair)
+        bool from_mask;  // tiled16 on axis ndim-2, computing the last-axis pass itself
         uint32_t fbits;  // tiled: value bits of a tile word
         uint32_t cap;    // tiled: search steps before the envelope fallback
     } fh[kMaxDim] = {};
@@ -224,6 +225,19 @@ int run(Request &r) {
                 offsets_fit) {
                 p.tiled16 = true;
                 p.lds = tp;
+                // Fold the last-axis pass into this one when it comes right
+                // after it, the last extent is whole 64-bit mask words, and
+                // the masks of the planes a workgroup touches fit next to the tile.
+                const uint32_t n2 = r.shape[nd - 1];
+                if (a == nd - 2 && n2 % 64 == 0 && uintptr_t(r.in) % 16 == 0) {
+                    const uint64_t planes = (kPairLines + n2 - 2) / n2 + 1;
+                    const uint64_t rows = planes * n;
+                    const size_t extra = size_t(rows * (n2 / 64) * 8 + rows * (n2 / 64) * 4);
+                    if (tp + extra + 1024 <= kLdsBytes) {
+                        p.from_mask = true;
+                        p.lds = tp + extra;
+                    }
+                }
                 continue;
             }
         }
@@ -255,7 +269,8 @@ int run(Request &r) {
 
     int rc;
     // ---- pass over the last axis: nearest zero in each contiguous line ----
-    {
+    // (computed by the next pass itself when that one reads the mask)
+    if (!(nd >= 2 && fh[nd - 2].from_mask)) {
         ScanArgs s{};
         s.in = r.in;
         s.n = nlast;
@@ -273,7 +288,7 @@ int run(Request &r) {
             s.dist = r.dist;
             s.sq = r.sq;
             s.idx = r.idx;
-            out = nullptr;
+            out = nullptr;   // scalar stores: no alignment needed
         } else if (index_path) {
             mode = kScanIndex;
             s.idx = r.idx;
@@ -287,7 +302,33 @@ int run(Request &r) {
             s.field_f = r.dist;
             out = r.dist;
         }
-        if (nlast <= uint32_t(kSpan)) {
+        const bool word_ok = nlast % kWave == 0 && nlast <= uint32_t(kWave * kWave) &&
+                             uintptr_t(r.in) % 16 == 0 && uintptr_t(out) % 16 == 0;
+        if (word_ok) {
+            WordScanArgs ws{};
+            ws.in = r.in;
+            ws.n = nlast;
+            ws.nw = nlast / kWave;
+            ws.lpw = kWave / ws.nw;
+            ws.lines = total / nlast;
+            ws.lps = uint32_t(vox / nlast);
+            ws.vox = uint32_t(vox);
+            ws.ndim = nd;
+            ws.w = r.w[nd - 1];
+            ws.field_i = s.field_i;
+            ws.field_f = s.field_f;
+            ws.idx = s.idx;
+            ws.dist = s.dist;
+            ws.sq = s.sq;
+            const uint64_t waves = (ws.lines + ws.lpw - 1) / ws.lpw;
+            const dim3 grid(uint32_t((waves + 3) / 4)), block(256);
+            switch (mode) {
+                case kScanFieldInt: rc = launch("scan_word", k_scan_word<kScanFieldInt>, grid, block, 0, r.stream, ws); break;
+                case kScanFieldFlt: rc = launch("scan_word", k_scan_word<kScanFieldFlt>, grid, block, 0, r.stream, ws); break;
+                case kScanIndex: rc = launch("scan_word", k_scan_word<kScanIndex>, grid, block, 0, r.stream, ws); break;
+                default: rc = launch("scan_word", k_scan_word<kScanFinal>, grid, block, 0, r.stream, ws); break;
+            }
+        } else if (nlast <= uint32_t(kSpan)) {
             s.span_lines = uint32_t(kSpan) / nlast;
             const uint64_t waves = (uint64_t(s.lines) + s.span_lines - 1) / s.span_lines;
             const dim3 grid(uint32_t((waves + 3) / 4)), block(256);
@@ -328,6 +369,8 @@ int run(Request &r) {
         if (p.tiled16) {
             PairArgs tg{};
             tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
+            tg.mask = r.in;
+            tg.n2 = r.shape[nd - 1];
             tg.total = total;
             tg.lines = lines;
             tg.n = n;
@@ -340,8 +383,12 @@ int run(Request &r) {
                 tg.wall[b] = r.w[b];
             }
             const dim3 tgrid(uint32_t((lines + kPairLines - 1) / kPairLines)), tblock(kWave * kPairWaves);
-            rc = fin ? launch("tile_pair_final", k_tile_pair<true>, tgrid, tblock, p.lds, r.stream, tg)
-                     : launch("tile_pair", k_tile_pair<false>, tgrid, tblock, p.lds, r.stream, tg);
+            if (p.from_mask)
+                rc = fin ? launch("plane_pair_final", k_tile_pair<true, true>, tgrid, tblock, p.lds, r.stream, tg)
+                         : launch("plane_pair", k_tile_pair<false, true>, tgrid, tblock, p.lds, r.stream, tg);
+            else
+                rc = fin ? launch("tile_pair_final", k_tile_pair<true, false>, tgrid, tblock, p.lds, r.stream, tg)
+                         : launch("tile_pair", k_tile_pair<false, false>, tgrid, tblock, p.lds, r.stream, tg);
         } else if (p.tiled) {
             TileArgs tg{};
             tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;

@@ -293,3 +293,151 @@ __global__ void __launch_bounds__(64) k_scan_long(ScanArgs a) {
 }
 
 }  // namespace tmedt
+
+namespace tmedt {
+
+// ---------------------------------------------------------------------------
+// Lines whose length is a multiple of 64: one lane per 64-position word.
+// A wavefront holds 64 / words-per-line whole lines (lanes past them idle).
+// Each lane loads its 64 mask bytes (four 16-byte loads), builds the 64-bit
+// zero mask, takes the last zero of the earlier words and the first zero of
+// the later words of its line from two segmented wave scans, then walks its
+// 64 positions left to right (distance to the last zero) and right to left
+// (distance to the next zero), keeping the left zero on ties.
+// ---------------------------------------------------------------------------
+struct WordScanArgs {
+    const uint8_t *in;
+    uint32_t n;            // line length, a multiple of 64
+    uint32_t nw;           // words per line = n / 64 (<= 64)
+    uint32_t lpw;          // whole lines per wavefront = 64 / nw
+    uint64_t lines;        // lines in the batch
+    uint32_t lps;          // lines per sample
+    uint32_t vox;          // elements per sample
+    int32_t ndim;
+    double w;              // squared sampling of the last axis
+    int32_t *field_i;      // kScanFieldInt output
+    float *field_f;        // kScanFieldFlt output
+    int32_t *idx;          // kScanIndex: slice 0 of [batch][ndim][vox]; kScanFinal: coords
+    float *dist;           // kScanFinal outputs (each may be null)
+    int32_t *sq;
+};
+
+template <int MODE>
+__global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const uint64_t wave = uint64_t(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
+    const int nw = int(a.nw);
+    const int lw = lane / nw;                 // line within the wavefront
+    const int w = lane - lw * nw;             // word within the line
+    const uint64_t line = wave * a.lpw + lw;
+    const bool live = lw < int(a.lpw) && line < a.lines;
+    if (wave * a.lpw >= a.lines) return;      // whole wavefront exits together
+
+    // ---- zero mask of this lane's 64 positions ---------------------------
+    const uint64_t pos0 = line * a.n + uint64_t(w) * 64;   // batch-flat first position
+    uint64_t mask = 0;
+    if (live) {
+        const uint4 *src = reinterpret_cast<const uint4 *>(a.in + pos0);
+        uint4 v[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = src[k];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t d4[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                // 0x80 in every zero byte (exact: no carries between bytes)
+                const uint32_t x = d4[c];
+                const uint32_t zb = ~(((x & 0x7f7f7f7fu) + 0x7f7f7f7fu) | x | 0x7f7f7f7fu);
+                // gather bits 7, 15, 23, 31 into a nibble
+                const uint32_t nib = ((zb >> 7) & 1u) | ((zb >> 14) & 2u) | ((zb >> 21) & 4u) | ((zb >> 28) & 8u);
+                mask |= uint64_t(nib) << (16 * k + 4 * c);
+            }
+        }
+    }
+
+    // ---- nearest zero in the other words of the line ---------------------
+    // Keys carry the line within the wavefront in their high bits so that a
+    // plain wave-wide max / min never mixes two lines.
+    const int base = w * 64;
+    const uint32_t hi = uint32_t(lw) << 16;
+    const uint32_t own_last = mask ? hi | uint32_t(base + 63 - __clzll(mask) + 1) : hi;
+    const uint32_t own_first = mask ? hi | uint32_t(base + __ffsll((unsigned long long)mask) - 1) : hi | 0xffffu;
+    uint32_t pm = own_last, sm = own_first;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const uint32_t u = __shfl_up(pm, d, kWave);
+        if (lane >= d) pm = max(pm, u);
+        const uint32_t v = __shfl_down(sm, d, kWave);
+        if (lane + d < kWave) sm = min(sm, v);
+    }
+    uint32_t before = __shfl_up(pm, 1, kWave);   // words < w of the line
+    uint32_t after = __shfl_down(sm, 1, kWave);  // words > w of the line
+    if (w == 0 || (before >> 16) != uint32_t(lw)) before = hi;
+    if (w == nw - 1 || (after >> 16) != uint32_t(lw)) after = hi | 0xffffu;
+    constexpr int kFar = 1 << 20;
+    int last = (before & 0xffffu) ? int(before & 0xffffu) - 1 : -kFar;  // line-relative
+    int next = (after & 0xffffu) != 0xffffu ? int(after & 0xffffu) : kFar;
+
+    // ---- per-position distances -------------------------------------------
+    int dl[64];
+#pragma unroll
+    for (int p = 0; p < 64; ++p) {
+        if ((mask >> p) & 1ull) last = base + p;
+        dl[p] = last;             // last zero at or before base + p
+    }
+    int32_t out[64];
+#pragma unroll
+    for (int p = 63; p >= 0; --p) {
+        if ((mask >> p) & 1ull) next = base + p;
+        const int x = base + p;
+        const int l = x - dl[p], r = next - x;   // l, r >= 0
+        const bool left = l <= r;
+        const int dd = left ? l : r;
+        const int y = left ? dl[p] : next;        // line-relative zero, valid if dd < kFar / 2
+        const bool none = dd >= kFar / 2;
+        if (MODE == kScanFieldInt) {
+            out[p] = none ? kInfI : dd * dd;
+        } else if (MODE == kScanFieldFlt) {
+            const double df = double(dd);
+            out[p] = none ? __builtin_bit_cast(int32_t, __builtin_inff())
+                          : __builtin_bit_cast(int32_t, float(a.w * (df * df)));
+        } else if (MODE == kScanIndex) {
+            const uint64_t s = line / a.lps;
+            const uint32_t local = uint32_t(line - s * a.lps) * a.n;
+            out[p] = none ? kNoIdx : int32_t(local + y);
+        } else {
+            out[p] = none ? -1 : y;   // kScanFinal: the line is the sample
+        }
+    }
+    if (!live) return;
+
+    // ---- stores -------------------------------------------------------------
+    if (MODE == kScanFieldInt || MODE == kScanFieldFlt) {
+        int4 *dst = reinterpret_cast<int4 *>(MODE == kScanFieldInt ? a.field_i
+                                                                  : reinterpret_cast<int32_t *>(a.field_f)) +
+                    pos0 / 4;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) dst[k] = make_int4(out[4 * k], out[4 * k + 1], out[4 * k + 2], out[4 * k + 3]);
+    } else if (MODE == kScanIndex) {
+        const uint64_t s = line / a.lps;
+        const uint64_t off = s * uint64_t(a.ndim) * a.vox + (line - s * a.lps) * a.n + uint64_t(w) * 64;
+        int4 *dst = reinterpret_cast<int4 *>(a.idx + off);
+#pragma unroll
+        for (int k = 0; k < 16; ++k) dst[k] = make_int4(out[4 * k], out[4 * k + 1], out[4 * k + 2], out[4 * k + 3]);
+    } else {
+        // rank 1: a line without any zero measures from the virtual zero at -1
+#pragma unroll
+        for (int p = 0; p < 64; ++p) {
+            const int x = base + p;
+            const int y = out[p];
+            const int64_t dd = y >= 0 ? int64_t(x - y) : int64_t(x + 1);
+            const uint64_t g = pos0 + p;
+            if (a.dist) a.dist[g] = float(sqrt(a.w * double(dd * dd)));
+            if (a.sq) a.sq[g] = int32_t(dd * dd);
+            if (a.idx) a.idx[g] = y;
+        }
+    }
+}
+
+}  // namespace tmedt

@@ -175,3 +175,33 @@ def test_sqrt_is_correctly_rounded():
         d2 = sum(g * g for g in grid)
         assert np.array_equal(res["sq"][0], d2)
         assert np.array_equal(res["dist"][0], np.sqrt(d2.astype(np.float64)).astype(np.float32))
+
+
+FUSED = [
+    ((7, 50, 64), 2, 0.05),        # final pass reads the mask; 3.5 workgroups
+    ((3, 33, 192), 2, 0.01),       # workgroups straddle planes; zeros several words apart
+    ((2, 9, 21, 128), 3, 0.2),
+    ((1, 5, 160, 64), 3, 0.002),   # long lines, mostly empty rows
+    ((2, 3, 4, 7, 64), 4, 0.5),
+]
+
+
+@pytest.mark.parametrize("shape,ndim,p_bg", FUSED, ids=["x".join(map(str, s)) for s, _, _ in FUSED])
+def test_pass_reading_the_mask(shape, ndim, p_bg):
+    """Last extent a multiple of 64: the axis ndim-2 pass computes the
+    last-axis distances from the mask itself (checked through the kernel
+    names the library reports)."""
+    from paper_2608_24738_amd import binding
+    mask = rand_mask(shape, p_bg, len(shape) + shape[-1])
+    binding.prof_enable(64)
+    try:
+        parity(mask, ndim, None, dist=True, idx=False, tag="fused")
+        names = {n for n, _ in binding.prof_read()}
+    finally:
+        binding.prof_enable(0)
+    assert any(n.startswith("plane_pair") for n in names), names
+    assert not any(n.startswith("scan") for n in names), names
+    for fill in (0, 1):
+        m = np.full(shape, fill, np.uint8)
+        m[..., -1, -1] = 1 - fill if fill else 0
+        parity(m, ndim, None, dist=True, idx=False, tag="fused fill=%d" % fill)
