@@ -751,12 +751,14 @@ __device__ __forceinline__ void search_pair(const uint32_t *b, u16x2 &best, int 
 
 struct PairArgs {
     int32_t *buf;         // int32 squared distances, batch-flat, in place
-    const uint8_t *mask;  // FROM_MASK: the input mask; this pass runs along axis ndim-2
-    uint32_t n2;          // FROM_MASK: extent of the last axis (a multiple of 64)
-    uint64_t total;       // elements of buf
-    uint64_t lines;
-    uint32_t n;
-    uint32_t inner;
+    const uint8_t *mask;  // FROM_MASK: the input mask
+    uint32_t total;       // elements of buf (below 2^32)
+    uint32_t lines;       // lines of this pass (lines + kPairLines below 2^32)
+    uint32_t n;           // line length
+    uint32_t inner;       // stride of the axis, in elements
+    uint32_t n2;          // FROM_MASK: extent of the last axis (a multiple of 32)
+    Div32 div_inner;      // division by inner
+    Div32 div_n2;         // FROM_MASK: division by n2
     float *dist;          // final pass outputs
     int32_t *sq;
     int32_t ndim;
@@ -764,29 +766,51 @@ struct PairArgs {
     double wall[kMaxDim];
 };
 
+constexpr uint32_t kFar16 = 0x3fff;   // "no zero on this side of the row"
+
+// Correctly rounded float square root of an integer 0 <= x < 2^24 (exact as
+// a float).  The hardware estimate y is one of the two floats around sqrt(x);
+// the result is y or one of its neighbours y-, y+, chosen by the signs of the
+// exact residuals x - y- * y and x - y+ * y (one fused multiply-add each):
+// y- * y and y+ * y fall strictly between the squares of the midpoints on
+// either side of y and the nearest representable x, so the signs tell on
+// which side of each midpoint sqrt(x) lies.
+__device__ __forceinline__ float sqrt_rn_int(uint32_t x) {
+    const float xf = float(x);
+    const float y = __builtin_amdgcn_sqrtf(xf);
+    const float ym = __uint_as_float(__float_as_uint(y) - 1u);
+    const float yp = __uint_as_float(__float_as_uint(y) + 1u);
+    float r = y;
+    if (__builtin_fmaf(-ym, y, xf) <= 0.0f) r = ym;
+    if (__builtin_fmaf(-yp, y, xf) > 0.0f) r = yp;
+    return r;
+}
+
 // FROM_MASK: the pass along axis ndim-2 computes its own input, the
 // last-axis pass, from the mask.  The workgroup's 128 lines are columns of
-// one or more mask planes (the last two axes); it loads those planes with
-// 16-byte loads, turns every 16 bytes into a 16-bit zero mask in LDS (so each
-// mask row is a run of 64-bit words), notes per row and word the nearest zero
-// in the words before and after it, and gives each column its squared
-// distance to the nearest zero of its row from one shift and a leading- or
-// trailing-zero count.  This removes the last-axis kernel's write and this
-// pass's read of the intermediate.
+// one or more mask planes (the last two axes).  It reads those planes with
+// 16-byte loads and keeps, for every mask row and 32-column word, the word's
+// zero bits and the distances from its first column back to the previous
+// zero and from its last column on to the next one.  These entries are
+// stored inside the tile row of the same index, which only the wave that
+// owns the row overwrites, after reading them.  A lane's two columns share a
+// word (the last extent is even), so one 8-byte read, one shift, and one
+// leading- and one trailing-zero count give both row distances.  This
+// removes the last-axis kernel's write and this pass's read of it.
 template <bool FINAL, bool FROM_MASK>
 __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
-    extern __shared__ __attribute__((aligned(16))) uint32_t tw[];  // rows [-kGuard16, n + kGuard16) x kWave words, then FROM_MASK data
+    extern __shared__ __attribute__((aligned(16))) uint32_t tw[];  // rows [-kGuard16, n + kGuard16) x kWave words
     __shared__ uint8_t any_site[kPairWaves][kWave];
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
     const int n = int(a.n);
-    const uint64_t inner = a.inner;
-    const uint64_t L0 = uint64_t(blockIdx.x) * kPairLines;
-    const uint64_t o0 = L0 / inner;
-    const uint64_t wg_base = o0 * uint64_t(n) * inner + (L0 - o0 * inner);
-    const uint64_t span = (a.total - wg_base) * 4;
-    const uint32_t row_bytes = uint32_t(inner * 4);
+    const uint32_t inner = a.inner;
+    const uint32_t L0 = blockIdx.x * uint32_t(kPairLines);
+    const uint32_t o0 = a.div_inner.div(L0);
+    const uint32_t wg_base = o0 * uint32_t(n) * inner + (L0 - o0 * inner);
+    const uint64_t span = uint64_t(a.total - wg_base) * 4;
+    const uint32_t row_bytes = inner * 4;
     const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.buf + wg_base, span);
     __amdgpu_buffer_rsrc_t rd = rb, rs = rb;
     if (FINAL) {
@@ -797,12 +821,12 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
     // Line j of the workgroup: liveness, position along the later axes, and
     // byte offset of its row 0 in the workgroup's buffer view.
     auto locate = [&](int j, bool &live, uint32_t &ipos, uint32_t &voff) {
-        const uint64_t L = L0 + j;
+        const uint32_t L = L0 + uint32_t(j);
         live = L < a.lines;
-        const uint64_t o = live ? L / inner : o0;
-        const uint64_t i = live ? L - o * inner : 0;
-        ipos = uint32_t(i);
-        voff = live ? uint32_t((o * uint64_t(n) * inner + i - wg_base) * 4) : 0u;
+        const uint32_t o = live ? a.div_inner.div(L) : o0;
+        const uint32_t i = live ? L - o * inner : 0u;
+        ipos = i;
+        voff = live ? (o * uint32_t(n) * inner + i - wg_base) * 4u : 0u;
     };
     bool live_a, live_b;
     uint32_t i_a, i_b, voff_a, voff_b;
@@ -817,100 +841,113 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
     uint32_t seen = 0;
     if constexpr (FROM_MASK) {
         const uint32_t n2 = a.n2;
-        const int nw = int(n2 / 64);
-        const uint64_t p_first = L0 / n2;
-        const uint64_t last_line = min(L0 + kPairLines, a.lines) - 1;
-        const int planes = int(last_line / n2 - p_first) + 1;
-        const int rows = planes * n;                                  // mask rows held
-        uint16_t *zm16 = reinterpret_cast<uint16_t *>(tw + (n + 2 * kGuard16) * kWave);
-        const uint64_t *zm = reinterpret_cast<const uint64_t *>(zm16);  // [row][word]
-        int16_t *before = reinterpret_cast<int16_t *>(zm16 + rows * nw * 4);  // last zero before word, or -1
-        int16_t *after = before + rows * nw;                                  // first zero after word, or -1
-        // zero masks: 16 bytes -> 16 bits
-        const uint4 *src = reinterpret_cast<const uint4 *>(a.mask + p_first * uint64_t(n) * n2);
-        const int chunks = rows * int(n2 / 16);
-        constexpr int MB = 4;
-        for (int k0 = t; k0 < chunks; k0 += kWave * kPairWaves * MB) {
-            uint4 v[MB];
+        const int nw = int(n2 >> 5);                        // mask words per row
+        const uint32_t p_first = a.div_n2.div(L0);
+        const uint32_t last_line = min(L0 + uint32_t(kPairLines), a.lines) - 1u;
+        const int planes = int(a.div_n2.div(last_line) - p_first) + 1;
+        // Entry (plane, word) of mask row q: words 2e (zero bits) and 2e + 1
+        // (distance back | distance on << 16) of tile row q, e = plane * nw + word.
+        const uint4 *src = reinterpret_cast<const uint4 *>(a.mask + size_t(p_first) * uint32_t(n) * n2);
+        const int tasks = planes * n * nw;                  // one per 32 mask bytes
+        for (int k0 = t; k0 < tasks; k0 += 2 * kWave * kPairWaves) {
+            const int kk[2] = {k0, min(k0 + kWave * kPairWaves, tasks - 1)};
+            uint4 v[4];
 #pragma unroll
-            for (int j = 0; j < MB; ++j) v[j] = src[min(k0 + j * kWave * kPairWaves, chunks - 1)];
+            for (int j = 0; j < 2; ++j) {
+                v[2 * j] = src[2 * kk[j]];
+                v[2 * j + 1] = src[2 * kk[j] + 1];
+            }
 #pragma unroll
-            for (int j = 0; j < MB; ++j) {
-                const int k = k0 + j * kWave * kPairWaves;
-                if (k >= chunks) break;
-                const uint32_t d4[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+            for (int j = 0; j < 2; ++j) {
+                if (j == 1 && k0 + kWave * kPairWaves >= tasks) break;
+                const uint32_t d8[8] = {v[2 * j].x, v[2 * j].y, v[2 * j].z, v[2 * j].w,
+                                        v[2 * j + 1].x, v[2 * j + 1].y, v[2 * j + 1].z, v[2 * j + 1].w};
                 uint32_t bits = 0;
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const uint32_t x = d4[c];
+                for (int c = 0; c < 8; ++c) {
+                    const uint32_t x = d8[c];
+                    // bit 7 of each byte set iff the byte is zero
                     const uint32_t zb = ~(((x & 0x7f7f7f7fu) + 0x7f7f7f7fu) | x | 0x7f7f7f7fu);
-                    bits |= (((zb >> 7) & 1u) | ((zb >> 14) & 2u) | ((zb >> 21) & 4u) | ((zb >> 28) & 8u)) << (4 * c);
+                    bits |= (((zb >> 7) & 1u) | ((zb >> 14) & 2u) | ((zb >> 21) & 4u) | ((zb >> 28) & 8u))
+                            << (4 * c);
                 }
-                zm16[k] = uint16_t(bits);
+                const int k = kk[j];
+                const int r = k / nw, w = k - (k / nw) * nw;   // mask row (plane-major), word
+                int pl = 0, q = r;
+                while (q >= n) {
+                    q -= n;
+                    ++pl;
+                }
+                row0[q * kWave + 2 * (pl * nw + w)] = bits;
             }
         }
         __syncthreads();
-        // nearest zero in the words before / after each word of each row
-        for (int r = t; r < rows; r += kWave * kPairWaves) {
-            int last = -1;
+        for (int r = t; r < planes * n; r += kWave * kPairWaves) {
+            int pl = 0, q = r;
+            while (q >= n) {
+                q -= n;
+                ++pl;
+            }
+            uint32_t *ent = row0 + q * kWave + 2 * pl * nw;
+            int last = -1;                                   // last zero seen, going right
             for (int w = 0; w < nw; ++w) {
-                before[r * nw + w] = int16_t(last);
-                const uint64_t m = zm[r * nw + w];
-                if (m) last = w * 64 + 63 - __clzll(m);
+                const uint32_t m = ent[2 * w];
+                ent[2 * w + 1] = last < 0 ? kFar16 : uint32_t(32 * w - last);
+                if (m) last = 32 * w + 31 - int(__builtin_clz(m));
             }
-            int first = -1;
+            int first = -1;                                  // first zero seen, going left
             for (int w = nw - 1; w >= 0; --w) {
-                after[r * nw + w] = int16_t(first);
-                const uint64_t m = zm[r * nw + w];
-                if (m) first = w * 64 + __ffsll((unsigned long long)m) - 1;
+                const uint32_t m = ent[2 * w];
+                ent[2 * w + 1] |= (first < 0 ? kFar16 : uint32_t(first - (32 * w + 31))) << 16;
+                if (m) first = 32 * w + int(__builtin_ctz(m));
             }
         }
         __syncthreads();
-        // row distances of this lane's two columns, straight into the tile
-        const uint64_t La = min(L0 + 2 * lane, last_line), Lb = min(L0 + 2 * lane + 1, last_line);
-        const int pa = int(La / n2 - p_first), pb = int(Lb / n2 - p_first);
-        const int ca = int(La % n2), cb = int(Lb % n2);
-        auto rowdist = [&](int pl, int c, int q) -> uint32_t {
-            const int r = pl * n + q;
-            const int w = c >> 6, b = c & 63;
-            const uint64_t m = zm[r * nw + w];
-            const uint64_t ml = m << (63 - b);     // zeros at or before c, top bit = c
-            const uint64_t mr = m >> b;            // zeros at or after c, bit 0 = c
-            const int yl = ml ? c - int(__clzll(ml)) : int(before[r * nw + w]);
-            const int yr = mr ? c + __ffsll((unsigned long long)mr) - 1 : int(after[r * nw + w]);
-            int d = kNone16;
-            if (yl >= 0) d = c - yl;
-            if (yr >= 0 && yr - c < d) d = yr - c;
-            return d == kNone16 ? uint32_t(kNone16) : uint32_t(d * d);
-        };
+        // Lines 2l and 2l+1 are columns c, c+1 (c even) of one plane.
+        const uint32_t La = min(L0 + 2u * uint32_t(lane), last_line);
+        const uint32_t pa = a.div_n2.div(La);
+        const int ca = int(La - pa * n2);
+        const int e = int(pa - p_first) * nw + (ca >> 5);
+        const int b = ca & 31;
+        const bool live = live_a && live_b;
+#pragma unroll 2
         for (int q = wv; q < n; q += kPairWaves) {
-            const uint32_t fa = live_a ? rowdist(pa, ca, q) : kNone16;
-            const uint32_t fb = live_b ? rowdist(pb, cb, q) : kNone16;
-            seen |= (fa != kNone16 ? 1u : 0u) | (fb != kNone16 ? 2u : 0u);
+            const uint2 en = *reinterpret_cast<const uint2 *>(row0 + q * kWave + 2 * e);
+            const uint32_t m = en.x;
+            const uint32_t ml = m << (31 - b);               // bit 31 = column c
+            const uint32_t mr = m >> (b + 1);                // bit 0 = column c + 1
+            const int la = ml ? int(__builtin_clz(ml)) : b + int(en.y & 0xffffu);
+            const int rb = mr ? int(__builtin_ctz(mr)) : 30 - b + int(en.y >> 16);
+            const int lb = (mr & 1u) ? 0 : la + 1;
+            const int ra = ((m >> b) & 1u) ? 0 : rb + 1;
+            const int da = min(la, ra), db = min(lb, rb);
+            const uint32_t fa = (live && da < 256) ? uint32_t(da * da) : uint32_t(kNone16);
+            const uint32_t fb = (live && db < 256) ? uint32_t(db * db) : uint32_t(kNone16);
+            seen |= (fa != uint32_t(kNone16) ? 1u : 0u) | (fb != uint32_t(kNone16) ? 2u : 0u);
             row0[q * kWave + lane] = fa | (fb << 16);
         }
     } else {
-    // Stage: wave wv reads rows wv, wv + 8, ...; SB rows are in flight at once.
-    constexpr int SB = 8;
-    for (int q0 = wv; q0 < n; q0 += kPairWaves * SB) {
-        uint32_t va[SB], vb[SB];
+        // Stage: wave wv reads rows wv, wv + 8, ...; SB rows are in flight at once.
+        constexpr int SB = 8;
+        for (int q0 = wv; q0 < n; q0 += kPairWaves * SB) {
+            uint32_t va[SB], vb[SB];
 #pragma unroll
-        for (int j = 0; j < SB; ++j) {
-            const uint32_t so = uint32_t(min(q0 + j * kPairWaves, n - 1)) * row_bytes;
-            va[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_a, so, 0);
-            vb[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_b, so, 0);
-        }
+            for (int j = 0; j < SB; ++j) {
+                const uint32_t so = uint32_t(min(q0 + j * kPairWaves, n - 1)) * row_bytes;
+                va[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_a, so, 0);
+                vb[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_b, so, 0);
+            }
 #pragma unroll
-        for (int j = 0; j < SB; ++j) {
-            const int q = q0 + j * kPairWaves;
-            if (q < n) {
-                const uint32_t fa = (!live_a || va[j] == uint32_t(kInfI)) ? kNone16 : va[j];
-                const uint32_t fb = (!live_b || vb[j] == uint32_t(kInfI)) ? kNone16 : vb[j];
-                seen |= (fa != kNone16 ? 1u : 0u) | (fb != kNone16 ? 2u : 0u);
-                row0[q * kWave + lane] = fa | (fb << 16);
+            for (int j = 0; j < SB; ++j) {
+                const int q = q0 + j * kPairWaves;
+                if (q < n) {
+                    const uint32_t fa = (!live_a || va[j] == uint32_t(kInfI)) ? kNone16 : va[j];
+                    const uint32_t fb = (!live_b || vb[j] == uint32_t(kInfI)) ? kNone16 : vb[j];
+                    seen |= (fa != kNone16 ? 1u : 0u) | (fb != kNone16 ? 2u : 0u);
+                    row0[q * kWave + lane] = fa | (fb << 16);
+                }
             }
         }
-    }
     }
     any_site[wv][lane] = uint8_t(seen);
     __syncthreads();
@@ -921,6 +958,11 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
     // them keeps them from holding the wave's stop vote open.
     const uint32_t searched = ((live_a && (has & 1u)) ? 0xffffu : 0u) |
                               ((live_b && (has & 2u)) ? 0xffff0000u : 0u);
+    // A final pass over a line with no site gives distances to the virtual
+    // background element; the wave takes that path only when one of its
+    // lines needs it.
+    const bool wave_virtual =
+        FINAL && __any((live_a && !(has & 1u)) || (live_b && !(has & 2u)));
 
     auto emit = [&](uint32_t voff, uint32_t ipos, int q, int32_t d2, bool none) {
         const uint32_t soff = uint32_t(q) * row_bytes;
@@ -929,13 +971,15 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
         } else {
             float df;
             int32_t dq;
-            if (none) {
+            if (!wave_virtual) {
+                df = sqrt_rn_int(uint32_t(d2));
+                dq = d2;
+            } else if (none) {
                 const int64_t v = virtual_sq<int64_t>(q, ipos, a.ndim, a.shape, a.wall);
                 df = float(sqrt(double(v)));
                 dq = int32_t(v);
             } else {
-                // d2 < 2^24 converts exactly; sqrtf is correctly rounded
-                df = sqrtf(float(d2));
+                df = sqrt_rn_int(uint32_t(d2));
                 dq = d2;
             }
             if (a.dist) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, df), rd, voff, soff, 0);

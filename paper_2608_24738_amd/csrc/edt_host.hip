@@ -222,21 +222,23 @@ int run(Request &r) {
             const bool offsets_fit =
                 (uint64_t(n) * inner * 2 + uint64_t(n) * kPairLines) * 4 < (uint64_t(1) << 31);
             if (fmax + uint64_t(n + 4) * (n + 4) < uint64_t(kNone16) && tp + 1024 <= kLdsBytes &&
-                offsets_fit) {
+                offsets_fit && total / n + kPairLines < (uint64_t(1) << 32)) {
                 p.tiled16 = true;
                 p.lds = tp;
                 // Fold the last-axis pass into this one when it comes right
-                // after it, the last extent is whole 64-bit mask words, and
-                // the masks of the planes a workgroup touches fit next to the tile.
+                // after it, the last extent is whole 32-column mask words, and
+                // the mask entries of the planes a workgroup touches fit in a
+                // tile row (two words per plane and mask word).
                 const uint32_t n2 = r.shape[nd - 1];
-                if (a == nd - 2 && n2 % 64 == 0 && uintptr_t(r.in) % 16 == 0) {
-                    const uint64_t planes = (kPairLines + n2 - 2) / n2 + 1;
-                    const uint64_t rows = planes * n;
-                    const size_t extra = size_t(rows * (n2 / 64) * 8 + rows * (n2 / 64) * 4);
-                    if (tp + extra + 1024 <= kLdsBytes) {
-                        p.from_mask = true;
-                        p.lds = tp + extra;
+                if (a == nd - 2 && n2 % 32 == 0 && uintptr_t(r.in) % 16 == 0) {
+                    uint32_t g = kPairLines;
+                    for (uint32_t x = n2; x;) {
+                        const uint32_t y = g % x;
+                        g = x;
+                        x = y;
                     }
+                    const uint64_t planes = (uint64_t(n2) - g + kPairLines - 1) / n2 + 1;
+                    if (planes * (n2 / 32) * 2 <= uint64_t(kWave)) p.from_mask = true;
                 }
                 continue;
             }
@@ -371,10 +373,12 @@ int run(Request &r) {
             tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
             tg.mask = r.in;
             tg.n2 = r.shape[nd - 1];
-            tg.total = total;
-            tg.lines = lines;
+            tg.div_n2 = Div32::make(tg.n2);
+            tg.total = uint32_t(total);
+            tg.lines = uint32_t(lines);
             tg.n = n;
             tg.inner = uint32_t(inner);
+            tg.div_inner = Div32::make(tg.inner);
             tg.dist = r.dist;
             tg.sq = r.sq;
             tg.ndim = nd;
