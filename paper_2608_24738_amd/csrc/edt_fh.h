@@ -687,19 +687,24 @@ namespace tmedt {
 // reach fit in 16 bits.  A workgroup owns 128 adjacent lines; lane l of each
 // wave holds lines 2l and 2l+1 packed in one 32-bit tile word, so one LDS
 // read fetches a row for both lines and packed 16-bit min / saturating add
-// (v_pk_min_u16, v_pk_add_u16 clamp) process both at once.  kGuard16 rows of
-// "no site" (0xffff) above and below the line make the first kCap16 steps
-// of every search read in bounds without a test, unrolled in blocks of four
-// with literal squared distances and immediate LDS offsets.  Searches that
-// need more steps continue with the row index clamped into the guard rows
-// (every row beyond the line is "no site" anyway), so the result is exact for
-// any input; only sparse inputs pay for the longer searches.
+// (v_pk_min_u16, v_pk_add_u16 clamp) process both at once.  Rows at least
+// kCap16 - kGuard16 away from both ends run the first kCap16 steps of their
+// search unrolled, in blocks of four with literal squared distances and
+// immediate LDS offsets; the kGuard16 rows of "no site" (0xffff) above and
+// below the line keep those reads in the tile.  Other rows, and searches
+// that need more steps, continue with the row index clamped into the guard
+// rows (every row beyond the line is "no site" anyway), so the result is
+// exact for any input.  Few guard rows keep the tile small enough for four
+// 128-line workgroups per compute unit at n = 128.
 // ---------------------------------------------------------------------------
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kCap16 = 16;                 // unrolled search steps
-constexpr int kReach16 = kCap16 + 3;       // farthest row the unrolled part reads
-constexpr int kGuard16 = kCap16 + 4;       // guard rows per side
+constexpr int kCap16 = 16;                 // unrolled search steps (farthest row read)
+constexpr int kGuard16 = 4;                // guard rows per side
+constexpr int kRowW = kWave + 8;           // tile row stride in words (8 words of padding)
+constexpr int kPatchRows = 8;              // search patch: 8 rows x 8 words (16 lines)
+static_assert(kCap16 == 16, "the patch search unrolls up to four blocks of four steps");
 constexpr int32_t kNone16 = 0xffff;
 constexpr int kPairWaves = 8;              // waves per workgroup
 constexpr int kPairLines = 2 * kWave;      // lines per workgroup
@@ -722,18 +727,19 @@ __device__ __forceinline__ bool stopped(u16x2 best, int d) {
 
 // Search blocks BLK .. NBLK-1 (four steps each) for both lines of a lane,
 // unrolled at compile time.  `b` points at the word of row (element row -
-// kReach16), row stride kWave words.  Leaves `dnext` = the first distance not
+// 4 NBLK), row stride kRowW words, so every read has a non-negative
+// immediate offset from it.  Leaves `dnext` = the first distance not
 // examined; ends early once both lines of every lane have stopped.
 template <int BLK, int NBLK>
 __device__ __forceinline__ void search_pair(const uint32_t *b, u16x2 &best, int &dnext) {
     if constexpr (BLK < NBLK) {
         constexpr int d = 1 + 4 * BLK;
-        constexpr int R = kReach16;
+        constexpr int R = 4 * NBLK;
         if (__all(stopped(best, d))) return;
-        const u16x2 u0 = as_pair(b[(R - d) * kWave]), u1 = as_pair(b[(R - d - 1) * kWave]);
-        const u16x2 u2 = as_pair(b[(R - d - 2) * kWave]), u3 = as_pair(b[(R - d - 3) * kWave]);
-        const u16x2 w0 = as_pair(b[(R + d) * kWave]), w1 = as_pair(b[(R + d + 1) * kWave]);
-        const u16x2 w2 = as_pair(b[(R + d + 2) * kWave]), w3 = as_pair(b[(R + d + 3) * kWave]);
+        const u16x2 u0 = as_pair(b[(R - d) * kRowW]), u1 = as_pair(b[(R - d - 1) * kRowW]);
+        const u16x2 u2 = as_pair(b[(R - d - 2) * kRowW]), u3 = as_pair(b[(R - d - 3) * kRowW]);
+        const u16x2 w0 = as_pair(b[(R + d) * kRowW]), w1 = as_pair(b[(R + d + 1) * kRowW]);
+        const u16x2 w2 = as_pair(b[(R + d + 2) * kRowW]), w3 = as_pair(b[(R + d + 3) * kRowW]);
         const u16x2 c0 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u0, w0), splat(d * d));
         const u16x2 c1 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u1, w1),
                                                        splat((d + 1) * (d + 1)));
@@ -799,7 +805,7 @@ __device__ __forceinline__ float sqrt_rn_int(uint32_t x) {
 // removes the last-axis kernel's write and this pass's read of it.
 template <bool FINAL, bool FROM_MASK>
 __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
-    extern __shared__ __attribute__((aligned(16))) uint32_t tw[];  // rows [-kGuard16, n + kGuard16) x kWave words
+    extern __shared__ __attribute__((aligned(16))) uint32_t tw[];  // rows [-kGuard16, n + kGuard16) x kRowW words
     __shared__ uint8_t any_site[kPairWaves][kWave];
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
@@ -832,11 +838,13 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
     uint32_t i_a, i_b, voff_a, voff_b;
     locate(2 * lane, live_a, i_a, voff_a);
     locate(2 * lane + 1, live_b, i_b, voff_b);
-    uint32_t *row0 = tw + kGuard16 * kWave;   // row 0 of the lines
+    uint32_t *row0 = tw + kGuard16 * kRowW;   // row 0 of the lines
+    // Even stride: lines 2l and 2l+1 are adjacent, both live or both absent.
+    const bool pair_io = (inner & 1u) == 0u;
 
-    for (int k = t; k < kGuard16 * kWave; k += kWave * kPairWaves) {
+    for (int k = t; k < kGuard16 * kRowW; k += kWave * kPairWaves) {
         tw[k] = 0xffffffffu;
-        row0[(n * kWave) + k] = 0xffffffffu;
+        row0[(n * kRowW) + k] = 0xffffffffu;
     }
     uint32_t seen = 0;
     if constexpr (FROM_MASK) {
@@ -878,7 +886,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
                     q -= n;
                     ++pl;
                 }
-                row0[q * kWave + 2 * (pl * nw + w)] = bits;
+                row0[q * kRowW + 2 * (pl * nw + w)] = bits;
             }
         }
         __syncthreads();
@@ -888,7 +896,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
                 q -= n;
                 ++pl;
             }
-            uint32_t *ent = row0 + q * kWave + 2 * pl * nw;
+            uint32_t *ent = row0 + q * kRowW + 2 * pl * nw;
             int last = -1;                                   // last zero seen, going right
             for (int w = 0; w < nw; ++w) {
                 const uint32_t m = ent[2 * w];
@@ -912,7 +920,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
         const bool live = live_a && live_b;
 #pragma unroll 2
         for (int q = wv; q < n; q += kPairWaves) {
-            const uint2 en = *reinterpret_cast<const uint2 *>(row0 + q * kWave + 2 * e);
+            const uint2 en = *reinterpret_cast<const uint2 *>(row0 + q * kRowW + 2 * e);
             const uint32_t m = en.x;
             const uint32_t ml = m << (31 - b);               // bit 31 = column c
             const uint32_t mr = m >> (b + 1);                // bit 0 = column c + 1
@@ -924,18 +932,30 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
             const uint32_t fa = (live && da < 256) ? uint32_t(da * da) : uint32_t(kNone16);
             const uint32_t fb = (live && db < 256) ? uint32_t(db * db) : uint32_t(kNone16);
             seen |= (fa != uint32_t(kNone16) ? 1u : 0u) | (fb != uint32_t(kNone16) ? 2u : 0u);
-            row0[q * kWave + lane] = fa | (fb << 16);
+            row0[q * kRowW + lane] = fa | (fb << 16);
         }
     } else {
-        // Stage: wave wv reads rows wv, wv + 8, ...; SB rows are in flight at once.
-        constexpr int SB = 8;
+        // Stage: wave wv reads rows wv, wv + 8, ...; SB rows are in flight at
+        // once.  With an even stride the lane's two lines are adjacent in
+        // memory and one 8-byte access serves both.
+        constexpr int SB = 16;
         for (int q0 = wv; q0 < n; q0 += kPairWaves * SB) {
             uint32_t va[SB], vb[SB];
+            if (pair_io) {
 #pragma unroll
-            for (int j = 0; j < SB; ++j) {
-                const uint32_t so = uint32_t(min(q0 + j * kPairWaves, n - 1)) * row_bytes;
-                va[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_a, so, 0);
-                vb[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_b, so, 0);
+                for (int j = 0; j < SB; ++j) {
+                    const uint32_t so = uint32_t(min(q0 + j * kPairWaves, n - 1)) * row_bytes;
+                    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rb, voff_a, so, 0);
+                    va[j] = v.x;
+                    vb[j] = v.y;
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < SB; ++j) {
+                    const uint32_t so = uint32_t(min(q0 + j * kPairWaves, n - 1)) * row_bytes;
+                    va[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_a, so, 0);
+                    vb[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_b, so, 0);
+                }
             }
 #pragma unroll
             for (int j = 0; j < SB; ++j) {
@@ -944,85 +964,125 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
                     const uint32_t fa = (!live_a || va[j] == uint32_t(kInfI)) ? kNone16 : va[j];
                     const uint32_t fb = (!live_b || vb[j] == uint32_t(kInfI)) ? kNone16 : vb[j];
                     seen |= (fa != kNone16 ? 1u : 0u) | (fb != kNone16 ? 2u : 0u);
-                    row0[q * kWave + lane] = fa | (fb << 16);
+                    row0[q * kRowW + lane] = fa | (fb << 16);
                 }
             }
         }
     }
     any_site[wv][lane] = uint8_t(seen);
     __syncthreads();
-    uint32_t has = 0;
+
+    // ---- windowed exact search over patches ----------------------------------
+    // Wave wv searches the 8 tile words (16 lines) of column block wv, 8 rows
+    // at a time: lane l takes row 8 rb + l / 8 of word 8 wv + l % 8.  Nearby
+    // rows of nearby lines need similar search lengths, so a compact patch
+    // stops much sooner than a whole row of 128 lines.  The 8 words of row
+    // padding put the 64 lanes of a patch read in distinct LDS banks.
+    const int cw = kPatchRows * wv + (lane & 7);       // tile word = line pair
+    const int pr = lane >> 3;                          // row within the patch
+    uint32_t has_p = 0, has = 0;
 #pragma unroll
-    for (int w = 0; w < kPairWaves; ++w) has |= any_site[w][lane];
+    for (int w = 0; w < kPairWaves; ++w) {
+        has_p |= any_site[w][cw];
+        has |= any_site[w][lane];
+    }
+    bool live_pa, live_pb;
+    {
+        uint32_t ip, vo;
+        locate(2 * cw, live_pa, ip, vo);
+        locate(2 * cw + 1, live_pb, ip, vo);
+    }
     // Halves whose line is absent or has no site need no search: clearing
     // them keeps them from holding the wave's stop vote open.
-    const uint32_t searched = ((live_a && (has & 1u)) ? 0xffffu : 0u) |
-                              ((live_b && (has & 2u)) ? 0xffff0000u : 0u);
+    const uint32_t searched = ((live_pa && (has_p & 1u)) ? 0xffffu : 0u) |
+                              ((live_pb && (has_p & 2u)) ? 0xffff0000u : 0u);
     // A final pass over a line with no site gives distances to the virtual
-    // background element; the wave takes that path only when one of its
-    // lines needs it.
+    // background element; the wave takes that path only when one of the
+    // lines it stores needs it.
     const bool wave_virtual =
         FINAL && __any((live_a && !(has & 1u)) || (live_b && !(has & 2u)));
 
-    auto emit = [&](uint32_t voff, uint32_t ipos, int q, int32_t d2, bool none) {
-        const uint32_t soff = uint32_t(q) * row_bytes;
+    // Values of one line at row q for the outputs: the stored field
+    // (non-final), or the distance and squared distance (final).
+    auto value = [&](uint32_t ipos, int q, int32_t d2, bool none, uint32_t &vd, uint32_t &vs) {
         if (!FINAL) {
-            __builtin_amdgcn_raw_buffer_store_b32(uint32_t(none ? kInfI : d2), rb, voff, soff, 0);
+            vd = uint32_t(none ? kInfI : d2);
+            vs = vd;
+        } else if (!wave_virtual || !none) {
+            vd = __builtin_bit_cast(uint32_t, sqrt_rn_int(uint32_t(d2)));
+            vs = uint32_t(d2);
         } else {
-            float df;
-            int32_t dq;
-            if (!wave_virtual) {
-                df = sqrt_rn_int(uint32_t(d2));
-                dq = d2;
-            } else if (none) {
-                const int64_t v = virtual_sq<int64_t>(q, ipos, a.ndim, a.shape, a.wall);
-                df = float(sqrt(double(v)));
-                dq = int32_t(v);
-            } else {
-                df = sqrt_rn_int(uint32_t(d2));
-                dq = d2;
-            }
-            if (a.dist) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, df), rd, voff, soff, 0);
-            if (a.sq) __builtin_amdgcn_raw_buffer_store_b32(uint32_t(dq), rs, voff, soff, 0);
+            const int64_t v = virtual_sq<int64_t>(q, ipos, a.ndim, a.shape, a.wall);
+            vd = __builtin_bit_cast(uint32_t, float(sqrt(double(v))));
+            vs = uint32_t(v);
         }
     };
+    const bool want_d = !FINAL || a.dist != nullptr;
+    const bool want_s = FINAL && a.sq != nullptr;
+    const __amdgpu_buffer_rsrc_t r_d = FINAL ? rd : rb;
+    // Results of a row block go through the row padding (8 words per row,
+    // never searched): slot s sits at word 64 + s % 8 of tile row s / 8
+    // (counting from the first guard row), two blocks of 512 slots
+    // alternating.  A row is rotated by 8 words per row within its 64 slots,
+    // so both the patch writes and the row reads hit distinct banks.
+    auto slot_word = [&](int s) { return (s >> 3) * kRowW + kWave + (s & 7); };
 
-    // ---- windowed exact search -------------------------------------------
-    // Rows are taken RB at a time and stored together after their searches.
-    constexpr int RB = 4;
-    for (int q0 = wv; q0 < n; q0 += kPairWaves * RB) {
-        u16x2 res[RB];
+    const int nrb = (n + kPatchRows - 1) / kPatchRows;
+    for (int rbk = 0; rbk < nrb; ++rbk) {
+        const int q0 = kPatchRows * rbk;               // first row of the patch (uniform)
+        const int q = min(q0 + pr, n - 1);             // this lane's row
+        u16x2 best = as_pair(row0[q * kRowW + cw] & searched);
+        int d = 1;
+        // Unrolled blocks whose reads stay in the tile for every row of the
+        // patch: block k reads up to 4 (k + 1) rows away (uniform choice).
+        const int room = min(q0 + kGuard16, n - 1 + kGuard16 - (q0 + kPatchRows - 1));
+        const int nb = room >= kCap16 ? kCap16 / 4 : room >> 2;
+        if (nb == 4) search_pair<0, 4>(row0 + (q - 16) * kRowW + cw, best, d);
+        else if (nb == 3) search_pair<0, 3>(row0 + (q - 12) * kRowW + cw, best, d);
+        else if (nb == 2) search_pair<0, 2>(row0 + (q - 8) * kRowW + cw, best, d);
+        else if (nb == 1) search_pair<0, 1>(row0 + (q - 4) * kRowW + cw, best, d);
+        // Longer searches and rows near the ends: row indices clamp into
+        // the guard rows.
+        while (!__all(stopped(best, d))) {
 #pragma unroll
-        for (int j = 0; j < RB; ++j) {
-            const int q = min(q0 + kPairWaves * j, n - 1);
-            // base row q - kReach16 (inside the guard rows)
-            const uint32_t *bp = row0 + (q - kReach16) * kWave + lane;
-            u16x2 best = as_pair(bp[kReach16 * kWave] & searched);
-            int d = 1;
-            search_pair<0, kCap16 / 4>(bp, best, d);
-            // Longer searches: row indices clamp into the guard rows.
-            while (!__all(stopped(best, d))) {
-#pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    const int dd = d + s;
-                    const int lo = max(q - dd, -kGuard16), hi = min(q + dd, n + kGuard16 - 1);
-                    const u16x2 u = as_pair(row0[lo * kWave + lane]);
-                    const u16x2 w = as_pair(row0[hi * kWave + lane]);
-                    best = __builtin_elementwise_min(
-                        best, __builtin_elementwise_add_sat(__builtin_elementwise_min(u, w),
-                                                            splat(dd * dd >= kNone16 ? kNone16 : dd * dd)));
-                }
-                d += 4;
-                if (d > n + 4) break;   // every row has been examined
+            for (int s = 0; s < 4; ++s) {
+                const int dd = d + s;
+                const int lo = max(q - dd, -kGuard16), hi = min(q + dd, n + kGuard16 - 1);
+                const u16x2 u = as_pair(row0[lo * kRowW + cw]);
+                const u16x2 w = as_pair(row0[hi * kRowW + cw]);
+                best = __builtin_elementwise_min(
+                    best, __builtin_elementwise_add_sat(__builtin_elementwise_min(u, w),
+                                                        splat(dd * dd >= kNone16 ? kNone16 : dd * dd)));
             }
-            res[j] = best;
+            d += 4;
+            if (d > n + 4) break;   // every row has been examined
         }
-#pragma unroll
-        for (int j = 0; j < RB; ++j) {
-            const int q = q0 + kPairWaves * j;
-            if (q >= n) continue;
-            if (live_a) emit(voff_a, i_a, q, int32_t(res[j].x), !(has & 1u));
-            if (live_b) emit(voff_b, i_b, q, int32_t(res[j].y), !(has & 2u));
+        const int buf = (rbk & 1) * 512;
+        tw[slot_word(buf + pr * kWave + ((cw + 8 * pr) & 63))] = as_word(best);
+        __syncthreads();
+        // Wave wv stores row 8 rb + wv of the block, one 8-byte pair per lane.
+        const int qs = q0 + wv;
+        if (qs < n) {
+            const u16x2 r = as_pair(tw[slot_word(buf + wv * kWave + ((lane + 8 * wv) & 63))]);
+            const uint32_t soff = uint32_t(qs) * row_bytes;
+            uint32_t da, sa, db, sb;
+            value(i_a, qs, int32_t(r.x), !(has & 1u), da, sa);
+            value(i_b, qs, int32_t(r.y), !(has & 2u), db, sb);
+            if (pair_io) {
+                if (live_a) {
+                    if (want_d) __builtin_amdgcn_raw_buffer_store_b64(u32x2{da, db}, r_d, voff_a, soff, 0);
+                    if (want_s) __builtin_amdgcn_raw_buffer_store_b64(u32x2{sa, sb}, rs, voff_a, soff, 0);
+                }
+            } else {
+                if (live_a) {
+                    if (want_d) __builtin_amdgcn_raw_buffer_store_b32(da, r_d, voff_a, soff, 0);
+                    if (want_s) __builtin_amdgcn_raw_buffer_store_b32(sa, rs, voff_a, soff, 0);
+                }
+                if (live_b) {
+                    if (want_d) __builtin_amdgcn_raw_buffer_store_b32(db, r_d, voff_b, soff, 0);
+                    if (want_s) __builtin_amdgcn_raw_buffer_store_b32(sb, rs, voff_b, soff, 0);
+                }
+            }
         }
     }
 }

@@ -216,7 +216,9 @@ int run(Request &r) {
             // within the line stays below the "no site" code, the tile (with
             // guard rows) fits LDS, and byte offsets within a workgroup's
             // buffer view stay below 2^31.
-            const size_t tp = size_t(n + 2 * kGuard16) * kWave * 4;
+            // at least 128 rows: the row padding also carries two blocks of
+            // 512 result slots
+            const size_t tp = size_t(n + 2 * kGuard16 < 128 ? 128 : n + 2 * kGuard16) * kRowW * 4;
             uint64_t inner = 1;
             for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
             const bool offsets_fit =
