@@ -755,6 +755,44 @@ __device__ __forceinline__ void search_pair(const uint32_t *b, u16x2 &best, int 
     }
 }
 
+// The same for two rows 8 apart (row r at `b` + 4 NBLK rows, row r + 8
+// eight rows further): two independent chains per block, one vote for both.
+template <int BLK, int NBLK>
+__device__ __forceinline__ void search_pair2(const uint32_t *b, u16x2 &best1, u16x2 &best2, int &dnext) {
+    if constexpr (BLK < NBLK) {
+        constexpr int d = 1 + 4 * BLK;
+        constexpr int R = 4 * NBLK;
+        constexpr int E = R + kPatchRows;
+        if (__all(stopped(__builtin_elementwise_max(best1, best2), d))) return;
+        const u16x2 u0 = as_pair(b[(R - d) * kRowW]), u1 = as_pair(b[(R - d - 1) * kRowW]);
+        const u16x2 u2 = as_pair(b[(R - d - 2) * kRowW]), u3 = as_pair(b[(R - d - 3) * kRowW]);
+        const u16x2 w0 = as_pair(b[(R + d) * kRowW]), w1 = as_pair(b[(R + d + 1) * kRowW]);
+        const u16x2 w2 = as_pair(b[(R + d + 2) * kRowW]), w3 = as_pair(b[(R + d + 3) * kRowW]);
+        const u16x2 x0 = as_pair(b[(E - d) * kRowW]), x1 = as_pair(b[(E - d - 1) * kRowW]);
+        const u16x2 x2 = as_pair(b[(E - d - 2) * kRowW]), x3 = as_pair(b[(E - d - 3) * kRowW]);
+        const u16x2 y0 = as_pair(b[(E + d) * kRowW]), y1 = as_pair(b[(E + d + 1) * kRowW]);
+        const u16x2 y2 = as_pair(b[(E + d + 2) * kRowW]), y3 = as_pair(b[(E + d + 3) * kRowW]);
+        const u16x2 s0 = splat(d * d), s1 = splat((d + 1) * (d + 1));
+        const u16x2 s2 = splat((d + 2) * (d + 2)), s3 = splat((d + 3) * (d + 3));
+        const u16x2 c0 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u0, w0), s0);
+        const u16x2 c1 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u1, w1), s1);
+        const u16x2 c2 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u2, w2), s2);
+        const u16x2 c3 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u3, w3), s3);
+        const u16x2 e0 = __builtin_elementwise_add_sat(__builtin_elementwise_min(x0, y0), s0);
+        const u16x2 e1 = __builtin_elementwise_add_sat(__builtin_elementwise_min(x1, y1), s1);
+        const u16x2 e2 = __builtin_elementwise_add_sat(__builtin_elementwise_min(x2, y2), s2);
+        const u16x2 e3 = __builtin_elementwise_add_sat(__builtin_elementwise_min(x3, y3), s3);
+        best1 = __builtin_elementwise_min(
+            best1, __builtin_elementwise_min(__builtin_elementwise_min(c0, c1),
+                                             __builtin_elementwise_min(c2, c3)));
+        best2 = __builtin_elementwise_min(
+            best2, __builtin_elementwise_min(__builtin_elementwise_min(e0, e1),
+                                             __builtin_elementwise_min(e2, e3)));
+        dnext = d + 4;
+        search_pair2<BLK + 1, NBLK>(b, best1, best2, dnext);
+    }
+}
+
 struct PairArgs {
     int32_t *buf;         // int32 squared distances, batch-flat, in place
     const uint8_t *mask;  // FROM_MASK: the input mask
@@ -803,8 +841,10 @@ __device__ __forceinline__ float sqrt_rn_int(uint32_t x) {
 // word (the last extent is even), so one 8-byte read, one shift, and one
 // leading- and one trailing-zero count give both row distances.  This
 // removes the last-axis kernel's write and this pass's read of it.
-template <bool FINAL, bool FROM_MASK>
-__global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
+// MAXRB = 8 (lines up to 128 rows) keeps to 64 VGPRs, so four workgroups
+// (eight waves per SIMD) share a compute unit.
+template <bool FINAL, bool FROM_MASK, int MAXRB>
+__global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile_pair(PairArgs a) {
     extern __shared__ __attribute__((aligned(16))) uint32_t tw[];  // rows [-kGuard16, n + kGuard16) x kRowW words
     __shared__ uint8_t any_site[kPairWaves][kWave];
     const int t = threadIdx.x;
@@ -1020,70 +1060,107 @@ __global__ void __launch_bounds__(kWave * kPairWaves) k_tile_pair(PairArgs a) {
     const bool want_d = !FINAL || a.dist != nullptr;
     const bool want_s = FINAL && a.sq != nullptr;
     const __amdgpu_buffer_rsrc_t r_d = FINAL ? rd : rb;
-    // Results of a row block go through the row padding (8 words per row,
-    // never searched): slot s sits at word 64 + s % 8 of tile row s / 8
-    // (counting from the first guard row), two blocks of 512 slots
-    // alternating.  A row is rotated by 8 words per row within its 64 slots,
-    // so both the patch writes and the row reads hit distinct banks.
-    auto slot_word = [&](int s) { return (s >> 3) * kRowW + kWave + (s & 7); };
-
-    const int nrb = (n + kPatchRows - 1) / kPatchRows;
-    for (int rbk = 0; rbk < nrb; ++rbk) {
-        const int q0 = kPatchRows * rbk;               // first row of the patch (uniform)
-        const int q = min(q0 + pr, n - 1);             // this lane's row
-        u16x2 best = as_pair(row0[q * kRowW + cw] & searched);
+    // Lane l searches rows 16 rb + l / 8 and 16 rb + 8 + l / 8 of word
+    // 8 wv + l % 8 (two independent chains per step, one stop vote) for every
+    // row block rb, keeping the results in registers until all searches of
+    // the workgroup are done; then they replace the tile and the waves store
+    // whole rows.
+    constexpr int PR = 2 * kPatchRows;
+    const int nrb = (n + PR - 1) / PR;                 // at most MAXRB (host)
+    u16x2 res1[MAXRB], res2[MAXRB];
+#pragma unroll
+    for (int rbk = 0; rbk < MAXRB; ++rbk) {
+        if (rbk >= nrb) break;
+        const int q0 = PR * rbk;                       // first row of the patch (uniform)
+        const int q1 = min(q0 + pr, n - 1), q2 = min(q0 + kPatchRows + pr, n - 1);
+        u16x2 best1 = as_pair(row0[q1 * kRowW + cw] & searched);
+        u16x2 best2 = as_pair(row0[q2 * kRowW + cw] & searched);
         int d = 1;
         // Unrolled blocks whose reads stay in the tile for every row of the
         // patch: block k reads up to 4 (k + 1) rows away (uniform choice).
-        const int room = min(q0 + kGuard16, n - 1 + kGuard16 - (q0 + kPatchRows - 1));
-        const int nb = room >= kCap16 ? kCap16 / 4 : room >> 2;
-        if (nb == 4) search_pair<0, 4>(row0 + (q - 16) * kRowW + cw, best, d);
-        else if (nb == 3) search_pair<0, 3>(row0 + (q - 12) * kRowW + cw, best, d);
-        else if (nb == 2) search_pair<0, 2>(row0 + (q - 8) * kRowW + cw, best, d);
-        else if (nb == 1) search_pair<0, 1>(row0 + (q - 4) * kRowW + cw, best, d);
+        // A patch that runs past the last row (its clamped rows are not 8
+        // apart) takes the clamped loop only.
+        const int room = min(q0 + kGuard16, n - 1 + kGuard16 - (q0 + PR - 1));
+        const int nb = q0 + PR > n ? 0 : room >= kCap16 ? kCap16 / 4 : room >> 2;
+        if (nb == 4) search_pair2<0, 4>(row0 + (q1 - 16) * kRowW + cw, best1, best2, d);
+        else if (nb == 3) search_pair2<0, 3>(row0 + (q1 - 12) * kRowW + cw, best1, best2, d);
+        else if (nb == 2) search_pair2<0, 2>(row0 + (q1 - 8) * kRowW + cw, best1, best2, d);
+        else if (nb == 1) search_pair2<0, 1>(row0 + (q1 - 4) * kRowW + cw, best1, best2, d);
         // Longer searches and rows near the ends: row indices clamp into
         // the guard rows.
-        while (!__all(stopped(best, d))) {
+        while (!__all(stopped(__builtin_elementwise_max(best1, best2), d))) {
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
                 const int dd = d + s;
-                const int lo = max(q - dd, -kGuard16), hi = min(q + dd, n + kGuard16 - 1);
-                const u16x2 u = as_pair(row0[lo * kRowW + cw]);
-                const u16x2 w = as_pair(row0[hi * kRowW + cw]);
-                best = __builtin_elementwise_min(
-                    best, __builtin_elementwise_add_sat(__builtin_elementwise_min(u, w),
-                                                        splat(dd * dd >= kNone16 ? kNone16 : dd * dd)));
+                const u16x2 sq = splat(dd * dd >= kNone16 ? kNone16 : dd * dd);
+                const int lo1 = max(q1 - dd, -kGuard16), hi1 = min(q1 + dd, n + kGuard16 - 1);
+                const int lo2 = max(q2 - dd, -kGuard16), hi2 = min(q2 + dd, n + kGuard16 - 1);
+                const u16x2 u = as_pair(row0[lo1 * kRowW + cw]), w = as_pair(row0[hi1 * kRowW + cw]);
+                const u16x2 x = as_pair(row0[lo2 * kRowW + cw]), y = as_pair(row0[hi2 * kRowW + cw]);
+                best1 = __builtin_elementwise_min(
+                    best1, __builtin_elementwise_add_sat(__builtin_elementwise_min(u, w), sq));
+                best2 = __builtin_elementwise_min(
+                    best2, __builtin_elementwise_add_sat(__builtin_elementwise_min(x, y), sq));
             }
             d += 4;
             if (d > n + 4) break;   // every row has been examined
         }
-        const int buf = (rbk & 1) * 512;
-        tw[slot_word(buf + pr * kWave + ((cw + 8 * pr) & 63))] = as_word(best);
-        __syncthreads();
-        // Wave wv stores row 8 rb + wv of the block, one 8-byte pair per lane.
-        const int qs = q0 + wv;
-        if (qs < n) {
-            const u16x2 r = as_pair(tw[slot_word(buf + wv * kWave + ((lane + 8 * wv) & 63))]);
-            const uint32_t soff = uint32_t(qs) * row_bytes;
-            uint32_t da, sa, db, sb;
+        res1[rbk] = best1;
+        res2[rbk] = best2;
+    }
+    __syncthreads();   // every search has read the tile
+#pragma unroll
+    for (int rbk = 0; rbk < MAXRB; ++rbk) {
+        if (rbk >= nrb) break;
+        const int q1 = PR * rbk + pr, q2 = q1 + kPatchRows;
+        if (q1 < n) row0[q1 * kRowW + cw] = as_word(res1[rbk]);
+        if (q2 < n) row0[q2 * kRowW + cw] = as_word(res2[rbk]);
+    }
+    __syncthreads();
+
+    // ---- store: wave wv writes rows wv, wv + 8, ..., one 8-byte pair per lane
+    auto emit_row = [&](int qs, u16x2 r) {
+        const uint32_t soff = uint32_t(qs) * row_bytes;
+        uint32_t da, sa, db, sb;
+        if (!FINAL) {
+            da = (has & 1u) ? uint32_t(r.x) : uint32_t(kInfI);
+            db = (has & 2u) ? uint32_t(r.y) : uint32_t(kInfI);
+            sa = da;
+            sb = db;
+        } else if (!wave_virtual) {
+            // every line of the wave has a site
+            da = __builtin_bit_cast(uint32_t, sqrt_rn_int(r.x));
+            db = __builtin_bit_cast(uint32_t, sqrt_rn_int(r.y));
+            sa = r.x;
+            sb = r.y;
+        } else {
             value(i_a, qs, int32_t(r.x), !(has & 1u), da, sa);
             value(i_b, qs, int32_t(r.y), !(has & 2u), db, sb);
-            if (pair_io) {
-                if (live_a) {
-                    if (want_d) __builtin_amdgcn_raw_buffer_store_b64(u32x2{da, db}, r_d, voff_a, soff, 0);
-                    if (want_s) __builtin_amdgcn_raw_buffer_store_b64(u32x2{sa, sb}, rs, voff_a, soff, 0);
-                }
-            } else {
-                if (live_a) {
-                    if (want_d) __builtin_amdgcn_raw_buffer_store_b32(da, r_d, voff_a, soff, 0);
-                    if (want_s) __builtin_amdgcn_raw_buffer_store_b32(sa, rs, voff_a, soff, 0);
-                }
-                if (live_b) {
-                    if (want_d) __builtin_amdgcn_raw_buffer_store_b32(db, r_d, voff_b, soff, 0);
-                    if (want_s) __builtin_amdgcn_raw_buffer_store_b32(sb, rs, voff_b, soff, 0);
-                }
+        }
+        if (pair_io) {
+            if (live_a) {
+                if (want_d) __builtin_amdgcn_raw_buffer_store_b64(u32x2{da, db}, r_d, voff_a, soff, 0);
+                if (want_s) __builtin_amdgcn_raw_buffer_store_b64(u32x2{sa, sb}, rs, voff_a, soff, 0);
+            }
+        } else {
+            if (live_a) {
+                if (want_d) __builtin_amdgcn_raw_buffer_store_b32(da, r_d, voff_a, soff, 0);
+                if (want_s) __builtin_amdgcn_raw_buffer_store_b32(sa, rs, voff_a, soff, 0);
+            }
+            if (live_b) {
+                if (want_d) __builtin_amdgcn_raw_buffer_store_b32(db, r_d, voff_b, soff, 0);
+                if (want_s) __builtin_amdgcn_raw_buffer_store_b32(sb, rs, voff_b, soff, 0);
             }
         }
+    };
+    constexpr int RB = 4;
+    for (int q0 = wv; q0 < n; q0 += kPairWaves * RB) {
+        u16x2 r[RB];
+#pragma unroll
+        for (int j = 0; j < RB; ++j) r[j] = as_pair(row0[min(q0 + kPairWaves * j, n - 1) * kRowW + lane]);
+#pragma unroll
+        for (int j = 0; j < RB; ++j)
+            if (q0 + kPairWaves * j < n) emit_row(q0 + kPairWaves * j, r[j]);
     }
 }
 

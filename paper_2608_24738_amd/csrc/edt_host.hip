@@ -216,14 +216,12 @@ int run(Request &r) {
             // within the line stays below the "no site" code, the tile (with
             // guard rows) fits LDS, and byte offsets within a workgroup's
             // buffer view stay below 2^31.
-            // at least 128 rows: the row padding also carries two blocks of
-            // 512 result slots
-            const size_t tp = size_t(n + 2 * kGuard16 < 128 ? 128 : n + 2 * kGuard16) * kRowW * 4;
+            const size_t tp = size_t(n + 2 * kGuard16) * kRowW * 4;
             uint64_t inner = 1;
             for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
             const bool offsets_fit =
                 (uint64_t(n) * inner * 2 + uint64_t(n) * kPairLines) * 4 < (uint64_t(1) << 31);
-            if (fmax + uint64_t(n + 4) * (n + 4) < uint64_t(kNone16) && tp + 1024 <= kLdsBytes &&
+            if (n <= 256 && fmax + uint64_t(n + 4) * (n + 4) < uint64_t(kNone16) && tp + 1024 <= kLdsBytes &&
                 offsets_fit && total / n + kPairLines < (uint64_t(1) << 32)) {
                 p.tiled16 = true;
                 p.lds = tp;
@@ -389,12 +387,22 @@ int run(Request &r) {
                 tg.wall[b] = r.w[b];
             }
             const dim3 tgrid(uint32_t((lines + kPairLines - 1) / kPairLines)), tblock(kWave * kPairWaves);
-            if (p.from_mask)
-                rc = fin ? launch("plane_pair_final", k_tile_pair<true, true>, tgrid, tblock, p.lds, r.stream, tg)
-                         : launch("plane_pair", k_tile_pair<false, true>, tgrid, tblock, p.lds, r.stream, tg);
-            else
-                rc = fin ? launch("tile_pair_final", k_tile_pair<true, false>, tgrid, tblock, p.lds, r.stream, tg)
-                         : launch("tile_pair", k_tile_pair<false, false>, tgrid, tblock, p.lds, r.stream, tg);
+            // search results stay in registers: 2 per lane and 16-row block
+            if (n <= 128) {
+                if (p.from_mask)
+                    rc = fin ? launch("plane_pair_final", k_tile_pair<true, true, 8>, tgrid, tblock, p.lds, r.stream, tg)
+                             : launch("plane_pair", k_tile_pair<false, true, 8>, tgrid, tblock, p.lds, r.stream, tg);
+                else
+                    rc = fin ? launch("tile_pair_final", k_tile_pair<true, false, 8>, tgrid, tblock, p.lds, r.stream, tg)
+                             : launch("tile_pair", k_tile_pair<false, false, 8>, tgrid, tblock, p.lds, r.stream, tg);
+            } else {
+                if (p.from_mask)
+                    rc = fin ? launch("plane_pair_final", k_tile_pair<true, true, 16>, tgrid, tblock, p.lds, r.stream, tg)
+                             : launch("plane_pair", k_tile_pair<false, true, 16>, tgrid, tblock, p.lds, r.stream, tg);
+                else
+                    rc = fin ? launch("tile_pair_final", k_tile_pair<true, false, 16>, tgrid, tblock, p.lds, r.stream, tg)
+                             : launch("tile_pair", k_tile_pair<false, false, 16>, tgrid, tblock, p.lds, r.stream, tg);
+            }
         } else if (p.tiled) {
             TileArgs tg{};
             tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
