@@ -805,10 +805,21 @@ struct PairArgs {
     Div32 div_n2;         // FROM_MASK: division by n2
     float *dist;          // final pass outputs
     int32_t *sq;
+    int32_t in_seg;       // the input field is in the 16-bit segment layout
+    int32_t out_seg;      // write the result in the 16-bit segment layout
     int32_t ndim;
     uint32_t shape[kMaxDim];
     double wall[kMaxDim];
 };
+
+// 16-bit segment layout of an intermediate field: the values of each
+// 128-element aligned run of the buffer are kept as 16-bit numbers (0xffff:
+// no site) in the first 256 bytes of that run's own 512 bytes.  A pass whose
+// rows are whole runs reads and writes half the bytes, and a later pass that
+// writes the 32-bit outputs over a run only ever overwrites its own input.
+__host__ __device__ inline uint32_t seg_offset(uint32_t byte_off32) {
+    return (byte_off32 & ~511u) + ((byte_off32 & 511u) >> 1);
+}
 
 constexpr uint32_t kFar16 = 0x3fff;   // "no zero on this side of the row"
 
@@ -979,6 +990,26 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         // once.  With an even stride the lane's two lines are adjacent in
         // memory and one 8-byte access serves both.
         constexpr int SB = 16;
+        if (a.in_seg) {
+            // whole runs: one 4-byte read per lane holds both lines
+            const uint32_t vs = seg_offset(voff_a);
+            for (int q0 = wv; q0 < n; q0 += kPairWaves * SB) {
+                uint32_t v[SB];
+#pragma unroll
+                for (int j = 0; j < SB; ++j) {
+                    const uint32_t so = uint32_t(min(q0 + j * kPairWaves, n - 1)) * row_bytes;
+                    v[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, vs, so, 0);
+                }
+#pragma unroll
+                for (int j = 0; j < SB; ++j) {
+                    const int q = q0 + j * kPairWaves;
+                    if (q < n) {
+                        seen |= ((v[j] & 0xffffu) != 0xffffu ? 1u : 0u) | ((v[j] >> 16) != 0xffffu ? 2u : 0u);
+                        row0[q * kRowW + lane] = v[j];
+                    }
+                }
+            }
+        } else
         for (int q0 = wv; q0 < n; q0 += kPairWaves * SB) {
             uint32_t va[SB], vb[SB];
             if (pair_io) {
@@ -1122,6 +1153,11 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
     auto emit_row = [&](int qs, u16x2 r) {
         const uint32_t soff = uint32_t(qs) * row_bytes;
         uint32_t da, sa, db, sb;
+        if (!FINAL && a.out_seg) {
+            const uint32_t w = ((has & 1u) ? uint32_t(r.x) : 0xffffu) | ((has & 2u) ? uint32_t(r.y) : 0xffffu) << 16;
+            __builtin_amdgcn_raw_buffer_store_b32(w, rb, seg_offset(voff_a), soff, 0);
+            return;
+        }
         if (!FINAL) {
             da = (has & 1u) ? uint32_t(r.x) : uint32_t(kInfI);
             db = (has & 2u) ? uint32_t(r.y) : uint32_t(kInfI);

@@ -264,6 +264,18 @@ int run(Request &r) {
         if ((lines + p.lpw - 1) / p.lpw >= (uint64_t(1) << 31)) return TM_ERR_UNSUPPORTED;
         p.lds = size_t(n) * p.lpw * eb;
     }
+    // Consecutive paired passes whose rows are whole 128-element runs hand
+    // their field over in the 16-bit segment layout.
+    bool out_seg[kMaxDim] = {};
+    {
+        bool seg_ok[kMaxDim] = {};
+        for (int a = nd - 2; a >= 0; --a) {
+            uint64_t inner = 1;
+            for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
+            seg_ok[a] = fh[a].tiled16 && inner % kPairLines == 0;
+        }
+        for (int a = nd - 2; a >= 1; --a) out_seg[a] = seg_ok[a] && seg_ok[a - 1];
+    }
     const uint32_t nlast = r.shape[nd - 1];
     if (nlast > uint32_t(kSpan) &&
         (uint64_t(nlast + kSpan - 1) / kSpan + 1) * 4 > kLdsBytes)
@@ -379,6 +391,8 @@ int run(Request &r) {
             tg.n = n;
             tg.inner = uint32_t(inner);
             tg.div_inner = Div32::make(tg.inner);
+            tg.out_seg = out_seg[a] ? 1 : 0;
+            tg.in_seg = (a + 1 <= nd - 2 && out_seg[a + 1]) ? 1 : 0;
             tg.dist = r.dist;
             tg.sq = r.sq;
             tg.ndim = nd;

@@ -205,3 +205,21 @@ def test_pass_reading_the_mask(shape, ndim, p_bg):
         m = np.full(shape, fill, np.uint8)
         m[..., -1, -1] = 1 - fill if fill else 0
         parity(m, ndim, None, dist=True, idx=False, tag="fused fill=%d" % fill)
+
+
+SEG = [
+    ((3, 33, 20, 128), 3, 0.03),     # fused pass hands 16-bit runs to the final pass
+    ((2, 6, 10, 4, 64), 4, 0.1),     # axis-1 pass writes 16-bit runs (its input is 32-bit)
+    ((2, 5, 6, 7, 128), 4, 0.004),   # a middle pass both reads and writes 16-bit runs
+]
+
+
+@pytest.mark.parametrize("shape,ndim,p_bg", SEG, ids=["x".join(map(str, s)) for s, _, _ in SEG])
+def test_half_width_intermediates(shape, ndim, p_bg):
+    """Strides that are multiples of 128: consecutive paired passes keep the
+    field as 16-bit values in the first half of each 128-element run."""
+    mask = rand_mask(shape, p_bg, 7 + len(shape))
+    parity(mask, ndim, None, dist=True, idx=False, tag="half-width")
+    mask[0] = 1                                   # a sample with no background
+    mask[-1] = 0                                  # and one that is all background
+    parity(mask, ndim, None, dist=True, idx=False, tag="half-width extremes")
