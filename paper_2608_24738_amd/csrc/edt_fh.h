@@ -709,10 +709,12 @@ constexpr int32_t kNone16 = 0xffff;
 constexpr int kPairWaves = 8;              // waves per workgroup
 constexpr int kPairLines = 2 * kWave;      // lines per workgroup
 
-// Buffer resource over `bytes` bytes from `p` (gfx9 raw-buffer descriptor):
-// loads past the end read 0 and stores past it are dropped.
+// Buffer resource over `bytes` bytes from `p` (gfx9 raw-buffer descriptor),
+// at most 2^31 - 1 bytes: loads past the end read 0 and stores past it are
+// dropped, so a lane given the offset kDeadOff touches no memory.
+constexpr uint32_t kDeadOff = 0x80000000u;
 __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void *p, uint64_t bytes) {
-    const int32_t n = bytes >= 0xffffffffull ? int32_t(0xffffffff) : int32_t(bytes);
+    const int32_t n = bytes >= 0x7fffffffull ? int32_t(0x7fffffff) : int32_t(bytes);
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, n, 0x00020000);
 }
 
@@ -857,7 +859,7 @@ __device__ __forceinline__ float sqrt_rn_int(uint32_t x) {
 template <bool FINAL, bool FROM_MASK, int MAXRB>
 __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile_pair(PairArgs a) {
     extern __shared__ __attribute__((aligned(16))) uint32_t tw[];  // rows [-kGuard16, n + kGuard16) x kRowW words
-    __shared__ uint8_t any_site[kPairWaves][kWave];
+    __shared__ __attribute__((aligned(8))) uint8_t any_site[kWave][kPairWaves];   // [tile word][wave]
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
@@ -883,7 +885,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         const uint32_t o = live ? a.div_inner.div(L) : o0;
         const uint32_t i = live ? L - o * inner : 0u;
         ipos = i;
-        voff = live ? (o * uint32_t(n) * inner + i - wg_base) * 4u : 0u;
+        voff = live ? (o * uint32_t(n) * inner + i - wg_base) * 4u : kDeadOff;
     };
     bool live_a, live_b;
     uint32_t i_a, i_b, voff_a, voff_b;
@@ -968,23 +970,36 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         const int ca = int(La - pa * n2);
         const int e = int(pa - p_first) * nw + (ca >> 5);
         const int b = ca & 31;
-        const bool live = live_a && live_b;
-#pragma unroll 2
-        for (int q = wv; q < n; q += kPairWaves) {
-            const uint2 en = *reinterpret_cast<const uint2 *>(row0 + q * kRowW + 2 * e);
-            const uint32_t m = en.x;
-            const uint32_t ml = m << (31 - b);               // bit 31 = column c
-            const uint32_t mr = m >> (b + 1);                // bit 0 = column c + 1
-            const int la = ml ? int(__builtin_clz(ml)) : b + int(en.y & 0xffffu);
-            const int rb = mr ? int(__builtin_ctz(mr)) : 30 - b + int(en.y >> 16);
-            const int lb = (mr & 1u) ? 0 : la + 1;
-            const int ra = ((m >> b) & 1u) ? 0 : rb + 1;
-            const int da = min(la, ra), db = min(lb, rb);
-            const uint32_t fa = (live && da < 256) ? uint32_t(da * da) : uint32_t(kNone16);
-            const uint32_t fb = (live && db < 256) ? uint32_t(db * db) : uint32_t(kNone16);
-            seen |= (fa != uint32_t(kNone16) ? 1u : 0u) | (fb != uint32_t(kNone16) ? 2u : 0u);
-            row0[q * kRowW + lane] = fa | (fb << 16);
+        u16x2 seenw = splat(kNone16);                 // per half: smallest value seen
+        // Entries of four rows are read before any of them is overwritten.
+        constexpr int EB = 4;
+        for (int q0 = wv; q0 < n; q0 += EB * kPairWaves) {
+            uint2 en[EB];
+#pragma unroll
+            for (int j = 0; j < EB; ++j)
+                en[j] = *reinterpret_cast<const uint2 *>(row0 + min(q0 + j * kPairWaves, n - 1) * kRowW + 2 * e);
+#pragma unroll
+            for (int j = 0; j < EB; ++j) {
+                const int q = q0 + j * kPairWaves;
+                if (q >= n) break;
+                const uint32_t m = en[j].x;
+                const uint32_t ml = m << (31 - b);           // bit 31 = column c
+                const uint32_t mr = m >> (b + 1);            // bit 0 = column c + 1
+                const int la = ml ? int(__builtin_clz(ml)) : b + int(en[j].y & 0xffffu);
+                const int rb = mr ? int(__builtin_ctz(mr)) : 30 - b + int(en[j].y >> 16);
+                const int lb = (mr & 1u) ? 0 : la + 1;
+                const int ra = ((m >> b) & 1u) ? 0 : rb + 1;
+                // Distances past the row ends are at least kFar16: clamped to
+                // 256, their square saturates to "no site".  (Absent lines need
+                // no code: they are never searched and their stores are dropped.)
+                const uint32_t da = min(uint32_t(min(la, ra)), 256u), db = min(uint32_t(min(lb, rb)), 256u);
+                const uint32_t w = min(uint32_t(__umul24(da, da)), uint32_t(kNone16)) |
+                                   (min(uint32_t(__umul24(db, db)), uint32_t(kNone16)) << 16);
+                seenw = __builtin_elementwise_min(seenw, as_pair(w));
+                row0[q * kRowW + lane] = w;
+            }
         }
+        seen = (seenw.x != kNone16 ? 1u : 0u) | (seenw.y != kNone16 ? 2u : 0u);
     } else {
         // Stage: wave wv reads rows wv, wv + 8, ...; SB rows are in flight at
         // once.  With an even stride the lane's two lines are adjacent in
@@ -1040,33 +1055,26 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             }
         }
     }
-    any_site[wv][lane] = uint8_t(seen);
+    any_site[lane][wv] = uint8_t(seen);
     __syncthreads();
 
     // ---- windowed exact search over patches ----------------------------------
-    // Wave wv searches the 8 tile words (16 lines) of column block wv, 8 rows
-    // at a time: lane l takes row 8 rb + l / 8 of word 8 wv + l % 8.  Nearby
-    // rows of nearby lines need similar search lengths, so a compact patch
-    // stops much sooner than a whole row of 128 lines.  The 8 words of row
-    // padding put the 64 lanes of a patch read in distinct LDS banks.
-    const int cw = kPatchRows * wv + (lane & 7);       // tile word = line pair
-    const int pr = lane >> 3;                          // row within the patch
-    uint32_t has_p = 0, has = 0;
-#pragma unroll
-    for (int w = 0; w < kPairWaves; ++w) {
-        has_p |= any_site[w][cw];
-        has |= any_site[w][lane];
-    }
-    bool live_pa, live_pb;
-    {
-        uint32_t ip, vo;
-        locate(2 * cw, live_pa, ip, vo);
-        locate(2 * cw + 1, live_pb, ip, vo);
-    }
-    // Halves whose line is absent or has no site need no search: clearing
-    // them keeps them from holding the wave's stop vote open.
-    const uint32_t searched = ((live_pa && (has_p & 1u)) ? 0xffffu : 0u) |
-                              ((live_pb && (has_p & 2u)) ? 0xffff0000u : 0u);
+    // Patches are 16 rows by 16 lines (8 tile words): lane l takes rows
+    // 16 rb + l / 8 and 16 rb + 8 + l / 8 of word 8 cb + l % 8.  Nearby rows of
+    // nearby lines need similar search lengths, so a compact patch stops much
+    // sooner than a whole row of 128 lines.  Wave wv takes column block
+    // cb = (wv + rb) % 8 of row block rb, so every wave sees every column
+    // block once and heavy blocks are shared out.  The 8 words of row padding
+    // put the 64 lanes of a patch read in distinct LDS banks.
+    auto has_of = [&](int word) {
+        const uint2 v = *reinterpret_cast<const uint2 *>(&any_site[word][0]);
+        uint32_t o = v.x | v.y;
+        o |= o >> 16;
+        o |= o >> 8;
+        return o & 3u;
+    };
+    const uint32_t has = has_of(lane);                 // lines of this lane's stores
+    const int pr = lane >> 3;                          // row within the half patch
     // A final pass over a line with no site gives distances to the virtual
     // background element; the wave takes that path only when one of the
     // lines it stores needs it.
@@ -1091,17 +1099,23 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
     const bool want_d = !FINAL || a.dist != nullptr;
     const bool want_s = FINAL && a.sq != nullptr;
     const __amdgpu_buffer_rsrc_t r_d = FINAL ? rd : rb;
-    // Lane l searches rows 16 rb + l / 8 and 16 rb + 8 + l / 8 of word
-    // 8 wv + l % 8 (two independent chains per step, one stop vote) for every
-    // row block rb, keeping the results in registers until all searches of
-    // the workgroup are done; then they replace the tile and the waves store
+    // Each lane's two rows are two independent chains per step under one
+    // stop vote.  Results stay in registers until all searches of the
+    // workgroup are done; then they replace the tile and the waves store
     // whole rows.
     constexpr int PR = 2 * kPatchRows;
     const int nrb = (n + PR - 1) / PR;                 // at most MAXRB (host)
+    auto patch_word = [&](int rbk) { return kPatchRows * ((wv + rbk) & (kPairWaves - 1)) + (lane & 7); };
     u16x2 res1[MAXRB], res2[MAXRB];
 #pragma unroll
     for (int rbk = 0; rbk < MAXRB; ++rbk) {
         if (rbk >= nrb) break;
+        const int cw = patch_word(rbk);
+        // Halves whose line is absent or has no site need no search: clearing
+        // them keeps them from holding the wave's stop vote open.
+        const uint32_t has_p = has_of(cw);
+        const uint32_t searched = ((L0 + 2u * cw < a.lines && (has_p & 1u)) ? 0xffffu : 0u) |
+                                  ((L0 + 2u * cw + 1u < a.lines && (has_p & 2u)) ? 0xffff0000u : 0u);
         const int q0 = PR * rbk;                       // first row of the patch (uniform)
         const int q1 = min(q0 + pr, n - 1), q2 = min(q0 + kPatchRows + pr, n - 1);
         u16x2 best1 = as_pair(row0[q1 * kRowW + cw] & searched);
@@ -1143,6 +1157,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
 #pragma unroll
     for (int rbk = 0; rbk < MAXRB; ++rbk) {
         if (rbk >= nrb) break;
+        const int cw = patch_word(rbk);
         const int q1 = PR * rbk + pr, q2 = q1 + kPatchRows;
         if (q1 < n) row0[q1 * kRowW + cw] = as_word(res1[rbk]);
         if (q2 < n) row0[q2 * kRowW + cw] = as_word(res2[rbk]);
@@ -1150,54 +1165,80 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
     __syncthreads();
 
     // ---- store: wave wv writes rows wv, wv + 8, ..., one 8-byte pair per lane
-    auto emit_row = [&](int qs, u16x2 r) {
-        const uint32_t soff = uint32_t(qs) * row_bytes;
-        uint32_t da, sa, db, sb;
-        if (!FINAL && a.out_seg) {
-            const uint32_t w = ((has & 1u) ? uint32_t(r.x) : 0xffffu) | ((has & 2u) ? uint32_t(r.y) : 0xffffu) << 16;
-            __builtin_amdgcn_raw_buffer_store_b32(w, rb, seg_offset(voff_a), soff, 0);
-            return;
+    // Lanes of absent lines carry the offset kDeadOff, so their stores are
+    // dropped without a test; the common cases get loops without branches.
+    auto store_rows = [&](auto &&emit) {
+        constexpr int RB = 4;
+        for (int q0 = wv; q0 < n; q0 += kPairWaves * RB) {
+            u16x2 r[RB];
+#pragma unroll
+            for (int j = 0; j < RB; ++j) r[j] = as_pair(row0[min(q0 + kPairWaves * j, n - 1) * kRowW + lane]);
+#pragma unroll
+            for (int j = 0; j < RB; ++j)
+                if (q0 + kPairWaves * j < n)
+                    emit(q0 + kPairWaves * j, uint32_t(q0 + kPairWaves * j) * row_bytes, r[j]);
         }
+    };
+    const uint32_t none_lo = (has & 1u) ? 0u : 0xffffu, none_hi = (has & 2u) ? 0u : 0xffff0000u;
+    if (!FINAL && a.out_seg) {
+        const uint32_t vs = seg_offset(voff_a);
+        store_rows([&](int, uint32_t soff, u16x2 r) {
+            __builtin_amdgcn_raw_buffer_store_b32(as_word(r) | none_lo | none_hi, rb, vs, soff, 0);
+        });
+        return;
+    }
+    if (!FINAL && pair_io) {
+        store_rows([&](int, uint32_t soff, u16x2 r) {
+            const uint32_t da = (has & 1u) ? uint32_t(r.x) : uint32_t(kInfI);
+            const uint32_t db = (has & 2u) ? uint32_t(r.y) : uint32_t(kInfI);
+            __builtin_amdgcn_raw_buffer_store_b64(u32x2{da, db}, rb, voff_a, soff, 0);
+        });
+        return;
+    }
+    if (FINAL && pair_io && !wave_virtual) {
+        // every line of the wave has a site
+        auto dist2 = [](u16x2 r) {
+            return u32x2{__builtin_bit_cast(uint32_t, sqrt_rn_int(r.x)),
+                         __builtin_bit_cast(uint32_t, sqrt_rn_int(r.y))};
+        };
+        if (want_d && !want_s) {
+            store_rows([&](int, uint32_t soff, u16x2 r) {
+                __builtin_amdgcn_raw_buffer_store_b64(dist2(r), rd, voff_a, soff, 0);
+            });
+        } else if (!want_d) {
+            store_rows([&](int, uint32_t soff, u16x2 r) {
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{uint32_t(r.x), uint32_t(r.y)}, rs, voff_a, soff, 0);
+            });
+        } else {
+            store_rows([&](int, uint32_t soff, u16x2 r) {
+                __builtin_amdgcn_raw_buffer_store_b64(dist2(r), rd, voff_a, soff, 0);
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{uint32_t(r.x), uint32_t(r.y)}, rs, voff_a, soff, 0);
+            });
+        }
+        return;
+    }
+    // general case: odd strides, lines without a site in a final pass
+    store_rows([&](int qs, uint32_t soff, u16x2 r) {
+        uint32_t da, sa, db, sb;
         if (!FINAL) {
             da = (has & 1u) ? uint32_t(r.x) : uint32_t(kInfI);
             db = (has & 2u) ? uint32_t(r.y) : uint32_t(kInfI);
             sa = da;
             sb = db;
-        } else if (!wave_virtual) {
-            // every line of the wave has a site
-            da = __builtin_bit_cast(uint32_t, sqrt_rn_int(r.x));
-            db = __builtin_bit_cast(uint32_t, sqrt_rn_int(r.y));
-            sa = r.x;
-            sb = r.y;
         } else {
             value(i_a, qs, int32_t(r.x), !(has & 1u), da, sa);
             value(i_b, qs, int32_t(r.y), !(has & 2u), db, sb);
         }
         if (pair_io) {
-            if (live_a) {
-                if (want_d) __builtin_amdgcn_raw_buffer_store_b64(u32x2{da, db}, r_d, voff_a, soff, 0);
-                if (want_s) __builtin_amdgcn_raw_buffer_store_b64(u32x2{sa, sb}, rs, voff_a, soff, 0);
-            }
+            if (want_d) __builtin_amdgcn_raw_buffer_store_b64(u32x2{da, db}, r_d, voff_a, soff, 0);
+            if (want_s) __builtin_amdgcn_raw_buffer_store_b64(u32x2{sa, sb}, rs, voff_a, soff, 0);
         } else {
-            if (live_a) {
-                if (want_d) __builtin_amdgcn_raw_buffer_store_b32(da, r_d, voff_a, soff, 0);
-                if (want_s) __builtin_amdgcn_raw_buffer_store_b32(sa, rs, voff_a, soff, 0);
-            }
-            if (live_b) {
-                if (want_d) __builtin_amdgcn_raw_buffer_store_b32(db, r_d, voff_b, soff, 0);
-                if (want_s) __builtin_amdgcn_raw_buffer_store_b32(sb, rs, voff_b, soff, 0);
-            }
+            if (want_d) __builtin_amdgcn_raw_buffer_store_b32(da, r_d, voff_a, soff, 0);
+            if (want_s) __builtin_amdgcn_raw_buffer_store_b32(sa, rs, voff_a, soff, 0);
+            if (want_d) __builtin_amdgcn_raw_buffer_store_b32(db, r_d, voff_b, soff, 0);
+            if (want_s) __builtin_amdgcn_raw_buffer_store_b32(sb, rs, voff_b, soff, 0);
         }
-    };
-    constexpr int RB = 4;
-    for (int q0 = wv; q0 < n; q0 += kPairWaves * RB) {
-        u16x2 r[RB];
-#pragma unroll
-        for (int j = 0; j < RB; ++j) r[j] = as_pair(row0[min(q0 + kPairWaves * j, n - 1) * kRowW + lane]);
-#pragma unroll
-        for (int j = 0; j < RB; ++j)
-            if (q0 + kPairWaves * j < n) emit_row(q0 + kPairWaves * j, r[j]);
-    }
+    });
 }
 
 }  // namespace tmedt
