@@ -42,21 +42,25 @@ def source_digest():
 def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
     """Bytes one launch of kernel `name` must move (separable-pass model):
     the last-axis scan reads the 1-byte mask and writes the 4-byte field,
-    every envelope pass reads and writes the 4-byte field, and the final
-    pass reads the field and writes the outputs."""
-    if name.startswith("scan"):
+    every strided pass reads and writes the field, and the final pass reads
+    the field and writes the outputs.  A ".i16" / ".o16" suffix marks a
+    field read / written as 16-bit values (2 bytes per voxel)."""
+    base, *tags = name.split(".")
+    fin = 2 if "i16" in tags else 4          # field bytes read
+    fout = 2 if "o16" in tags else 4         # field bytes written
+    if base.startswith("scan"):
         return total * (1 + 4)
-    if name == "plane_pair":          # reads the mask, writes the field
-        return total * (1 + 4)
-    if name == "plane_pair_final":
+    if base == "plane_pair":                 # reads the mask, writes the field
+        return total * (1 + fout)
+    if base == "plane_pair_final":
         return total * (1 + out_bytes)
-    if name in ("fh_field", "tile_field", "tile_pair"):
+    if base in ("fh_field", "tile_field", "tile_pair"):
+        return total * (fin + fout)
+    if base in ("fh_field_final", "tile_field_final", "tile_pair_final"):
+        return total * (fin + out_bytes)
+    if base == "fh_index":
         return total * (4 + 4)
-    if name in ("fh_field_final", "tile_field_final", "tile_pair_final"):
-        return total * (4 + out_bytes)
-    if name == "fh_index":
-        return total * (4 + 4)
-    if name == "fh_index_final":
+    if base == "fh_index_final":
         return total * (4 + 4 * ndim + (out_bytes if want_idx else 0))
     raise KeyError(name)
 

@@ -401,21 +401,29 @@ int run(Request &r) {
                 tg.wall[b] = r.w[b];
             }
             const dim3 tgrid(uint32_t((lines + kPairLines - 1) / kPairLines)), tblock(kWave * kPairWaves);
+            // Launch names carry the field layout: ".i16" reads and ".o16"
+            // writes 16-bit runs (the measurement counts bytes from them).
+            static const char *const names[2][2][2][2] = {
+                {{{"tile_pair", "tile_pair.o16"}, {"tile_pair.i16", "tile_pair.i16.o16"}},
+                 {{"tile_pair_final", "tile_pair_final"}, {"tile_pair_final.i16", "tile_pair_final.i16"}}},
+                {{{"plane_pair", "plane_pair.o16"}, {"plane_pair", "plane_pair.o16"}},
+                 {{"plane_pair_final", "plane_pair_final"}, {"plane_pair_final", "plane_pair_final"}}}};
+            const char *nm = names[p.from_mask][fin][tg.in_seg][tg.out_seg];
             // search results stay in registers: 2 per lane and 16-row block
             if (n <= 128) {
                 if (p.from_mask)
-                    rc = fin ? launch("plane_pair_final", k_tile_pair<true, true, 8>, tgrid, tblock, p.lds, r.stream, tg)
-                             : launch("plane_pair", k_tile_pair<false, true, 8>, tgrid, tblock, p.lds, r.stream, tg);
+                    rc = fin ? launch(nm, k_tile_pair<true, true, 8>, tgrid, tblock, p.lds, r.stream, tg)
+                             : launch(nm, k_tile_pair<false, true, 8>, tgrid, tblock, p.lds, r.stream, tg);
                 else
-                    rc = fin ? launch("tile_pair_final", k_tile_pair<true, false, 8>, tgrid, tblock, p.lds, r.stream, tg)
-                             : launch("tile_pair", k_tile_pair<false, false, 8>, tgrid, tblock, p.lds, r.stream, tg);
+                    rc = fin ? launch(nm, k_tile_pair<true, false, 8>, tgrid, tblock, p.lds, r.stream, tg)
+                             : launch(nm, k_tile_pair<false, false, 8>, tgrid, tblock, p.lds, r.stream, tg);
             } else {
                 if (p.from_mask)
-                    rc = fin ? launch("plane_pair_final", k_tile_pair<true, true, 16>, tgrid, tblock, p.lds, r.stream, tg)
-                             : launch("plane_pair", k_tile_pair<false, true, 16>, tgrid, tblock, p.lds, r.stream, tg);
+                    rc = fin ? launch(nm, k_tile_pair<true, true, 16>, tgrid, tblock, p.lds, r.stream, tg)
+                             : launch(nm, k_tile_pair<false, true, 16>, tgrid, tblock, p.lds, r.stream, tg);
                 else
-                    rc = fin ? launch("tile_pair_final", k_tile_pair<true, false, 16>, tgrid, tblock, p.lds, r.stream, tg)
-                             : launch("tile_pair", k_tile_pair<false, false, 16>, tgrid, tblock, p.lds, r.stream, tg);
+                    rc = fin ? launch(nm, k_tile_pair<true, false, 16>, tgrid, tblock, p.lds, r.stream, tg)
+                             : launch(nm, k_tile_pair<false, false, 16>, tgrid, tblock, p.lds, r.stream, tg);
             }
         } else if (p.tiled) {
             TileArgs tg{};
