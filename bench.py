@@ -58,9 +58,9 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
         return total * (fin + fout)
     if base in ("fh_field_final", "tile_field_final", "tile_pair_final"):
         return total * (fin + out_bytes)
-    if base == "fh_index":
+    if base in ("fh_index", "tile_idx"):
         return total * (4 + 4)
-    if base == "fh_index_final":
+    if base in ("fh_index_final", "tile_idx_final"):
         return total * (4 + 4 * ndim + (out_bytes if want_idx else 0))
     raise KeyError(name)
 

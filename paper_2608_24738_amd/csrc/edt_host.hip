@@ -24,6 +24,7 @@
 #include "../../include/tm_edt.h"
 #include "edt_common.h"
 #include "edt_fh.h"
+#include "edt_tidx.h"
 #include "edt_scan.h"
 
 using namespace tmedt;
@@ -186,6 +187,8 @@ int run(Request &r) {
         bool tiled;      // staged tile + windowed search (k_tile_field)
         bool tiled16;    // paired 16-bit tile with guard rows (k_tile_pair)
         bool from_mask;  // tiled16 on axis ndim-2, computing the last-axis pass itself
+        bool tidx;       // tiled pass on the index carrier (k_tile_idx)
+        uint32_t rbits;  // tidx, unit sampling: bits of the row in a key
         uint32_t fbits;  // tiled: value bits of a tile word
         uint32_t cap;    // tiled: search steps before the envelope fallback
     } fh[kMaxDim] = {};
@@ -256,6 +259,21 @@ int run(Request &r) {
                 p.fbits = uint32_t(fbits);
                 p.cap = cap;
                 p.lds = tile;
+                continue;
+            }
+        }
+        // Index carrier, lines up to 256 rows: tiled windowed search.  Unit
+        // sampling packs (value, row) into one key below 2^31.
+        if (index_path && n <= 256) {
+            const size_t tb = size_t(2) * idx_tile_words(n) * 4;
+            int rb = bits_for(n - 1);
+            if (rb < 1) rb = 1;
+            const bool keys_fit = !r.unit || rb < 31 &&
+                ((fmax + uint64_t(n - 1) * (n - 1)) << rb | uint64_t(n - 1)) < (uint64_t(1) << 31);
+            if (tb + 1024 <= kLdsBytes && keys_fit && total / n + kWave < (uint64_t(1) << 32)) {
+                p.tidx = true;
+                p.rbits = uint32_t(rb);
+                p.lds = tb;
                 continue;
             }
         }
@@ -470,6 +488,33 @@ int run(Request &r) {
             else if (p.pack) rc = fin ? TM_FIELD(ArI64, true, true) : TM_FIELD(ArI64, true, false);
             else rc = fin ? TM_FIELD(ArI64, false, true) : TM_FIELD(ArI64, false, false);
 #undef TM_FIELD
+        } else if (p.tidx) {
+            IdxTileArgs x{};
+            x.idx = r.idx;
+            x.lines = uint32_t(lines);
+            x.lps = uint32_t(vox / n);
+            x.n = n;
+            x.inner = uint32_t(inner);
+            x.vox = uint32_t(vox);
+            x.rbits = p.rbits;
+            x.ndim = nd;
+            x.axis = a;
+            x.div_inner = Div32::make(uint32_t(inner));
+            x.div_lps = Div32::make(x.lps);
+            for (int b = 0; b < nd; ++b) {
+                x.div_shape[b] = Div32::make(r.shape[b]);
+                x.wall[b] = r.w[b];
+                x.shape[b] = r.shape[b];
+            }
+            x.dist = fin ? r.dist : nullptr;
+            x.sq = fin ? r.sq : nullptr;
+            const dim3 igrid(uint32_t((lines + kWave - 1) / kWave)), iblock(kWave * kIdxWaves);
+            if (r.unit)
+                rc = fin ? launch("tile_idx_final", k_tile_idx<false, true>, igrid, iblock, p.lds, r.stream, x)
+                         : launch("tile_idx", k_tile_idx<false, false>, igrid, iblock, p.lds, r.stream, x);
+            else
+                rc = fin ? launch("tile_idx_final", k_tile_idx<true, true>, igrid, iblock, p.lds, r.stream, x)
+                         : launch("tile_idx", k_tile_idx<true, false>, igrid, iblock, p.lds, r.stream, x);
         } else {
             IndexArgs x{};
             x.idx = r.idx;
