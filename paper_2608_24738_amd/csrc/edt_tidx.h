@@ -22,7 +22,7 @@
 
 namespace tmedt {
 
-constexpr int kIdxWaves = 8;
+constexpr int kIdxWaves = 16;
 constexpr int kIdxGuard = 4;       // guard rows of "no site" per side
 constexpr int kIdxRowW = kWave + 8;  // padded row stride (words)
 constexpr int kIdxPatch = 8;       // patch: 8 rows x 8 lines
@@ -52,7 +52,7 @@ __host__ __device__ constexpr uint32_t idx_tile_words(uint32_t n) { return (n + 
 template <bool SAMP, bool FINAL>
 __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
     extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
-    __shared__ __attribute__((aligned(8))) uint8_t any_site[kWave][kIdxWaves];   // [line][wave]
+    __shared__ __attribute__((aligned(16))) uint8_t any_site[kWave][kIdxWaves];   // [line][wave]
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
@@ -139,16 +139,18 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
     __syncthreads();
 
     // ---- search and output, patch by patch ----------------------------------
-    // Lane l takes row 8 rb + l / 8 of line 8 cb + l % 8, cb = (wv + rb) % 8.
+    // Patch p = (row block p / 8, line block (p + p / 8) % 8); lane l takes
+    // row 8 rb + l / 8 of line 8 cb + l % 8.
     const int pr = lane >> 3;
     const float w = float(a.wall[ax]);
     const uint32_t rmask = (1u << a.rbits) - 1u;
-    const int nrb = (n + kIdxPatch - 1) / kIdxPatch;
+    const int npatch = 8 * ((n + kIdxPatch - 1) / kIdxPatch);
     int32_t *slice0 = nullptr;
-    for (int rbk = 0; rbk < nrb; ++rbk) {
-        const int ln = kIdxPatch * ((wv + rbk) & (kIdxWaves - 1)) + (lane & 7);
-        const uint2 hv = *reinterpret_cast<const uint2 *>(&any_site[ln][0]);
-        const bool has = (hv.x | hv.y) != 0u;
+    for (int p = wv; p < npatch; p += kIdxWaves) {
+        const int rbk = p >> 3;
+        const int ln = kIdxPatch * ((p + rbk) & 7) + (lane & 7);
+        const uint4 hv = *reinterpret_cast<const uint4 *>(&any_site[ln][0]);
+        const bool has = (hv.x | hv.y | hv.z | hv.w) != 0u;
         const int qr = kIdxPatch * rbk + pr;
         const int q = min(qr, n - 1);
         const uint32_t *col = val0 + ln;
