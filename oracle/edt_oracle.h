@@ -52,6 +52,23 @@ int oracle_edt(const uint8_t *mask, int ndim, const int64_t *shape,
                int64_t *out_sq_i, double *out_sq_d, float *out_dist,
                int32_t *out_idx, int nthreads);
 
+/*
+ * oracle_dt_bf -- brute-force distance transform under a metric.
+ *
+ * metric    0 euclidean (value = squared distance sum_a s_a^2 d_a^2),
+ *           1 taxicab (sum_a s_a |d_a|), 2 chessboard (max_a s_a |d_a|).
+ * sampling  NULL (all ones) or ndim positive finite spacings.
+ * out_value NULL or [batch][voxels] double: the metric value to the nearest
+ *           background element.
+ * out_idx   NULL or [batch][ndim][voxels] int32: its coordinates (the
+ *           nearest one with the smallest row-major flat index).
+ * Other arguments, the virtual element for samples without background and
+ * the return codes are as for oracle_edt.  O(voxels x background) per sample.
+ */
+int oracle_dt_bf(const uint8_t *mask, int ndim, const int64_t *shape,
+                 int64_t batch, int metric, const double *sampling,
+                 double *out_value, int32_t *out_idx, int nthreads);
+
 /* Number of threads the OpenMP runtime would actually use for `nthreads`. */
 int oracle_threads_used(int nthreads);
 

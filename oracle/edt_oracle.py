@@ -44,6 +44,10 @@ class Oracle:
             ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
             ctypes.c_void_p, ctypes.c_int]
+        lib.oracle_dt_bf.restype = ctypes.c_int
+        lib.oracle_dt_bf.argtypes = [
+            ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
         lib.oracle_threads_used.restype = ctypes.c_int
         lib.oracle_threads_used.argtypes = [ctypes.c_int]
         self.lib = lib
@@ -96,6 +100,46 @@ class Oracle:
         }
 
 
+    def dt_bf(self, mask: np.ndarray, ndim: int | None = None, metric: str = "euclidean",
+              sampling=None, *, want_idx: bool = True, nthreads: int = 1) -> dict:
+        """Brute-force transform of ``mask`` (batch..., *spatial) under ``metric``
+        ("euclidean", "taxicab" or "chessboard").  Returns a dict with
+          ``value`` float64 metric value (euclidean: the squared distance),
+          ``dist``  float32 distance (euclidean: sqrt of the value, correctly
+                    rounded; the others: the value),
+          ``idx``   int32 coordinates (batch..., ndim, *spatial) or None."""
+        mask = np.ascontiguousarray(mask)
+        if mask.dtype != np.uint8:
+            mask = (mask != 0).astype(np.uint8)
+        if ndim is None:
+            ndim = mask.ndim - 1
+        code = METRICS[metric]
+        lead = mask.shape[:mask.ndim - ndim]
+        spatial = tuple(int(s) for s in mask.shape[mask.ndim - ndim:])
+        batch = int(np.prod(lead, dtype=np.int64))
+        vox = int(np.prod(spatial, dtype=np.int64))
+        samp = None
+        if sampling is not None:
+            samp = np.ascontiguousarray(
+                np.broadcast_to(np.asarray(sampling, dtype=np.float64), (ndim,)))
+        shape = np.asarray(spatial, dtype=np.int64)
+        value = np.empty((batch, vox), np.float64)
+        idx = np.empty((batch, ndim, vox), np.int32) if want_idx else None
+        rc = self.lib.oracle_dt_bf(_ptr(mask), ndim, _ptr(shape), batch, code, _ptr(samp),
+                                   _ptr(value), _ptr(idx), int(nthreads))
+        if rc != 0:
+            raise ValueError("oracle_dt_bf failed with code %d" % rc)
+        dist = (np.sqrt(value) if code == 0 else value).astype(np.float32)
+        return {
+            "value": value.reshape(lead + spatial),
+            "dist": dist.reshape(lead + spatial),
+            "idx": None if idx is None else idx.reshape(lead + (ndim,) + spatial),
+        }
+
+
+METRICS = {"euclidean": 0, "taxicab": 1, "chessboard": 2}
+
+
 def _ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
@@ -122,3 +166,7 @@ def threads_used(nthreads: int) -> int:
 
 def edt(mask, ndim=None, sampling=None, **kw) -> dict:
     return default().edt(mask, ndim, sampling, **kw)
+
+
+def dt_bf(mask, ndim=None, metric="euclidean", sampling=None, **kw) -> dict:
+    return default().dt_bf(mask, ndim, metric, sampling, **kw)
