@@ -112,6 +112,47 @@ def cpu_baseline(mask_np, ndim, sampling, budget_s=10.0):
             "single_thread_value": vox_per / dt1}
 
 
+def bench_bf(args, dev, stream):
+    """Brute-force transform: 8 x 256^2 images whose background is a seeded
+    1 % Bernoulli sample (the paper times its brute-force transform on 256^2
+    inputs); metric from --metric, float32 distances and int32 indices."""
+    import numpy as np
+    import torch
+
+    from paper_2608_24738_amd import binding
+    batch, n = 8, 256
+    rng = np.random.default_rng([260824738, 99])
+    mask = (rng.random((batch, 1, n, n)) >= 0.01).astype(np.uint8)
+    x = torch.from_numpy(mask).to(dev)
+    dist = torch.empty(mask.shape, dtype=torch.float32, device=dev)
+    idx = torch.empty((batch, 1, 2, n, n), dtype=torch.int32, device=dev)
+    code = binding.METRICS[args.metric]
+
+    def step():
+        binding.tm_dt_bf(x, 2, code, None, dist, idx, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    zeros = int((mask == 0).sum())
+    pairs = zeros * n * n                       # (element, background element) pairs per step
+    print(json.dumps({
+        "metric": "brute-force DT inputs/ms (%s), batch 8x1x256^2" % args.metric,
+        "value": batch / ms, "unit": "inputs/ms", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "int32", "data": "synthetic",
+        "config": {"workload": "bf2d_8x256x256_bernoulli1pct", "metric": args.metric,
+                   "outputs": "float32 distances + int32 indices"},
+        "pair_evaluations_per_s": pairs / (ms * 1e-3)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -121,6 +162,10 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run only a plain 256 MiB device copy (counter calibration)")
+    ap.add_argument("--op", default="edt", choices=["edt", "bf"],
+                    help="edt: the exact transform (headline); bf: the brute-force transform")
+    ap.add_argument("--metric", default="euclidean", choices=["euclidean", "taxicab", "chessboard"],
+                    help="metric of --op bf")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -150,6 +195,8 @@ def main():
     if not os.path.exists(binding.LIB_PATH):
         hip_build.build()
     binding.load()
+    if args.op == "bf":
+        return bench_bf(args, dev, stream)
 
     w = workloads.WORKLOADS[args.workload]
     log("generating %s" % w.name)

@@ -59,7 +59,8 @@ typedef enum {
                                 or (unit sampling) squared distances may exceed int32 */
     TM_ERR_ALIAS = -8,       /* two of the buffers overlap */
     TM_ERR_UNSUPPORTED = -9, /* a line is longer than the envelope kernels hold in LDS */
-    TM_ERR_HIP = -10         /* the HIP runtime reported an error while enqueuing */
+    TM_ERR_HIP = -10,        /* the HIP runtime reported an error while enqueuing */
+    TM_ERR_METRIC = -11      /* metric is not one of tm_metric */
 } tm_status;
 
 /*
@@ -108,6 +109,31 @@ const char *tm_strerror(int status);
 int tm_prof_enable(int max_kernels);
 int tm_prof_count(void);
 int tm_prof_read(int i, const char **name, float *ms);
+
+/* Metrics of the brute-force transform (paper, Section 2.3.2). */
+typedef enum {
+    TM_METRIC_EUCLIDEAN = 0,   /* sqrt( sum_a (s_a (x_a - y_a))^2 ) */
+    TM_METRIC_TAXICAB = 1,     /* sum_a s_a |x_a - y_a| */
+    TM_METRIC_CHESSBOARD = 2   /* max_a s_a |x_a - y_a| */
+} tm_metric;
+
+/*
+ * tm_dt_bf -- brute-force distance transform (paper, Section 2.3.2: the
+ * transform that checks the separable ones, templated over metric and rank,
+ * and the only route to anisotropic taxicab and chessboard distances).
+ *
+ * For every element, the nearest background element of its sample under
+ * `metric`, found by visiting every background element: O(elements x
+ * background elements) per sample, meant for moderate sizes.  out_dist (may
+ * be NULL) receives the distance as float32 (euclidean: the correctly
+ * rounded square root of the exact squared distance under unit sampling);
+ * out_idx (may be NULL) the coordinates, [batch][ndim][shape...].  sampling
+ * as for tm_edt (NULL = all ones, exact integer arithmetic; otherwise float).
+ * Ties, the virtual element and the other conventions are those above.
+ * Errors: as tm_edt, plus TM_ERR_METRIC for an unknown metric.
+ */
+int tm_dt_bf(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, int metric,
+             const double *sampling, float *out_dist, int32_t *out_idx, hipStream_t stream);
 
 /*
  * tm_selftest_host -- checks the host-side planning arithmetic (the

@@ -5,9 +5,10 @@ turns torch tensors into device pointers, shapes and the current HIP stream,
 and turns status codes into exceptions.  There is no fallback: if the library
 is missing, every call raises.
 
-Entry points with the C names (``tm_edt``, ``tm_edt_sq``, ``tm_strerror``)
-plus a ``scipy.ndimage.distance_transform_edt``-style wrapper over
-(B, C, *spatial) tensors (paper, Section 2.2.1).
+Entry points with the C names (``tm_edt``, ``tm_edt_sq``, ``tm_dt_bf``,
+``tm_strerror``) plus ``scipy.ndimage``-style wrappers
+(``distance_transform_edt``, ``distance_transform_bf``) over (B, C, *spatial)
+tensors (paper, Section 2.2.1).
 """
 from __future__ import annotations
 
@@ -46,6 +47,8 @@ def load() -> ctypes.CDLL:
             lib.tm_edt.argtypes = [vp, i32, vp, i64, vp, vp, vp, vp]
             lib.tm_edt_sq.restype = i32
             lib.tm_edt_sq.argtypes = [vp, i32, vp, i64, vp, vp, vp]
+            lib.tm_dt_bf.restype = i32
+            lib.tm_dt_bf.argtypes = [vp, i32, vp, i64, i32, vp, vp, vp, vp]
             lib.tm_strerror.restype = ctypes.c_char_p
             lib.tm_strerror.argtypes = [i32]
             lib.tm_prof_enable.restype = i32
@@ -138,6 +141,29 @@ def tm_edt_sq(in_u8: torch.Tensor, ndim: int, out_sq=None, out_idx=None, stream=
         raise TMError(rc, "tm_edt_sq")
 
 
+METRICS = {"euclidean": 0, "taxicab": 1, "chessboard": 2}
+
+
+def tm_dt_bf(in_u8: torch.Tensor, ndim: int, metric: int, sampling=None, out_dist=None,
+             out_idx=None, stream=None) -> None:
+    """Calls tm_dt_bf (brute-force transform, metric code 0/1/2)."""
+    _check_mask(in_u8)
+    spatial, batch = _shape_args(in_u8, ndim)
+    vox = in_u8.numel() // max(batch, 1)
+    _check_out(out_dist, torch.float32, batch * vox, "out_dist", in_u8.device)
+    _check_out(out_idx, torch.int32, batch * vox * ndim, "out_idx", in_u8.device)
+    shape = (ctypes.c_int64 * ndim)(*spatial)
+    samp = None
+    if sampling is not None:
+        samp = (ctypes.c_double * ndim)(*[float(s) for s in sampling])
+    with torch.cuda.device(in_u8.device):
+        st = _stream_handle(stream)
+        rc = load().tm_dt_bf(_ptr(in_u8), ndim, shape, batch, int(metric), samp, _ptr(out_dist),
+                             _ptr(out_idx), ctypes.c_void_p(st))
+    if rc != TM_OK:
+        raise TMError(rc, "tm_dt_bf")
+
+
 def _normalise_sampling(sampling, ndim):
     if sampling is None:
         return None
@@ -204,6 +230,33 @@ def distance_transform_edt(input: torch.Tensor, sampling=None, return_distances:
     if not result:
         return None
     return result[0] if len(result) == 1 else tuple(result)
+
+
+def distance_transform_bf(input: torch.Tensor, metric: str = "euclidean", sampling=None,
+                          return_distances: bool = True, return_indices: bool = False):
+    """``scipy.ndimage.distance_transform_bf``-style brute-force transform of a
+    (B, C, *spatial) batch under "euclidean", "taxicab" or "chessboard"
+    (sampling applies to every metric).  Returns float32 distances and/or
+    int32 indices (B, C, len(S), *S)."""
+    if input.dim() < 3:
+        raise ValueError("input must be (B, C, *spatial) with 1 to 8 spatial dimensions")
+    ndim = input.dim() - 2
+    if not (return_distances or return_indices):
+        raise RuntimeError("at least one of return_distances/return_indices must be True")
+    if metric not in METRICS:
+        raise ValueError("metric must be one of %s" % sorted(METRICS))
+    samp = _normalise_sampling(sampling, ndim)
+    mask = _as_mask(input)
+    dev = mask.device
+    dist = torch.empty(mask.shape, dtype=torch.float32, device=dev) if return_distances else None
+    idx = None
+    if return_indices:
+        idx = torch.empty(tuple(mask.shape[:2]) + (ndim,) + tuple(mask.shape[2:]),
+                          dtype=torch.int32, device=dev)
+    tm_dt_bf(mask, ndim, METRICS[metric], samp, dist, idx)
+    if dist is not None and idx is not None:
+        return dist, idx
+    return dist if dist is not None else idx
 
 
 def distance_transform_edt_sq(input: torch.Tensor, return_indices: bool = False):

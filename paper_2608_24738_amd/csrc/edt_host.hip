@@ -23,6 +23,7 @@
 
 #include "../../include/tm_edt.h"
 #include "edt_common.h"
+#include "edt_bf.h"
 #include "edt_fh.h"
 #include "edt_tidx.h"
 #include "edt_scan.h"
@@ -576,6 +577,44 @@ extern "C" int tm_edt_sq(const uint8_t *in_u8, int ndim, const int64_t *shape, i
     return run(r);
 }
 
+extern "C" int tm_dt_bf(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, int metric,
+                        const double *sampling, float *out_dist, int32_t *out_idx, hipStream_t stream) {
+    Request r{};
+    int rc = validate(in_u8, ndim, shape, batch, sampling, out_dist, out_idx, nullptr, r);
+    if (rc != TM_OK) return rc;
+    if (metric < TM_METRIC_EUCLIDEAN || metric > TM_METRIC_CHESSBOARD) return TM_ERR_METRIC;
+    uint64_t vox = 1;
+    for (int a = 0; a < ndim; ++a) vox *= r.shape[a];
+    const uint64_t total = r.batch * vox;
+    if (overlaps(in_u8, total, out_dist, 4 * total) || overlaps(in_u8, total, out_idx, 4 * total * ndim) ||
+        overlaps(out_dist, 4 * total, out_idx, 4 * total * ndim))
+        return TM_ERR_ALIAS;
+    BfArgs x{};
+    x.in = in_u8;
+    x.dist = out_dist;
+    x.idx = out_idx;
+    x.vox = uint32_t(vox);
+    x.bps = uint32_t((vox + kBfOut - 1) / kBfOut);
+    if (uint64_t(x.bps) * r.batch >= (uint64_t(1) << 31)) return TM_ERR_TOO_LARGE;
+    x.ndim = ndim;
+    for (int a = 0; a < ndim; ++a) {
+        x.div_shape[a] = Div32::make(r.shape[a]);
+        x.sd[a] = sampling ? sampling[a] : 1.0;
+        x.s[a] = float(x.sd[a]);
+    }
+    const dim3 grid(uint32_t(x.bps * r.batch)), block(kBfThreads);
+    const bool samp = !r.unit;
+#define TM_BF(M, S)                                                                               \
+    (ndim == 2   ? launch("dt_bf", k_dt_bf<M, S, 2>, grid, block, 0, stream, x)                   \
+     : ndim == 3 ? launch("dt_bf", k_dt_bf<M, S, 3>, grid, block, 0, stream, x)                   \
+                 : launch("dt_bf", k_dt_bf<M, S, 0>, grid, block, 0, stream, x))
+    if (metric == TM_METRIC_EUCLIDEAN) rc = samp ? TM_BF(0, true) : TM_BF(0, false);
+    else if (metric == TM_METRIC_TAXICAB) rc = samp ? TM_BF(1, true) : TM_BF(1, false);
+    else rc = samp ? TM_BF(2, true) : TM_BF(2, false);
+#undef TM_BF
+    return rc;
+}
+
 extern "C" const char *tm_strerror(int status) {
     switch (status) {
         case TM_OK: return "success";
@@ -589,6 +628,7 @@ extern "C" const char *tm_strerror(int status) {
         case TM_ERR_ALIAS: return "input and output buffers overlap";
         case TM_ERR_UNSUPPORTED: return "a line is longer than the envelope stack held in LDS";
         case TM_ERR_HIP: return "HIP runtime error while enqueuing kernels";
+        case TM_ERR_METRIC: return "metric must be euclidean, taxicab or chessboard";
         default: return "unknown status";
     }
 }

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 TM_OK, TM_ERR_NDIM, TM_ERR_SHAPE, TM_ERR_BATCH, TM_ERR_NULL = 0, -1, -2, -3, -4
 TM_ERR_NO_OUTPUT, TM_ERR_SAMPLING, TM_ERR_TOO_LARGE, TM_ERR_ALIAS = -5, -6, -7, -8
-TM_ERR_UNSUPPORTED, TM_ERR_HIP = -9, -10
+TM_ERR_UNSUPPORTED, TM_ERR_HIP, TM_ERR_METRIC = -9, -10, -11
 
 FAKE_IN = 0x100000           # never dereferenced: every call below fails validation
 FAKE_OUT = 0x40000000
@@ -38,7 +38,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert {"tm_edt", "tm_edt_sq", "tm_strerror"} <= set(names)
+    assert {"tm_edt", "tm_edt_sq", "tm_dt_bf", "tm_strerror"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -48,7 +48,7 @@ def test_host_division_constants(lib):
 
 
 def test_strerror_covers_every_status(lib):
-    for s in range(0, -11, -1):
+    for s in range(0, -12, -1):
         msg = binding.tm_strerror(s)
         assert msg and msg != "unknown status", s
     assert binding.tm_strerror(-99) == "unknown status"
@@ -121,3 +121,19 @@ def test_binding_rejects_bad_python_arguments():
         binding.distance_transform_edt(x.float())
     with pytest.raises(ValueError):
         binding.distance_transform_edt(torch.zeros((4, 4), dtype=torch.uint8))
+
+
+def call_bf(lib, shape, metric=0, batch=1, sampling=None, inp=FAKE_IN, dist=FAKE_OUT, idx=None):
+    sh = (ctypes.c_int64 * len(shape))(*shape)
+    samp = (ctypes.c_double * len(sampling))(*sampling) if sampling is not None else None
+    return lib.tm_dt_bf(ctypes.c_void_p(inp), len(shape), sh, batch, metric, samp,
+                        dist and ctypes.c_void_p(dist), idx and ctypes.c_void_p(idx), None)
+
+
+def test_brute_force_argument_checks(lib):
+    assert call_bf(lib, [4, 4], metric=3) == TM_ERR_METRIC
+    assert call_bf(lib, [4, 4], metric=-1) == TM_ERR_METRIC
+    assert call_bf(lib, [4, 4], dist=0) == TM_ERR_NO_OUTPUT
+    assert call_bf(lib, [4, 0]) == TM_ERR_SHAPE
+    assert call_bf(lib, [4, 4], sampling=[1.0, 0.0]) == TM_ERR_SAMPLING
+    assert call_bf(lib, [16, 16], dist=FAKE_IN + 8) == TM_ERR_ALIAS
