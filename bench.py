@@ -50,13 +50,15 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
     fout = 2 if "o16" in tags else 4         # field bytes written
     if base.startswith("scan"):
         return total * (1 + 4)
-    if base == "plane_pair":                 # reads the mask, writes the field
+    if base in ("plane_pair", "cdt_plane"):  # reads the mask, writes the field
         return total * (1 + fout)
-    if base == "plane_pair_final":
+    if base in ("plane_pair_final", "cdt_plane_final"):
         return total * (1 + out_bytes)
-    if base in ("fh_field", "tile_field", "tile_pair"):
+    if base in ("fh_field", "tile_field", "tile_pair", "cdt_pair", "cdt_line", "cdt_none",
+                "line_search"):
         return total * (fin + fout)
-    if base in ("fh_field_final", "tile_field_final", "tile_pair_final"):
+    if base in ("fh_field_final", "tile_field_final", "tile_pair_final", "cdt_pair_final",
+                "cdt_line_final", "line_search_final"):
         return total * (fin + out_bytes)
     if base in ("fh_index", "tile_idx"):
         return total * (4 + 4)
@@ -112,17 +114,105 @@ def cpu_baseline(mask_np, ndim, sampling, budget_s=10.0):
             "single_thread_value": vox_per / dt1}
 
 
+def time_op(step, args, stream):
+    """Warm up, time args.steps steps between two events on `stream`, then
+    time every kernel of the same number of steps with the library's own
+    per-launch events.  Returns (ms per step, {kernel: {avg_ms, launches}})."""
+    import torch
+
+    from paper_2608_24738_amd import binding
+    log("warmup %d" % args.warmup)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("timing %d steps" % args.steps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    log("timing kernels over %d steps" % args.steps)
+    binding.prof_enable(8 * args.steps)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    per = {}
+    for name, t in binding.prof_read():
+        per.setdefault(name, []).append(t)
+    binding.prof_enable(0)
+    kernels = {k: {"avg_ms": sum(v) / len(v), "launches": len(v)} for k, v in per.items()}
+    return ms, kernels
+
+
+def roofline_of(kernels, steps, total, ndim, want_idx, workload_name, out_bytes=4):
+    """Roofline entry of the kernel with the largest share of the step, and
+    per-kernel algorithmic rates (kernels is updated in place)."""
+    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
+    dom_launches_per_step = kernels[dom]["launches"] / steps
+    algo = algorithmic_bytes(dom, total, ndim, want_idx, out_bytes)
+    achieved = algo / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
+    for k, v in kernels.items():
+        b = algorithmic_bytes(k, total, ndim, want_idx, out_bytes)
+        v["algorithmic_bytes"] = b
+        v["achieved_GBs"] = round(b / (v["avg_ms"] * 1e-3) / 1e9, 1)
+        v["avg_ms"] = round(v["avg_ms"], 5)
+        v["launches"] = int(v["launches"] / steps)
+    traffic = read_counters(dom, workload_name)
+    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "kernel": dom, "launches_per_step": dom_launches_per_step}
+
+
+def bench_cdt(args, dev, stream):
+    """Chamfer transform (taxicab or chessboard from --metric, default
+    chessboard) of workload 7 (8 x 1024^2) or 8 (8 x 256^2), the two sizes the
+    paper's throughput table times it on; int32 distances."""
+    import torch
+
+    from paper_2608_24738_amd import binding, workloads
+    key = args.workload if args.workload in (7, 8) else 7
+    metric = args.metric if args.metric != "euclidean" else "chessboard"
+    w = workloads.WORKLOADS[key]
+    log("generating %s" % w.name)
+    mask = workloads.make_mask(key)
+    x = torch.from_numpy(mask).to(dev)
+    out = torch.empty(mask.shape, dtype=torch.int32, device=dev)
+    code = binding.METRICS[metric]
+
+    def step():
+        binding.tm_cdt(x, w.ndim, code, out, stream=stream)
+
+    ms, kernels = time_op(step, args, stream)
+    total = int(mask.size)
+    roofline = roofline_of(kernels, args.steps, total, w.ndim, False, w.name)
+    print(json.dumps({
+        "metric": "chamfer DT inputs/ms (%s), batch %dx1x%s" % (metric, w.batch,
+                                                                "x".join(map(str, w.spatial))),
+        "value": w.batch / ms, "unit": "inputs/ms", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "int32", "data": "synthetic",
+        "config": {"workload": w.name, "metric": metric, "outputs": "int32 distances",
+                   "mask_sha256": workloads.mask_digest(mask)[:16]},
+        "voxels_per_s": total / (ms * 1e-3),
+        "roofline": roofline,
+        "kernels": kernels,
+        "source_digest": source_digest()}), flush=True)
+
+
 def bench_bf(args, dev, stream):
     """Brute-force transform: 8 x 256^2 images whose background is a seeded
     1 % Bernoulli sample (the paper times its brute-force transform on 256^2
     inputs); metric from --metric, float32 distances and int32 indices."""
-    import numpy as np
     import torch
 
     from paper_2608_24738_amd import binding
-    batch, n = 8, 256
-    rng = np.random.default_rng([260824738, 99])
-    mask = (rng.random((batch, 1, n, n)) >= 0.01).astype(np.uint8)
+    from paper_2608_24738_amd import workloads
+    w = workloads.WORKLOADS[6]
+    batch, n = w.batch, w.spatial[0]
+    mask = workloads.make_mask(6)
     x = torch.from_numpy(mask).to(dev)
     dist = torch.empty(mask.shape, dtype=torch.float32, device=dev)
     idx = torch.empty((batch, 1, 2, n, n), dtype=torch.int32, device=dev)
@@ -148,7 +238,7 @@ def bench_bf(args, dev, stream):
         "value": batch / ms, "unit": "inputs/ms", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "int32", "data": "synthetic",
-        "config": {"workload": "bf2d_8x256x256_bernoulli1pct", "metric": args.metric,
+        "config": {"workload": w.name, "metric": args.metric,
                    "outputs": "float32 distances + int32 indices"},
         "pair_evaluations_per_s": pairs / (ms * 1e-3)}), flush=True)
 
@@ -158,14 +248,16 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", type=int, default=3, help="workload key 1-5 (3 = headline)")
+    ap.add_argument("--workload", type=int, default=3,
+                    help="workload key: 1-5 and 9 edt (3 = headline), 7-8 cdt")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run only a plain 256 MiB device copy (counter calibration)")
-    ap.add_argument("--op", default="edt", choices=["edt", "bf"],
-                    help="edt: the exact transform (headline); bf: the brute-force transform")
+    ap.add_argument("--op", default="edt", choices=["edt", "bf", "cdt"],
+                    help="edt: the exact transform (headline); bf: the brute-force transform; "
+                         "cdt: the chamfer transform (workload 7 or 8)")
     ap.add_argument("--metric", default="euclidean", choices=["euclidean", "taxicab", "chessboard"],
-                    help="metric of --op bf")
+                    help="metric of --op bf / cdt (cdt: euclidean means chessboard)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -197,6 +289,8 @@ def main():
     binding.load()
     if args.op == "bf":
         return bench_bf(args, dev, stream)
+    if args.op == "cdt":
+        return bench_cdt(args, dev, stream)
 
     w = workloads.WORKLOADS[args.workload]
     log("generating %s" % w.name)
@@ -213,48 +307,10 @@ def main():
     def step():
         binding.tm_edt(x, ndim, samp, dist, idx, stream=stream)
 
-    log("warmup %d" % args.warmup)
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    log("timing %d steps" % args.steps)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
-
     # per-kernel durations: HIP events recorded by the library around each of
     # its launches, on the launch stream, over the same number of steps
-    log("timing kernels over %d steps" % args.steps)
-    binding.prof_enable(8 * args.steps)
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    per = {}
-    for name, t in binding.prof_read():
-        per.setdefault(name, []).append(t)
-    binding.prof_enable(0)
-    kernels = {k: {"avg_ms": sum(v) / len(v), "launches": len(v)} for k, v in per.items()}
-    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
-    dom_launches_per_step = kernels[dom]["launches"] / args.steps
-    algo = algorithmic_bytes(dom, total, ndim, w.want_idx)
-    achieved = algo / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
-    for k, v in kernels.items():
-        b = algorithmic_bytes(k, total, ndim, w.want_idx)
-        v["algorithmic_bytes"] = b
-        v["achieved_GBs"] = round(b / (v["avg_ms"] * 1e-3) / 1e9, 1)
-        v["avg_ms"] = round(v["avg_ms"], 5)
-        v["launches"] = int(v["launches"] / args.steps)
-
-    traffic = read_counters(dom, w.name)
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": dom, "launches_per_step": dom_launches_per_step}
+    ms, kernels = time_op(step, args, stream)
+    roofline = roofline_of(kernels, args.steps, total, ndim, w.want_idx, w.name)
 
     cpu = None
     if not args.no_cpu:
@@ -263,7 +319,8 @@ def main():
 
     vox_s = total / (ms * 1e-3)
     out = {
-        "metric": "EDT voxels/sec and achieved HBM GB/s (% of peak), batch 8x1x128^3",
+        "metric": ("EDT voxels/sec and achieved HBM GB/s (% of peak), batch 8x1x128^3"
+                   if args.workload == 3 else "EDT voxels/sec, %s" % w.name),
         "value": vox_s,
         "unit": "voxels/s",
         "n_gpus": 1,
@@ -282,6 +339,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,
+        "inputs_per_ms": w.batch / ms,
         "model_GBs_per_step": round(sum(v["algorithmic_bytes"] * v["launches"]
                                         for v in kernels.values()) / (ms * 1e-3) / 1e9, 1),
         "source_digest": source_digest(),

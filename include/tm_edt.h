@@ -136,6 +136,27 @@ int tm_dt_bf(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch
              const double *sampling, float *out_dist, int32_t *out_idx, hipStream_t stream);
 
 /*
+ * tm_cdt -- chamfer distance transform (paper, Section 2.3.2 and Table 1:
+ * the taxicab and chessboard transforms, with no sampling argument).
+ *
+ * For every element of each sample, the distance to the nearest background
+ * element under `metric` (TM_METRIC_TAXICAB: sum of |x_a - y_a|;
+ * TM_METRIC_CHESSBOARD: max of |x_a - y_a|), on the unit grid.  This is
+ * what a chamfer sweep with unit weights over the face neighbours (taxicab)
+ * or all 3^ndim - 1 neighbours (chessboard) computes, and the result is
+ * exact in int32.  A sample with no background gets -1 everywhere (nothing
+ * is reachable).  in_u8, ndim, shape, batch as for tm_edt.  out_dist:
+ * device int32 [batch][shape...], written completely, not aliasing in_u8.
+ * Errors: as tm_edt_sq (TM_ERR_NO_OUTPUT for a NULL out_dist), plus
+ * TM_ERR_METRIC for TM_METRIC_EUCLIDEAN or an unknown metric, and
+ * TM_ERR_UNSUPPORTED for lines longer than the kernels take along an axis
+ * other than the last (about 20000 elements while every distance fits 16
+ * bits, else about 10000).
+ */
+int tm_cdt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, int metric,
+           int32_t *out_dist, hipStream_t stream);
+
+/*
  * tm_selftest_host -- checks the host-side planning arithmetic (the
  * division-by-invariant-integer constants the kernels use to split flat
  * indices) without touching any GPU.  Returns TM_OK or a negative count of

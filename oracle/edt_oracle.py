@@ -4,7 +4,9 @@ Test infrastructure only (tests, smoke check, CPU-baseline timing); it imports
 nothing from the GPU library.  What the oracle computes is documented in
 ``edt_oracle.c``: the exact Euclidean distance transform by the separable
 lower-envelope method of the paper's Section 2.3.2, in int64 arithmetic for
-unit sampling and in double otherwise.
+unit sampling and in double otherwise, and the brute-force transform under
+the euclidean, taxicab and chessboard metrics.  The chamfer transform and the
+point-wise spot check below are plain numpy over the brute-force values.
 """
 from __future__ import annotations
 
@@ -137,6 +139,52 @@ class Oracle:
         }
 
 
+    def cdt(self, mask: np.ndarray, ndim: int | None = None, metric: str = "chessboard", *,
+            nthreads: int = 1) -> np.ndarray:
+        """Chamfer transform (paper, Section 2.3.2; Table 1 lists it as exact):
+        for metric "taxicab" or "chessboard", the int32 distance from every
+        element to the nearest background element of its sample, which is the
+        brute-force value above, and -1 throughout a sample with no background
+        (a unit-weight chamfer sweep reaches nothing there)."""
+        if metric not in ("taxicab", "chessboard"):
+            raise ValueError(metric)
+        mask = np.ascontiguousarray(mask)
+        if ndim is None:
+            ndim = mask.ndim - 1
+        value = self.dt_bf(mask, ndim, metric, want_idx=False, nthreads=nthreads)["value"]
+        lead = mask.shape[:mask.ndim - ndim]
+        flat = value.reshape(int(np.prod(lead, dtype=np.int64)), -1)
+        out = flat.astype(np.int64)
+        has_bg = (mask.reshape(flat.shape) == 0).any(axis=1)
+        out[~has_bg] = -1
+        return out.astype(np.int32).reshape(mask.shape)
+
+
+def metric_dt_at(sample: np.ndarray, metric: str, points: np.ndarray) -> np.ndarray:
+    """The metric value (euclidean: squared distance) from each of `points`
+    (k x ndim integer coordinates) to the nearest background element of one
+    unit-sampled sample, by visiting every background element: the definition
+    of the transform, for spot checks at sizes where the whole brute-force
+    transform is too slow.  NaN where the sample has no background."""
+    z = np.argwhere(np.asarray(sample) == 0).astype(np.int64)
+    pts = np.asarray(points, dtype=np.int64)
+    out = np.full(len(pts), np.nan)
+    if len(z) == 0:
+        return out
+    for i0 in range(0, len(pts), 64):
+        d = np.abs(pts[i0:i0 + 64, None, :] - z[None, :, :])
+        if metric == "euclidean":
+            v = (d * d).sum(axis=2)
+        elif metric == "taxicab":
+            v = d.sum(axis=2)
+        elif metric == "chessboard":
+            v = d.max(axis=2)
+        else:
+            raise ValueError(metric)
+        out[i0:i0 + 64] = v.min(axis=1)
+    return out
+
+
 METRICS = {"euclidean": 0, "taxicab": 1, "chessboard": 2}
 
 
@@ -170,3 +218,7 @@ def edt(mask, ndim=None, sampling=None, **kw) -> dict:
 
 def dt_bf(mask, ndim=None, metric="euclidean", sampling=None, **kw) -> dict:
     return default().dt_bf(mask, ndim, metric, sampling, **kw)
+
+
+def cdt(mask, ndim=None, metric="chessboard", **kw) -> np.ndarray:
+    return default().cdt(mask, ndim, metric, **kw)

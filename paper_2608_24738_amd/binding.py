@@ -6,9 +6,10 @@ and turns status codes into exceptions.  There is no fallback: if the library
 is missing, every call raises.
 
 Entry points with the C names (``tm_edt``, ``tm_edt_sq``, ``tm_dt_bf``,
-``tm_strerror``) plus ``scipy.ndimage``-style wrappers
-(``distance_transform_edt``, ``distance_transform_bf``) over (B, C, *spatial)
-tensors (paper, Section 2.2.1).
+``tm_cdt``, ``tm_strerror``) plus ``scipy.ndimage``-style wrappers
+(``distance_transform_edt``, ``distance_transform_bf``,
+``distance_transform_cdt``) over (B, C, *spatial) tensors (paper, Section
+2.2.1).
 """
 from __future__ import annotations
 
@@ -49,6 +50,8 @@ def load() -> ctypes.CDLL:
             lib.tm_edt_sq.argtypes = [vp, i32, vp, i64, vp, vp, vp]
             lib.tm_dt_bf.restype = i32
             lib.tm_dt_bf.argtypes = [vp, i32, vp, i64, i32, vp, vp, vp, vp]
+            lib.tm_cdt.restype = i32
+            lib.tm_cdt.argtypes = [vp, i32, vp, i64, i32, vp, vp]
             lib.tm_strerror.restype = ctypes.c_char_p
             lib.tm_strerror.argtypes = [i32]
             lib.tm_prof_enable.restype = i32
@@ -164,6 +167,21 @@ def tm_dt_bf(in_u8: torch.Tensor, ndim: int, metric: int, sampling=None, out_dis
         raise TMError(rc, "tm_dt_bf")
 
 
+def tm_cdt(in_u8: torch.Tensor, ndim: int, metric: int, out_dist, stream=None) -> None:
+    """Calls tm_cdt (chamfer transform, metric code 1 taxicab / 2 chessboard)."""
+    _check_mask(in_u8)
+    spatial, batch = _shape_args(in_u8, ndim)
+    vox = in_u8.numel() // max(batch, 1)
+    _check_out(out_dist, torch.int32, batch * vox, "out_dist", in_u8.device)
+    shape = (ctypes.c_int64 * ndim)(*spatial)
+    with torch.cuda.device(in_u8.device):
+        st = _stream_handle(stream)
+        rc = load().tm_cdt(_ptr(in_u8), ndim, shape, batch, int(metric), _ptr(out_dist),
+                           ctypes.c_void_p(st))
+    if rc != TM_OK:
+        raise TMError(rc, "tm_cdt")
+
+
 def _normalise_sampling(sampling, ndim):
     if sampling is None:
         return None
@@ -257,6 +275,27 @@ def distance_transform_bf(input: torch.Tensor, metric: str = "euclidean", sampli
     if dist is not None and idx is not None:
         return dist, idx
     return dist if dist is not None else idx
+
+
+def distance_transform_cdt(input: torch.Tensor, metric: str = "chessboard", distances=None):
+    """``scipy.ndimage.distance_transform_cdt`` over a (B, C, *spatial) batch
+    for metric "chessboard" or "taxicab": int32 distances, -1 throughout a
+    sample with no background.  A pre-allocated ``distances`` is filled in
+    place and not returned."""
+    if input.dim() < 3:
+        raise ValueError("input must be (B, C, *spatial) with 1 to 8 spatial dimensions")
+    ndim = input.dim() - 2
+    if metric not in ("chessboard", "taxicab"):
+        raise ValueError("metric must be 'chessboard' or 'taxicab'")
+    mask = _as_mask(input)
+    if distances is not None:
+        if distances.shape != mask.shape or distances.dtype != torch.int32:
+            raise RuntimeError("distances array has wrong shape or type")
+        out = distances
+    else:
+        out = torch.empty(mask.shape, dtype=torch.int32, device=mask.device)
+    tm_cdt(mask, ndim, METRICS[metric], out)
+    return None if distances is not None else out
 
 
 def distance_transform_edt_sq(input: torch.Tensor, return_indices: bool = False):

@@ -727,6 +727,22 @@ __device__ __forceinline__ bool stopped(u16x2 best, int d) {
     return as_word(__builtin_elementwise_sub_sat(best, splat(lim))) == 0;
 }
 
+// Metrics of the paired search: 0 squared euclidean (candidate f + d^2),
+// 1 taxicab (f + d), 2 chessboard (max(f, d)); "no site" (0xffff) absorbs.
+constexpr int kL2 = 0, kL1 = 1, kLinf = 2;
+template <int METRIC>
+__device__ __forceinline__ u16x2 cand(u16x2 m, int d) {
+    if constexpr (METRIC == kL2) return __builtin_elementwise_add_sat(m, splat(d * d >= kNone16 ? kNone16 : d * d));
+    else if constexpr (METRIC == kL1) return __builtin_elementwise_add_sat(m, splat(d >= kNone16 ? kNone16 : d));
+    else return __builtin_elementwise_max(m, splat(d >= kNone16 ? kNone16 : d));
+}
+// true when no row at distance >= d can lower either half of `best`
+template <int METRIC>
+__device__ __forceinline__ bool stop_at(u16x2 best, int d) {
+    if constexpr (METRIC == kL2) return stopped(best, d);
+    else return as_word(__builtin_elementwise_sub_sat(best, splat(d >= kNone16 ? kNone16 : d))) == 0;
+}
+
 // Search blocks BLK .. NBLK-1 (four steps each) for both lines of a lane,
 // unrolled at compile time.  `b` points at the word of row (element row -
 // 4 NBLK), row stride kRowW words, so every read has a non-negative
@@ -759,13 +775,13 @@ __device__ __forceinline__ void search_pair(const uint32_t *b, u16x2 &best, int 
 
 // The same for two rows 8 apart (row r at `b` + 4 NBLK rows, row r + 8
 // eight rows further): two independent chains per block, one vote for both.
-template <int BLK, int NBLK>
+template <int BLK, int NBLK, int METRIC>
 __device__ __forceinline__ void search_pair2(const uint32_t *b, u16x2 &best1, u16x2 &best2, int &dnext) {
     if constexpr (BLK < NBLK) {
         constexpr int d = 1 + 4 * BLK;
         constexpr int R = 4 * NBLK;
         constexpr int E = R + kPatchRows;
-        if (__all(stopped(__builtin_elementwise_max(best1, best2), d))) return;
+        if (__all(stop_at<METRIC>(__builtin_elementwise_max(best1, best2), d))) return;
         const u16x2 u0 = as_pair(b[(R - d) * kRowW]), u1 = as_pair(b[(R - d - 1) * kRowW]);
         const u16x2 u2 = as_pair(b[(R - d - 2) * kRowW]), u3 = as_pair(b[(R - d - 3) * kRowW]);
         const u16x2 w0 = as_pair(b[(R + d) * kRowW]), w1 = as_pair(b[(R + d + 1) * kRowW]);
@@ -774,16 +790,14 @@ __device__ __forceinline__ void search_pair2(const uint32_t *b, u16x2 &best1, u1
         const u16x2 x2 = as_pair(b[(E - d - 2) * kRowW]), x3 = as_pair(b[(E - d - 3) * kRowW]);
         const u16x2 y0 = as_pair(b[(E + d) * kRowW]), y1 = as_pair(b[(E + d + 1) * kRowW]);
         const u16x2 y2 = as_pair(b[(E + d + 2) * kRowW]), y3 = as_pair(b[(E + d + 3) * kRowW]);
-        const u16x2 s0 = splat(d * d), s1 = splat((d + 1) * (d + 1));
-        const u16x2 s2 = splat((d + 2) * (d + 2)), s3 = splat((d + 3) * (d + 3));
-        const u16x2 c0 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u0, w0), s0);
-        const u16x2 c1 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u1, w1), s1);
-        const u16x2 c2 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u2, w2), s2);
-        const u16x2 c3 = __builtin_elementwise_add_sat(__builtin_elementwise_min(u3, w3), s3);
-        const u16x2 e0 = __builtin_elementwise_add_sat(__builtin_elementwise_min(x0, y0), s0);
-        const u16x2 e1 = __builtin_elementwise_add_sat(__builtin_elementwise_min(x1, y1), s1);
-        const u16x2 e2 = __builtin_elementwise_add_sat(__builtin_elementwise_min(x2, y2), s2);
-        const u16x2 e3 = __builtin_elementwise_add_sat(__builtin_elementwise_min(x3, y3), s3);
+        const u16x2 c0 = cand<METRIC>(__builtin_elementwise_min(u0, w0), d);
+        const u16x2 c1 = cand<METRIC>(__builtin_elementwise_min(u1, w1), d + 1);
+        const u16x2 c2 = cand<METRIC>(__builtin_elementwise_min(u2, w2), d + 2);
+        const u16x2 c3 = cand<METRIC>(__builtin_elementwise_min(u3, w3), d + 3);
+        const u16x2 e0 = cand<METRIC>(__builtin_elementwise_min(x0, y0), d);
+        const u16x2 e1 = cand<METRIC>(__builtin_elementwise_min(x1, y1), d + 1);
+        const u16x2 e2 = cand<METRIC>(__builtin_elementwise_min(x2, y2), d + 2);
+        const u16x2 e3 = cand<METRIC>(__builtin_elementwise_min(x3, y3), d + 3);
         best1 = __builtin_elementwise_min(
             best1, __builtin_elementwise_min(__builtin_elementwise_min(c0, c1),
                                              __builtin_elementwise_min(c2, c3)));
@@ -791,7 +805,7 @@ __device__ __forceinline__ void search_pair2(const uint32_t *b, u16x2 &best1, u1
             best2, __builtin_elementwise_min(__builtin_elementwise_min(e0, e1),
                                              __builtin_elementwise_min(e2, e3)));
         dnext = d + 4;
-        search_pair2<BLK + 1, NBLK>(b, best1, best2, dnext);
+        search_pair2<BLK + 1, NBLK, METRIC>(b, best1, best2, dnext);
     }
 }
 
@@ -856,7 +870,10 @@ __device__ __forceinline__ float sqrt_rn_int(uint32_t x) {
 // removes the last-axis kernel's write and this pass's read of it.
 // MAXRB = 8 (lines up to 128 rows) keeps to 64 VGPRs, so four workgroups
 // (eight waves per SIMD) share a compute unit.
-template <bool FINAL, bool FROM_MASK, int MAXRB>
+// METRIC (kL2, kL1, kLinf) selects the transform; the taxicab and
+// chessboard ones (chamfer transforms) write int32 distances in the final
+// pass, -1 for samples without background.
+template <bool FINAL, bool FROM_MASK, int MAXRB, int METRIC = kL2>
 __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile_pair(PairArgs a) {
     extern __shared__ __attribute__((aligned(16))) uint32_t tw[];  // rows [-kGuard16, n + kGuard16) x kRowW words
     __shared__ __attribute__((aligned(8))) uint8_t any_site[kWave][kPairWaves];   // [tile word][wave]
@@ -992,9 +1009,15 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
                 // Distances past the row ends are at least kFar16: clamped to
                 // 256, their square saturates to "no site".  (Absent lines need
                 // no code: they are never searched and their stores are dropped.)
-                const uint32_t da = min(uint32_t(min(la, ra)), 256u), db = min(uint32_t(min(lb, rb)), 256u);
-                const uint32_t w = min(uint32_t(__umul24(da, da)), uint32_t(kNone16)) |
-                                   (min(uint32_t(__umul24(db, db)), uint32_t(kNone16)) << 16);
+                uint32_t w;
+                if constexpr (METRIC == kL2) {
+                    const uint32_t da = min(uint32_t(min(la, ra)), 256u), db = min(uint32_t(min(lb, rb)), 256u);
+                    w = min(uint32_t(__umul24(da, da)), uint32_t(kNone16)) |
+                        (min(uint32_t(__umul24(db, db)), uint32_t(kNone16)) << 16);
+                } else {
+                    const uint32_t da = uint32_t(min(la, ra)), db = uint32_t(min(lb, rb));
+                    w = (da >= kFar16 ? uint32_t(kNone16) : da) | ((db >= kFar16 ? uint32_t(kNone16) : db) << 16);
+                }
                 seenw = __builtin_elementwise_min(seenw, as_pair(w));
                 row0[q * kRowW + lane] = w;
             }
@@ -1127,25 +1150,22 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         // apart) takes the clamped loop only.
         const int room = min(q0 + kGuard16, n - 1 + kGuard16 - (q0 + PR - 1));
         const int nb = q0 + PR > n ? 0 : room >= kCap16 ? kCap16 / 4 : room >> 2;
-        if (nb == 4) search_pair2<0, 4>(row0 + (q1 - 16) * kRowW + cw, best1, best2, d);
-        else if (nb == 3) search_pair2<0, 3>(row0 + (q1 - 12) * kRowW + cw, best1, best2, d);
-        else if (nb == 2) search_pair2<0, 2>(row0 + (q1 - 8) * kRowW + cw, best1, best2, d);
-        else if (nb == 1) search_pair2<0, 1>(row0 + (q1 - 4) * kRowW + cw, best1, best2, d);
+        if (nb == 4) search_pair2<0, 4, METRIC>(row0 + (q1 - 16) * kRowW + cw, best1, best2, d);
+        else if (nb == 3) search_pair2<0, 3, METRIC>(row0 + (q1 - 12) * kRowW + cw, best1, best2, d);
+        else if (nb == 2) search_pair2<0, 2, METRIC>(row0 + (q1 - 8) * kRowW + cw, best1, best2, d);
+        else if (nb == 1) search_pair2<0, 1, METRIC>(row0 + (q1 - 4) * kRowW + cw, best1, best2, d);
         // Longer searches and rows near the ends: row indices clamp into
         // the guard rows.
-        while (!__all(stopped(__builtin_elementwise_max(best1, best2), d))) {
+        while (!__all(stop_at<METRIC>(__builtin_elementwise_max(best1, best2), d))) {
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
                 const int dd = d + s;
-                const u16x2 sq = splat(dd * dd >= kNone16 ? kNone16 : dd * dd);
                 const int lo1 = max(q1 - dd, -kGuard16), hi1 = min(q1 + dd, n + kGuard16 - 1);
                 const int lo2 = max(q2 - dd, -kGuard16), hi2 = min(q2 + dd, n + kGuard16 - 1);
                 const u16x2 u = as_pair(row0[lo1 * kRowW + cw]), w = as_pair(row0[hi1 * kRowW + cw]);
                 const u16x2 x = as_pair(row0[lo2 * kRowW + cw]), y = as_pair(row0[hi2 * kRowW + cw]);
-                best1 = __builtin_elementwise_min(
-                    best1, __builtin_elementwise_add_sat(__builtin_elementwise_min(u, w), sq));
-                best2 = __builtin_elementwise_min(
-                    best2, __builtin_elementwise_add_sat(__builtin_elementwise_min(x, y), sq));
+                best1 = __builtin_elementwise_min(best1, cand<METRIC>(__builtin_elementwise_min(u, w), dd));
+                best2 = __builtin_elementwise_min(best2, cand<METRIC>(__builtin_elementwise_min(x, y), dd));
             }
             d += 4;
             if (d > n + 4) break;   // every row has been examined
@@ -1192,6 +1212,21 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             const uint32_t da = (has & 1u) ? uint32_t(r.x) : uint32_t(kInfI);
             const uint32_t db = (has & 2u) ? uint32_t(r.y) : uint32_t(kInfI);
             __builtin_amdgcn_raw_buffer_store_b64(u32x2{da, db}, rb, voff_a, soff, 0);
+        });
+        return;
+    }
+    if constexpr (FINAL && METRIC != kL2) {
+        // chamfer transforms: int32 distances, -1 where the sample has no
+        // background (lines without a site)
+        store_rows([&](int, uint32_t soff, u16x2 r) {
+            const uint32_t da = (has & 1u) ? uint32_t(r.x) : 0xffffffffu;
+            const uint32_t db = (has & 2u) ? uint32_t(r.y) : 0xffffffffu;
+            if (pair_io) {
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{da, db}, rs, voff_a, soff, 0);
+            } else {
+                __builtin_amdgcn_raw_buffer_store_b32(da, rs, voff_a, soff, 0);
+                __builtin_amdgcn_raw_buffer_store_b32(db, rs, voff_b, soff, 0);
+            }
         });
         return;
     }

@@ -24,6 +24,8 @@
 #include "../../include/tm_edt.h"
 #include "edt_common.h"
 #include "edt_bf.h"
+#include "edt_cdt.h"
+#include "edt_lsearch.h"
 #include "edt_fh.h"
 #include "edt_tidx.h"
 #include "edt_scan.h"
@@ -129,11 +131,12 @@ struct Request {
     int32_t *sq;
     int32_t *idx;
     hipStream_t stream;
+    int metric;      // kL2 (exact transform) or kL1 / kLinf (chamfer; output in sq)
 };
 
 int validate(const uint8_t *in, int ndim, const int64_t *shape, int64_t batch,
              const double *sampling, const void *o1, const void *o2, const void *o3,
-             Request &r) {
+             Request &r, bool squared = true) {
     if (ndim < 1 || ndim > kMaxDim) return TM_ERR_NDIM;
     if (!shape) return TM_ERR_SHAPE;
     for (int a = 0; a < ndim; ++a)
@@ -157,11 +160,45 @@ int validate(const uint8_t *in, int ndim, const int64_t *shape, int64_t batch,
         r.shape[a] = uint32_t(shape[a]);
     }
     if (uint64_t(batch) >= (uint64_t(1) << 32) / vox) return TM_ERR_TOO_LARGE;
-    if (r.unit && sumsq >= (uint64_t(1) << 31) - 1) return TM_ERR_TOO_LARGE;
+    if (squared && r.unit && sumsq >= (uint64_t(1) << 31) - 1) return TM_ERR_TOO_LARGE;
     r.in = in;
     r.ndim = ndim;
     r.batch = uint64_t(batch);
     return TM_OK;
+}
+
+// Plan of one strided pass.
+struct FhPlan {
+    uint32_t lpw;
+    bool pack;
+    int acc;  // 0 int32 with 24-bit multiplies, 1 int32, 2 int64, 3 double
+    size_t lds;
+    bool tiled;      // staged tile + windowed search (k_tile_field)
+    bool tiled16;    // paired 16-bit tile with guard rows (k_tile_pair)
+    bool from_mask;  // tiled16 on axis ndim-2, computing the last-axis pass itself
+    bool tidx;       // tiled pass on the index carrier (k_tile_idx)
+    int ls_lpw;      // whole lines in LDS, windowed search (k_line_search): lines per workgroup (8 or 4), 0 = not
+    bool ls_w16;     //   with a 16-bit tile
+    uint32_t rbits;  // tidx, unit sampling: bits of the row in a key
+    uint32_t fbits;  // tiled: value bits of a tile word
+    uint32_t cap;    // tiled: search steps before the envelope fallback
+};
+
+// Whole-line windowed search: 8 lines per workgroup (a wave covers 8 rows
+// of 8 lines, whose search lengths vary less than those of 64 lines of one
+// row), or 4 when the tile of 8 does not fit LDS.
+bool plan_line_search(FhPlan &p, uint32_t n, uint64_t total, bool w16) {
+    const int tb = w16 ? 2 : 4;
+    const uint64_t lines = total / n;
+    int lpw = 0;
+    for (int c = 8; c >= 4 && !lpw; c /= 2)
+        if (line_search_lds(n, c, tb) + 1024 <= kLdsBytes) lpw = c;
+    if (!lpw || lines + uint64_t(lpw) >= (uint64_t(1) << 32) || (lines + lpw - 1) / lpw >= (uint64_t(1) << 31))
+        return false;
+    p.ls_lpw = lpw;
+    p.ls_w16 = w16;
+    p.lds = line_search_lds(n, lpw, tb);
+    return true;
 }
 
 int run(Request &r) {
@@ -180,24 +217,45 @@ int run(Request &r) {
     const bool index_path = r.idx != nullptr;
 
     // Plan and check every strided pass before launching anything.
-    struct FhPlan {
-        uint32_t lpw;
-        bool pack;
-        int acc;  // 0 int32 with 24-bit multiplies, 1 int32, 2 int64, 3 double
-        size_t lds;
-        bool tiled;      // staged tile + windowed search (k_tile_field)
-        bool tiled16;    // paired 16-bit tile with guard rows (k_tile_pair)
-        bool from_mask;  // tiled16 on axis ndim-2, computing the last-axis pass itself
-        bool tidx;       // tiled pass on the index carrier (k_tile_idx)
-        uint32_t rbits;  // tidx, unit sampling: bits of the row in a key
-        uint32_t fbits;  // tiled: value bits of a tile word
-        uint32_t cap;    // tiled: search steps before the envelope fallback
-    } fh[kMaxDim] = {};
+    FhPlan fh[kMaxDim] = {};
     for (int a = nd - 2; a >= 0; --a) {
         const uint32_t n = r.shape[a];
         uint64_t fmax = 0;
         for (int b = a + 1; b < nd; ++b) fmax += uint64_t(r.shape[b] - 1) * (r.shape[b] - 1);
         FhPlan &p = fh[a];
+        if (r.metric != kL2) {
+            // Chamfer transforms: the paired tile with the metric's largest
+            // value plus any in-line distance below "no site", else whole
+            // lines staged in LDS.
+            uint64_t vmax = 0;
+            for (int b = a + 1; b < nd; ++b)
+                vmax = r.metric == kL1 ? vmax + (r.shape[b] - 1) : std::max<uint64_t>(vmax, r.shape[b] - 1);
+            const size_t tp = size_t(n + 2 * kGuard16) * kRowW * 4;
+            uint64_t inner = 1;
+            for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
+            const bool offsets_fit =
+                (uint64_t(n) * inner * 2 + uint64_t(n) * kPairLines) * 4 < (uint64_t(1) << 31);
+            if (n <= 256 && vmax + n + 4 < uint64_t(kNone16) && tp + 1024 <= kLdsBytes && offsets_fit &&
+                total / n + kPairLines < (uint64_t(1) << 32)) {
+                p.tiled16 = true;
+                p.lds = tp;
+                const uint32_t n2 = r.shape[nd - 1];
+                if (a == nd - 2 && n2 % 32 == 0 && uintptr_t(r.in) % 16 == 0) {
+                    uint32_t g = kPairLines;
+                    for (uint32_t x = n2; x;) {
+                        const uint32_t y = g % x;
+                        g = x;
+                        x = y;
+                    }
+                    const uint64_t planes = (uint64_t(n2) - g + kPairLines - 1) / n2 + 1;
+                    if (planes * (n2 / 32) * 2 <= uint64_t(kWave)) p.from_mask = true;
+                }
+                continue;
+            }
+            const uint64_t cmax = r.metric == kL1 ? vmax + n + 4 : std::max<uint64_t>(vmax, n + 4);
+            if (!plan_line_search(p, n, total, cmax < uint64_t(kNone16))) return TM_ERR_UNSUPPORTED;
+            continue;
+        }
         p.acc = !r.unit ? 3 : int24_safe(fmax, n) ? 0 : int32_safe(fmax, n) ? 1 : 2;
         uint32_t eb;
         if (index_path) {
@@ -247,6 +305,7 @@ int run(Request &r) {
                 continue;
             }
         }
+        if (!index_path && r.unit && n > 256 && plan_line_search(p, n, total, false)) continue;
         if (!index_path && r.unit && n <= 256) {
             const uint32_t cap = n - 1 < 64 ? n - 1 : 64;
             int vbits = bits_for(n - 1);
@@ -269,8 +328,8 @@ int run(Request &r) {
             const size_t tb = size_t(2) * idx_tile_words(n) * 4;
             int rb = bits_for(n - 1);
             if (rb < 1) rb = 1;
-            const bool keys_fit = !r.unit || rb < 31 &&
-                ((fmax + uint64_t(n - 1) * (n - 1)) << rb | uint64_t(n - 1)) < (uint64_t(1) << 31);
+            const bool keys_fit = !r.unit || (rb < 31 &&
+                ((fmax + uint64_t(n - 1) * (n - 1)) << rb | uint64_t(n - 1)) < (uint64_t(1) << 31));
             if (tb + 1024 <= kLdsBytes && keys_fit && total / n + kWave < (uint64_t(1) << 32)) {
                 p.tidx = true;
                 p.rbits = uint32_t(rb);
@@ -316,7 +375,11 @@ int run(Request &r) {
         s.w = r.w[nd - 1];
         int mode;
         void *out;
-        if (nd == 1) {
+        if (r.metric != kL2) {
+            mode = kScanFieldL1;      // |d|, also the whole rank-1 chamfer result
+            s.field_i = r.sq;
+            out = r.sq;
+        } else if (nd == 1) {
             mode = kScanFinal;
             s.dist = r.dist;
             s.sq = r.sq;
@@ -357,6 +420,7 @@ int run(Request &r) {
             const dim3 grid(uint32_t((waves + 3) / 4)), block(256);
             switch (mode) {
                 case kScanFieldInt: rc = launch("scan_word", k_scan_word<kScanFieldInt>, grid, block, 0, r.stream, ws); break;
+                case kScanFieldL1: rc = launch("scan_word", k_scan_word<kScanFieldL1>, grid, block, 0, r.stream, ws); break;
                 case kScanFieldFlt: rc = launch("scan_word", k_scan_word<kScanFieldFlt>, grid, block, 0, r.stream, ws); break;
                 case kScanIndex: rc = launch("scan_word", k_scan_word<kScanIndex>, grid, block, 0, r.stream, ws); break;
                 default: rc = launch("scan_word", k_scan_word<kScanFinal>, grid, block, 0, r.stream, ws); break;
@@ -370,6 +434,8 @@ int run(Request &r) {
             switch (mode * 2 + (vec ? 1 : 0)) {
                 case kScanFieldInt * 2: rc = launch("scan_span", k_scan_span<kScanFieldInt, false>, grid, block, 0, r.stream, s); break;
                 case kScanFieldInt * 2 + 1: rc = launch("scan_span", k_scan_span<kScanFieldInt, true>, grid, block, 0, r.stream, s); break;
+                case kScanFieldL1 * 2: rc = launch("scan_span", k_scan_span<kScanFieldL1, false>, grid, block, 0, r.stream, s); break;
+                case kScanFieldL1 * 2 + 1: rc = launch("scan_span", k_scan_span<kScanFieldL1, true>, grid, block, 0, r.stream, s); break;
                 case kScanFieldFlt * 2: rc = launch("scan_span", k_scan_span<kScanFieldFlt, false>, grid, block, 0, r.stream, s); break;
                 case kScanFieldFlt * 2 + 1: rc = launch("scan_span", k_scan_span<kScanFieldFlt, true>, grid, block, 0, r.stream, s); break;
                 case kScanIndex * 2: rc = launch("scan_span", k_scan_span<kScanIndex, false>, grid, block, 0, r.stream, s); break;
@@ -382,12 +448,19 @@ int run(Request &r) {
             const size_t lds = size_t(nlast / kSpan + 2) * 4;
             switch (mode) {
                 case kScanFieldInt: rc = launch("scan_long", k_scan_long<kScanFieldInt>, grid, block, lds, r.stream, s); break;
+                case kScanFieldL1: rc = launch("scan_long", k_scan_long<kScanFieldL1>, grid, block, lds, r.stream, s); break;
                 case kScanFieldFlt: rc = launch("scan_long", k_scan_long<kScanFieldFlt>, grid, block, lds, r.stream, s); break;
                 case kScanIndex: rc = launch("scan_long", k_scan_long<kScanIndex>, grid, block, lds, r.stream, s); break;
                 default: rc = launch("scan_long", k_scan_long<kScanFinal>, grid, block, lds, r.stream, s); break;
             }
         }
         if (rc != TM_OK) return rc;
+        if (nd == 1 && r.metric != kL2) {
+            const uint64_t nb = (total + 255) / 256;
+            rc = launch("cdt_none", k_cdt_none_to_minus1, dim3(uint32_t(nb)), dim3(256), 0, r.stream,
+                        NoneArgs{r.sq, total});
+            if (rc != TM_OK) return rc;
+        }
     }
 
     // ---- strided lower-envelope passes, axis nd-2 down to 0 ----------------
@@ -397,7 +470,8 @@ int run(Request &r) {
         uint64_t inner = 1;
         for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
         const uint64_t lines = total / n;
-        const dim3 grid(uint32_t((lines + p.lpw - 1) / p.lpw)), block(kWave);
+        const uint32_t lpw = p.lpw ? p.lpw : 1;     // lines per wave of the envelope kernels
+        const dim3 grid(uint32_t((lines + lpw - 1) / lpw)), block(kWave);
         const bool fin = a == 0;
         if (p.tiled16) {
             PairArgs tg{};
@@ -429,7 +503,20 @@ int run(Request &r) {
                  {{"plane_pair_final", "plane_pair_final"}, {"plane_pair_final", "plane_pair_final"}}}};
             const char *nm = names[p.from_mask][fin][tg.in_seg][tg.out_seg];
             // search results stay in registers: 2 per lane and 16-row block
-            if (n <= 128) {
+            if (r.metric != kL2) {
+                static const char *const cnames[2][2][2] = {
+                    {{"cdt_pair", "cdt_pair.o16"}, {"cdt_pair.i16", "cdt_pair.i16.o16"}},
+                    {{"cdt_pair_final", "cdt_pair_final"}, {"cdt_pair_final.i16", "cdt_pair_final.i16"}}};
+                nm = p.from_mask ? (fin ? "cdt_plane_final" : tg.out_seg ? "cdt_plane.o16" : "cdt_plane")
+                                 : cnames[fin][tg.in_seg][tg.out_seg];
+#define TM_CDT_PAIR(M)                                                                                   \
+    (p.from_mask ? (fin ? launch(nm, k_tile_pair<true, true, 16, M>, tgrid, tblock, p.lds, r.stream, tg)  \
+                        : launch(nm, k_tile_pair<false, true, 16, M>, tgrid, tblock, p.lds, r.stream, tg)) \
+                 : (fin ? launch(nm, k_tile_pair<true, false, 16, M>, tgrid, tblock, p.lds, r.stream, tg)  \
+                        : launch(nm, k_tile_pair<false, false, 16, M>, tgrid, tblock, p.lds, r.stream, tg)))
+                rc = r.metric == kL1 ? TM_CDT_PAIR(kL1) : TM_CDT_PAIR(kLinf);
+#undef TM_CDT_PAIR
+            } else if (n <= 128) {
                 if (p.from_mask)
                     rc = fin ? launch(nm, k_tile_pair<true, true, 8>, tgrid, tblock, p.lds, r.stream, tg)
                              : launch(nm, k_tile_pair<false, true, 8>, tgrid, tblock, p.lds, r.stream, tg);
@@ -444,6 +531,32 @@ int run(Request &r) {
                     rc = fin ? launch(nm, k_tile_pair<true, false, 16>, tgrid, tblock, p.lds, r.stream, tg)
                              : launch(nm, k_tile_pair<false, false, 16>, tgrid, tblock, p.lds, r.stream, tg);
             }
+        } else if (p.ls_lpw) {
+            LineSearchArgs la{};
+            la.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
+            la.dist = r.dist;
+            la.sq = r.sq;
+            la.lines = uint32_t(lines);
+            la.n = n;
+            la.inner = uint32_t(inner);
+            la.div_inner = Div32::make(la.inner);
+            la.ndim = nd;
+            for (int b = 0; b < nd; ++b) {
+                la.shape[b] = r.shape[b];
+                la.wall[b] = r.w[b];
+            }
+            const dim3 lgrid(uint32_t((lines + p.ls_lpw - 1) / p.ls_lpw)), lblock(kWave * kLsWaves);
+            const char *nm = r.metric == kL2 ? (fin ? "line_search_final" : "line_search")
+                                             : (fin ? "cdt_line_final" : "cdt_line");
+#define TM_LS(M, F, W)                                                                                  \
+    (p.ls_lpw == 8 ? launch(nm, k_line_search<M, F, W, 8>, lgrid, lblock, p.lds, r.stream, la)         \
+                   : launch(nm, k_line_search<M, F, W, 4>, lgrid, lblock, p.lds, r.stream, la))
+            if (r.metric == kL2) rc = fin ? TM_LS(kL2, true, false) : TM_LS(kL2, false, false);
+            else if (r.metric == kL1 && p.ls_w16) rc = fin ? TM_LS(kL1, true, true) : TM_LS(kL1, false, true);
+            else if (r.metric == kL1) rc = fin ? TM_LS(kL1, true, false) : TM_LS(kL1, false, false);
+            else if (p.ls_w16) rc = fin ? TM_LS(kLinf, true, true) : TM_LS(kLinf, false, true);
+            else rc = fin ? TM_LS(kLinf, true, false) : TM_LS(kLinf, false, false);
+#undef TM_LS
         } else if (p.tiled) {
             TileArgs tg{};
             tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
@@ -613,6 +726,20 @@ extern "C" int tm_dt_bf(const uint8_t *in_u8, int ndim, const int64_t *shape, in
     else rc = samp ? TM_BF(2, true) : TM_BF(2, false);
 #undef TM_BF
     return rc;
+}
+
+extern "C" int tm_cdt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, int metric,
+                      int32_t *out_dist, hipStream_t stream) {
+    Request r{};
+    int rc = validate(in_u8, ndim, shape, batch, nullptr, nullptr, out_dist, nullptr, r, false);
+    if (rc != TM_OK) return rc;
+    if (metric != TM_METRIC_TAXICAB && metric != TM_METRIC_CHESSBOARD) return TM_ERR_METRIC;
+    r.dist = nullptr;
+    r.sq = out_dist;
+    r.idx = nullptr;
+    r.stream = stream;
+    r.metric = metric == TM_METRIC_TAXICAB ? kL1 : kLinf;
+    return run(r);
 }
 
 extern "C" const char *tm_strerror(int status) {

@@ -1,0 +1,180 @@
+// Windowed exact search over lines longer than the paired 16-bit tile takes
+// (unit sampling, distances only): the exact transform and the two chamfer
+// transforms.
+//
+// Every metric here separates over the axes (paper, Section 2.3.2): with f
+// the value over the axes already processed,
+//     euclidean   g(q) = min over r of  f(r) + (q - r)^2
+//     taxicab     g(q) = min over r of  f(r) + |q - r|
+//     chessboard  g(q) = min over r of  max(f(r), |q - r|)
+// and every candidate at distance d along the line is at least d^2 (resp.
+// d), so a search outward from q can stop once the best value found is no
+// larger than that.  The result is the same minimum the lower envelope gives.
+//
+// A workgroup of 16 waves owns LPW adjacent lines (8, or 4 for the longest
+// lines) and stages them whole in LDS, [row][line], as 16-bit values when
+// every value plus any in-line distance term stays below the 16-bit "no
+// site" code, else 32-bit.  Lane l of a wave takes line l % LPW at row
+// (wave row) + l / LPW: a wave covers a compact patch of consecutive rows,
+// whose search lengths differ little (the result is 1-Lipschitz along the
+// line), and reads 64 consecutive entries (conflict-free) at every step.
+// Search steps come in eights between wave-wide stop votes, read from two
+// bases clamped into the guard rows (which hold "no site").  Results go
+// straight to global memory: the staged copy is what every search reads, and
+// no other workgroup reads these lines.  Fewer lines per workgroup give more
+// workgroups when there are few lines.
+#pragma once
+
+#include "edt_fh.h"
+
+namespace tmedt {
+
+constexpr int kLsWaves = 16;
+constexpr int kLsUnroll = 8;     // search steps between stop votes
+constexpr int kLsGuard = kLsUnroll;   // guard rows of "no site" per side
+
+struct LineSearchArgs {
+    int32_t *buf;          // int32 field, batch-flat, in place (kInfI = no site)
+    float *dist;           // final euclidean pass: outputs (each may be null)
+    int32_t *sq;
+    uint32_t lines;        // lines of this pass
+    uint32_t n;            // line length
+    uint32_t inner;        // element stride of the line
+    Div32 div_inner;
+    int32_t ndim;
+    uint32_t shape[kMaxDim];
+    double wall[kMaxDim];  // ones (virtual element of a final euclidean pass)
+};
+
+// LDS bytes of the staged tile.
+__host__ __device__ constexpr size_t line_search_lds(uint32_t n, int lpw, int tbytes) {
+    return size_t(n + 2 * kLsGuard) * size_t(lpw) * size_t(tbytes);
+}
+
+template <int METRIC, bool W16>
+__device__ __forceinline__ uint32_t ls_cand(uint32_t m, int d) {
+    // m: staged value (16-bit codes zero-extended); "no site" stays at or
+    // above the code, every real candidate below it (host eligibility)
+    if constexpr (METRIC == kLinf) return max(m, uint32_t(d));
+    const uint32_t step = METRIC == kL2 ? uint32_t(d) * uint32_t(d) : uint32_t(d);
+    if constexpr (W16) return m + step;
+    else return __builtin_elementwise_add_sat(m, step);
+}
+
+template <int METRIC>
+__device__ __forceinline__ bool ls_stop(uint32_t best, int d) {
+    if constexpr (METRIC == kL2) return best <= uint32_t(d) * uint32_t(d);
+    else return best <= uint32_t(d);
+}
+
+template <int METRIC, bool FINAL, bool W16, int LPW>
+__global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs a) {
+    using T = typename std::conditional<W16, uint16_t, uint32_t>::type;
+    constexpr uint32_t NONE = W16 ? 0xffffu : 0xffffffffu;
+    constexpr int RPW = kWave / LPW;                 // rows per wave and step
+    constexpr int STEP = kLsWaves * RPW;             // row step of one lane
+    extern __shared__ __attribute__((aligned(16))) uint8_t ls_lds[];
+    __shared__ uint32_t has_site[LPW];
+    T *tile = reinterpret_cast<T *>(ls_lds);
+    const int t = threadIdx.x;
+    const int lane = t & (kWave - 1);
+    const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
+    const int j = lane % LPW, sub = lane / LPW;
+    const int n = int(a.n);
+    const uint32_t L = blockIdx.x * uint32_t(LPW) + uint32_t(j);
+    const bool live = L < a.lines;
+    const uint32_t o = live ? a.div_inner.div(L) : 0u;
+    const uint32_t i = live ? L - o * a.inner : 0u;
+    const uint64_t base = uint64_t(o) * a.n * a.inner + i;   // row 0 of the line
+    int32_t *line = a.buf + base;
+    T *row0 = tile + kLsGuard * LPW;
+
+    for (int k = t; k < kLsGuard * LPW; k += kWave * kLsWaves) {
+        tile[k] = T(NONE);
+        row0[n * LPW + k] = T(NONE);
+    }
+    if (t < LPW) has_site[t] = 0u;
+    __syncthreads();
+
+    // ---- staging: SB rows in flight per lane ----------------------------------
+    const int qs = wv * RPW + sub;
+    uint32_t seen = 0;
+    constexpr int SB = 8;
+    for (int q0 = qs; q0 < n; q0 += STEP * SB) {
+        int32_t v[SB];
+#pragma unroll
+        for (int s = 0; s < SB; ++s) {
+            const int q = q0 + s * STEP;
+            v[s] = (live && q < n) ? line[uint64_t(q) * a.inner] : kInfI;
+        }
+#pragma unroll
+        for (int s = 0; s < SB; ++s) {
+            const int q = q0 + s * STEP;
+            if (q < n) {
+                row0[q * LPW + j] = v[s] == kInfI ? T(NONE) : T(v[s]);
+                seen |= v[s] != kInfI ? 1u : 0u;
+            }
+        }
+    }
+    if (seen) atomicOr(&has_site[j], 1u);
+    __syncthreads();
+    const bool has = has_site[j] != 0u;
+
+    // ---- search and output --------------------------------------------------
+    for (int qw = wv * RPW; qw < n; qw += STEP) {      // wave-uniform
+        const int q = qw + sub;
+        const bool mine = live && q < n;
+        const int qc = min(q, n - 1);
+        uint32_t best = (mine && has) ? uint32_t(row0[qc * LPW + j]) : 0u;
+        // Steps d .. d+7 read rows q-d-7 .. q-d and q+d .. q+d+7 at fixed
+        // offsets from two bases.  A base moves into the guard rows only
+        // when every row it stands for is beyond the line, so the reads stay
+        // exact.  Two register sets take turns: the next block is read
+        // before this one is folded in, hiding the LDS latency behind the
+        // vote.
+        const T *col = row0 + j;
+        auto read = [&](int d, uint32_t (&u)[kLsUnroll], uint32_t (&w)[kLsUnroll]) {
+            const T *pl = col + max(qc - d - (kLsUnroll - 1), -kLsGuard) * LPW;
+            const T *ph = col + min(qc + d, n + kLsGuard - kLsUnroll) * LPW;
+#pragma unroll
+            for (int s = 0; s < kLsUnroll; ++s) {
+                u[s] = pl[(kLsUnroll - 1 - s) * LPW];
+                w[s] = ph[s * LPW];
+            }
+        };
+        auto fold = [&](int d, const uint32_t (&u)[kLsUnroll], const uint32_t (&w)[kLsUnroll]) {
+#pragma unroll
+            for (int s = 0; s < kLsUnroll; ++s) best = min(best, ls_cand<METRIC, W16>(min(u[s], w[s]), d + s));
+        };
+        uint32_t ua[kLsUnroll], wa[kLsUnroll], ub[kLsUnroll], wb[kLsUnroll];
+        int d = 1;
+        read(d, ua, wa);
+        // every row has been examined once d passes n
+        while (!__all(ls_stop<METRIC>(best, d))) {
+            read(d + kLsUnroll, ub, wb);
+            fold(d, ua, wa);
+            d += kLsUnroll;
+            if (d > n || __all(ls_stop<METRIC>(best, d))) break;
+            read(d + kLsUnroll, ua, wa);
+            fold(d, ub, wb);
+            d += kLsUnroll;
+            if (d > n) break;
+        }
+        if (!mine) continue;
+        const uint64_t e = base + uint64_t(q) * a.inner;
+        if (!FINAL) {
+            a.buf[e] = has ? int32_t(best) : kInfI;
+        } else if (METRIC != kL2) {
+            a.buf[e] = has ? int32_t(best) : -1;       // chamfer: nothing reachable
+        } else {
+            int64_t v;
+            if (has) v = int64_t(best);
+            else v = virtual_sq<int64_t>(q, i, a.ndim, a.shape, a.wall);   // no background
+            const float dv = v < (int64_t(1) << 24) ? sqrt_rn_int(uint32_t(v)) : float(sqrt(double(v)));
+            if (a.dist) a.dist[e] = dv;
+            if (a.sq) a.sq[e] = int32_t(v);
+        }
+    }
+}
+
+}  // namespace tmedt

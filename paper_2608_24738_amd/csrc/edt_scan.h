@@ -20,7 +20,8 @@ enum ScanMode : int {
     kScanFieldInt = 0,   // int32 squared distance, kInfI if the line has no zero
     kScanFieldFlt = 1,   // float w * squared distance, +inf if none
     kScanIndex = 2,      // int32 in-sample flat index of the zero, -1 if none
-    kScanFinal = 3       // rank-1 input: the line is the sample; final outputs
+    kScanFinal = 3,      // rank-1 input: the line is the sample; final outputs
+    kScanFieldL1 = 4     // int32 distance (taxicab / chessboard first pass), kInfI if none
 };
 
 struct ScanArgs {
@@ -121,12 +122,13 @@ template <int MODE, bool VEC>
 __device__ inline void scan_store4(const ScanArgs &a, uint32_t gline, int x0, const int y[4],
                                    int count) {
     const uint64_t lbase = uint64_t(gline) * a.n;  // batch-flat start of the line
-    if (MODE == kScanFieldInt) {
+    if (MODE == kScanFieldInt || MODE == kScanFieldL1) {
         int32_t v[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             int d = x0 + j - y[j];
-            v[j] = y[j] >= 0 ? d * d : kInfI;
+            if (MODE == kScanFieldL1) d = d < 0 ? -d : d;
+            v[j] = y[j] >= 0 ? (MODE == kScanFieldL1 ? d : d * d) : kInfI;
         }
         int32_t *o = a.field_i + lbase + x0;
         if (VEC) {
@@ -396,8 +398,8 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
         const int dd = left ? l : r;
         const int y = left ? dl[p] : next;        // line-relative zero, valid if dd < kFar / 2
         const bool none = dd >= kFar / 2;
-        if (MODE == kScanFieldInt) {
-            out[p] = none ? kInfI : dd * dd;
+        if (MODE == kScanFieldInt || MODE == kScanFieldL1) {
+            out[p] = none ? kInfI : (MODE == kScanFieldL1 ? dd : dd * dd);
         } else if (MODE == kScanFieldFlt) {
             const double df = double(dd);
             out[p] = none ? __builtin_bit_cast(int32_t, __builtin_inff())
@@ -413,8 +415,8 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
     if (!live) return;
 
     // ---- stores -------------------------------------------------------------
-    if (MODE == kScanFieldInt || MODE == kScanFieldFlt) {
-        int4 *dst = reinterpret_cast<int4 *>(MODE == kScanFieldInt ? a.field_i
+    if (MODE == kScanFieldInt || MODE == kScanFieldL1 || MODE == kScanFieldFlt) {
+        int4 *dst = reinterpret_cast<int4 *>(MODE != kScanFieldFlt ? a.field_i
                                                                   : reinterpret_cast<int32_t *>(a.field_f)) +
                     pos0 / 4;
 #pragma unroll

@@ -1,4 +1,4 @@
-"""Seeded synthetic masks for the five EDT workloads.
+"""Seeded synthetic masks for the EDT, brute-force and chamfer workloads.
 
 This module only draws inputs: it holds none of the distance-transform
 arithmetic, and both the GPU tests and the CPU oracle's checks take their
@@ -22,6 +22,16 @@ these shapes, densities and structures stand in for them:
                             sampling (2.5, 0.8, 0.8)               (dist + idx)
   5  4-D  4x1x32x64x64x64,  background iff U < 1e-4, at least one
                             background voxel per sample            (dist)
+
+and, for the brute-force and chamfer transforms the paper also times on 2-D
+batches:
+
+  6  2-D  8x1x256x256,      background iff U < 0.01, at least one  (brute force)
+  7  2-D  8x1x1024x1024,    background = union of 20 discs,
+                            r ~ U[10, 120]                         (chamfer)
+  8  2-D  8x1x256x256,      background = union of 20 discs,
+                            r ~ U[2.5, 30]                         (chamfer)
+  9  2-D  8x1x1024x1024,    as 7                                   (EDT, dist)
 
 Smaller twins keep the generator and scale ball radii with the smallest
 extent, so parity tests can cover the same structure at sizes the oracle
@@ -68,6 +78,15 @@ WORKLOADS = {
                 {"p_bg": 0.01, "at_least_one": False}, (2.5, 0.8, 0.8), True),
     5: Workload(5, "edt4d_4x32x64x64x64_sparse", 4, (32, 64, 64, 64), "bernoulli_bg",
                 {"p_bg": 1e-4, "at_least_one": True}),
+    # the other transforms the paper times on 2-D batches (its throughput table)
+    6: Workload(6, "bf2d_8x256x256_bernoulli1pct", 8, (256, 256), "bernoulli_bg",
+                {"p_bg": 0.01, "at_least_one": True}),
+    7: Workload(7, "cdt2d_8x1024x1024_discs", 8, (1024, 1024), "discs_bg",
+                {"count": 20, "r_min": 10.0, "r_max": 120.0}),
+    8: Workload(8, "cdt2d_8x256x256_discs", 8, (256, 256), "discs_bg",
+                {"count": 20, "r_min": 2.5, "r_max": 30.0}),
+    9: Workload(9, "edt2d_8x1024x1024_discs", 8, (1024, 1024), "discs_bg",
+                {"count": 20, "r_min": 10.0, "r_max": 120.0}),
 }
 
 

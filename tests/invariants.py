@@ -65,3 +65,39 @@ def check_lipschitz(dist, sampling=None, slack=0.0):
         step = np.abs(np.diff(dist, axis=a))
         bad += int((step > s[a] * (1 + slack) + slack).sum())
     return bad
+
+
+def chamfer_fixed_point_violations(mask, d, metric):
+    """Number of elements where d breaks the chamfer equations on one sample.
+
+    With N(x) the face neighbours (taxicab) or all 3^nd - 1 neighbours
+    (chessboard) inside the grid, the graph distance D to the background is
+    the only integer field with D = 0 on the background and
+    D(x) = 1 + min over N(x) of D elsewhere (follow a shortest path for <=,
+    a chain of neighbours whose value drops by one for >=), and on the full
+    grid it equals the taxicab or chessboard distance.  A sample without
+    background must hold -1 everywhere.
+    """
+    mask = np.asarray(mask)
+    d = np.asarray(d).astype(np.int64)
+    if not (mask == 0).any():
+        return int((d != -1).sum())
+    nd = mask.ndim
+    big = np.int64(1) << 40
+    pad = np.pad(d, 1, constant_values=big)
+    if metric == "taxicab":
+        offs = []
+        for a in range(nd):
+            for s in (-1, 1):
+                o = [0] * nd
+                o[a] = s
+                offs.append(o)
+    else:
+        offs = [o for o in np.ndindex(*(3,) * nd)]
+        offs = [[v - 1 for v in o] for o in offs if any(v != 1 for v in o)]
+    nb = np.full(d.shape, big)
+    for o in offs:
+        sl = tuple(slice(1 + oa, 1 + oa + n) for oa, n in zip(o, d.shape))
+        nb = np.minimum(nb, pad[sl])
+    want = np.where(mask == 0, 0, nb + 1)
+    return int((d != want).sum() + (d < 0).sum())

@@ -38,7 +38,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert {"tm_edt", "tm_edt_sq", "tm_dt_bf", "tm_strerror"} <= set(names)
+    assert {"tm_edt", "tm_edt_sq", "tm_dt_bf", "tm_cdt", "tm_strerror"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -137,3 +137,36 @@ def test_brute_force_argument_checks(lib):
     assert call_bf(lib, [4, 0]) == TM_ERR_SHAPE
     assert call_bf(lib, [4, 4], sampling=[1.0, 0.0]) == TM_ERR_SAMPLING
     assert call_bf(lib, [16, 16], dist=FAKE_IN + 8) == TM_ERR_ALIAS
+
+
+def call_cdt(lib, shape, metric=1, batch=1, inp=FAKE_IN, dist=FAKE_OUT):
+    sh = (ctypes.c_int64 * len(shape))(*shape)
+    return lib.tm_cdt(ctypes.c_void_p(inp), len(shape), sh, batch, metric,
+                      dist and ctypes.c_void_p(dist), None)
+
+
+def test_chamfer_argument_checks(lib):
+    assert call_cdt(lib, [4, 4], metric=0) == TM_ERR_METRIC       # no euclidean chamfer
+    assert call_cdt(lib, [4, 4], metric=3) == TM_ERR_METRIC
+    assert call_cdt(lib, [4, 4], dist=0) == TM_ERR_NO_OUTPUT
+    assert call_cdt(lib, [4, 0]) == TM_ERR_SHAPE
+    assert call_cdt(lib, [4, 4], batch=0) == TM_ERR_BATCH
+    assert call_cdt(lib, [4] * 9) == TM_ERR_NDIM
+    assert call_cdt(lib, [16, 16], dist=FAKE_IN + 8) == TM_ERR_ALIAS
+    assert call_cdt(lib, [1 << 16, 1 << 15]) == TM_ERR_TOO_LARGE
+    # no bound on squared extents (values are sums, not squares), but lines
+    # past the whole-line pass's LDS budget along a strided axis are refused
+    for metric in (1, 2):
+        assert call_cdt(lib, [50000, 2], metric=metric) == TM_ERR_UNSUPPORTED
+        assert call_cdt(lib, [30000, 2], metric=metric) == TM_ERR_UNSUPPORTED
+
+
+def test_chamfer_binding_checks():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros((1, 1, 4, 4), dtype=torch.uint8)
+    with pytest.raises(ValueError):
+        binding.distance_transform_cdt(x, metric="euclidean")
+    with pytest.raises(ValueError):
+        binding.tm_cdt(x, 2, 1, torch.empty(16, dtype=torch.int32))       # not a GPU tensor
+    with pytest.raises(RuntimeError):
+        binding.distance_transform_cdt(x, distances=torch.empty((1, 1, 4, 4)))

@@ -124,14 +124,22 @@ def test_scan_line_lengths(n):
     parity(m2, 2, None, dist=True, idx=False, tag="2-D n=%d" % n)
 
 
-@pytest.mark.parametrize("n", [700, 1500, 3000])
+@pytest.mark.parametrize("n", [700, 1500, 3000, 6000])
 def test_long_strided_lines(n):
     """Strided lines long enough that fewer than 64 lanes share a workgroup's LDS,
-    and (n = 3000) products that need the int64 comparison path."""
+    products that need the int64 comparison path (n >= 3000, sampled), and
+    (n = 6000) a whole-line search with 4 lines per workgroup."""
     mask = rand_mask((n, 40), 0.003, n)
     parity(mask[None], 2, None, dist=True, idx=True, tag="long strided n=%d" % n)
     parity(mask[None], 2, None, dist=True, idx=False, tag="long strided n=%d" % n)
     parity(mask[None], 2, (1.25, 0.5), dist=True, idx=False, tag="long strided sampled n=%d" % n)
+
+
+def test_long_lines_without_background():
+    """Final whole-line passes over samples with and without background."""
+    mask = rand_mask((3, 600, 30), 0.002, 600)
+    mask[1] = 1
+    parity(mask, 2, None, dist=True, idx=False, sq=True, tag="long lines, no background")
 
 
 def test_sparse_long_envelopes():
