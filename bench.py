@@ -54,10 +54,10 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
         return total * (1 + fout)
     if base in ("plane_pair_final", "cdt_plane_final"):
         return total * (1 + out_bytes)
-    if base in ("fh_field", "tile_field", "tile_pair", "cdt_pair", "cdt_line", "cdt_none",
+    if base in ("fh_field", "tile_pair", "cdt_pair", "cdt_line", "cdt_none",
                 "line_search"):
         return total * (fin + fout)
-    if base in ("fh_field_final", "tile_field_final", "tile_pair_final", "cdt_pair_final",
+    if base in ("fh_field_final", "tile_pair_final", "cdt_pair_final",
                 "cdt_line_final", "line_search_final"):
         return total * (fin + out_bytes)
     if base in ("fh_index", "tile_idx"):

@@ -464,225 +464,6 @@ __global__ void __launch_bounds__(64) k_fh_index(IndexArgs a) {
 namespace tmedt {
 
 // ---------------------------------------------------------------------------
-// Tiled pass (unit sampling, field carrier): a workgroup stages the whole of
-// 64 adjacent lines in LDS as tile[q][lane] (coalesced 256-byte rows), then
-// every element q searches outwards, d = 1, 2, ..., for
-//     min over |p - q| <= d of g(p) + (q - p)^2,
-// stopping at the first d with d^2 greater than the best value so far (no
-// site farther away can do better).  The result is the exact minimum of the
-// envelope pass.  Elements are independent, so the four waves of the
-// workgroup split the rows and no per-line sequential chain remains.
-//
-// A search that has not stopped after `cap` steps marks the tile as hard;
-// the workgroup then recomputes every line of the tile with the sequential
-// lower-envelope build from the LDS copy (one lane per line), keeping the
-// envelope stack in the high bits of the tile words.  The tile's global
-// outputs are simply written again with the same exact values.
-// ---------------------------------------------------------------------------
-struct TileArgs {
-    int32_t *buf;         // int32 squared distances, batch-flat, updated in place
-    uint64_t lines;       // batch * voxels / n
-    uint32_t n;           // line length
-    uint32_t inner;       // element stride of the line
-    uint32_t cap;         // search steps before falling back
-    uint32_t fbits;       // tile words: value in the low fbits, stack apex above
-    // final pass only (axis 0)
-    float *dist;
-    int32_t *sq;
-    int32_t ndim;
-    uint32_t shape[kMaxDim];
-    double wall[kMaxDim];
-};
-
-constexpr int kTileWaves = 4;
-
-template <bool FINAL>
-__global__ void __launch_bounds__(kWave * kTileWaves) k_tile_field(TileArgs a) {
-    extern __shared__ int32_t tile[];  // [n][kWave]
-    __shared__ int hard;
-    __shared__ uint32_t any_site[kTileWaves][kWave];
-    const int t = threadIdx.x;
-    const int lane = t & (kWave - 1);
-    const int wv = __builtin_amdgcn_readfirstlane(t / kWave);  // wave-uniform
-    const int n = int(a.n);
-    const uint64_t L = uint64_t(blockIdx.x) * kWave + lane;
-    const bool live = L < a.lines;
-    const uint64_t inner = a.inner;
-    uint64_t o = 0, i = 0;
-    if (live) {
-        o = L / inner;
-        i = L - o * inner;
-    }
-    const uint64_t base = o * uint64_t(n) * inner + i;
-    // lanes past the last line read line 0 (always valid) and discard it
-    const int32_t *src = a.buf + (live ? base : 0);
-    const int32_t fmask = int32_t((1u << a.fbits) - 1u);  // also the "no site" code
-    const int cap = int(a.cap);
-
-    if (t == 0) hard = 0;
-    // Stage: each wave reads rows wv, wv + 4, ...; SB loads are issued before
-    // the first is consumed (row indices clamped so every load is in bounds).
-    uint32_t seen = 0;
-    constexpr int SB = 8;
-    for (int q0 = wv; q0 < n; q0 += kTileWaves * SB) {
-        int32_t v[SB];
-#pragma unroll
-        for (int j = 0; j < SB; ++j) {
-            const int q = min(q0 + j * kTileWaves, n - 1);
-            v[j] = src[uint64_t(q) * inner];
-        }
-#pragma unroll
-        for (int j = 0; j < SB; ++j) {
-            const int q = q0 + j * kTileWaves;
-            if (q < n) {
-                const int32_t f = (!live || v[j] == kInfI) ? fmask : v[j];
-                seen |= f != fmask;
-                tile[q * kWave + lane] = f;
-            }
-        }
-    }
-    any_site[wv][lane] = seen;
-    __syncthreads();
-    bool has_site = false;
-#pragma unroll
-    for (int w = 0; w < kTileWaves; ++w) has_site |= any_site[w][lane] != 0;
-
-    int32_t *out_i = a.buf + base;
-    auto emit = [&](int q, int32_t d2, bool none) {
-        const uint64_t off = uint64_t(q) * inner;  // uniform across the wave
-        const uint64_t g = base + off;
-        if (!FINAL) {
-            out_i[off] = none ? kInfI : d2;
-        } else {
-            int64_t v = none ? virtual_sq<int64_t>(q, uint32_t(i), a.ndim, a.shape, a.wall) : d2;
-            if (a.dist) a.dist[g] = float(sqrt(double(v)));
-            if (a.sq) a.sq[g] = int32_t(v);
-        }
-    };
-
-    // ---- windowed exact search ----------------------------------------
-    // The step loop is uniform across the wave: a lane whose search has
-    // stopped keeps taking minima, which cannot change its value (every
-    // farther candidate is at least d^2 > best).  One wave-wide vote per
-    // two steps ends the loop.
-    bool mine_hard = false;
-    const int32_t *col = tile + lane;
-    for (int q = wv; q < n; q += kTileWaves) {
-        if (!live) break;
-        int32_t best = col[q * kWave];
-        if (!has_site) {
-            emit(q, 0, true);
-            continue;
-        }
-        // Blocks of four steps per vote; a block whose rows all lie inside
-        // the line (the common case) reads without bound checks.
-        int d = 1;
-        while (d <= cap) {
-            if (__all(best < d * d)) break;
-            if (q - d - 3 >= 0 && q + d + 3 < n) {
-                const int32_t *up = col + (q - d) * kWave;
-                const int32_t *dn = col + (q + d) * kWave;
-                const int32_t u0 = up[0], u1 = up[-kWave], u2 = up[-2 * kWave], u3 = up[-3 * kWave];
-                const int32_t w0 = dn[0], w1 = dn[kWave], w2 = dn[2 * kWave], w3 = dn[3 * kWave];
-                const int32_t c0 = min(u0, w0) + d * d;
-                const int32_t c1 = min(u1, w1) + (d + 1) * (d + 1);
-                const int32_t c2 = min(u2, w2) + (d + 2) * (d + 2);
-                const int32_t c3 = min(u3, w3) + (d + 3) * (d + 3);
-                best = min(min(best, min(c0, c1)), min(c2, c3));
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int lo = q - d - j, hi = q + d + j;
-                    const int32_t x0 = lo >= 0 ? col[lo * kWave] : fmask;
-                    const int32_t x1 = hi < n ? col[hi * kWave] : fmask;
-                    best = min(best, min(x0, x1) + (d + j) * (d + j));
-                }
-            }
-            d += 4;
-        }
-        if (best >= d * d) {
-            mine_hard = true;
-        } else {
-            emit(q, best, false);
-        }
-    }
-    if (mine_hard) hard = 1;
-    __syncthreads();
-    if (!hard || wv != 0 || !live || !has_site) return;
-
-    // ---- fallback: sequential lower envelope from the LDS copy ----------
-    const int fb = int(a.fbits);
-    auto val = [&](int p) { return tile[p * kWave + lane] & fmask; };
-    auto apex = [&](int j) { return int(uint32_t(tile[j * kWave + lane]) >> fb); };
-    auto push = [&](int j, int v) {
-        int32_t &w = tile[j * kWave + lane];
-        w = (w & fmask) | int32_t(uint32_t(v) << fb);
-    };
-    int top = 0, vt = 0, vb = 0;
-    int32_t kt = 0, kb = 0, zn = 0, zd = 1;
-    for (int q = 0; q < n; ++q) {
-        const int32_t fq = val(q);
-        if (fq == fmask) continue;
-        const int32_t kq = fq + q * q;
-        int32_t num = 0, den = 1;
-        while (top > 0) {
-            num = kq - kt;
-            den = 2 * (q - vt);
-            if (top >= 2 && int64_t(num) * zd <= int64_t(zn) * den) {
-                --top;
-                vt = vb;
-                kt = kb;
-                if (top >= 2) {
-                    vb = apex(top - 2);
-                    kb = val(vb) + vb * vb;
-                    zn = kt - kb;
-                    zd = 2 * (vt - vb);
-                }
-                continue;
-            }
-            break;
-        }
-        push(top, q);
-        if (top >= 1) {
-            vb = vt;
-            kb = kt;
-            zn = num;
-            zd = den;
-        }
-        vt = q;
-        kt = kq;
-        ++top;
-    }
-    int k = 0;
-    int vc = apex(0), vn = 0;
-    int32_t kc = val(vc) + vc * vc, kn = 0, bn = 0, bd = 1;
-    if (top > 1) {
-        vn = apex(1);
-        kn = val(vn) + vn * vn;
-        bn = kn - kc;
-        bd = 2 * (vn - vc);
-    }
-    for (int q = 0; q < n; ++q) {
-        while (k + 1 < top && int64_t(bn) < int64_t(q) * bd) {
-            ++k;
-            vc = vn;
-            kc = kn;
-            if (k + 1 < top) {
-                vn = apex(k + 1);
-                kn = val(vn) + vn * vn;
-                bn = kn - kc;
-                bd = 2 * (vn - vc);
-            }
-        }
-        emit(q, kc - vc * vc + (q - vc) * (q - vc), false);
-    }
-}
-
-}  // namespace tmedt
-
-namespace tmedt {
-
-// ---------------------------------------------------------------------------
 // Paired 16-bit tiled pass: for passes whose values plus the squared search
 // reach fit in 16 bits.  A workgroup owns 128 adjacent lines; lane l of each
 // wave holds lines 2l and 2l+1 packed in one 32-bit tile word, so one LDS

@@ -167,21 +167,23 @@ int validate(const uint8_t *in, int ndim, const int64_t *shape, int64_t batch,
     return TM_OK;
 }
 
+// The paired tile takes 128 lines per workgroup: below this many lines in a
+// pass it leaves most of the chip idle, and the whole-line search (8 lines
+// per workgroup) is faster.
+constexpr uint64_t kPairMinLines = 256 * kPairLines;
+
 // Plan of one strided pass.
 struct FhPlan {
     uint32_t lpw;
     bool pack;
     int acc;  // 0 int32 with 24-bit multiplies, 1 int32, 2 int64, 3 double
     size_t lds;
-    bool tiled;      // staged tile + windowed search (k_tile_field)
     bool tiled16;    // paired 16-bit tile with guard rows (k_tile_pair)
     bool from_mask;  // tiled16 on axis ndim-2, computing the last-axis pass itself
     bool tidx;       // tiled pass on the index carrier (k_tile_idx)
     int ls_lpw;      // whole lines in LDS, windowed search (k_line_search): lines per workgroup (8 or 4), 0 = not
     bool ls_w16;     //   with a 16-bit tile
     uint32_t rbits;  // tidx, unit sampling: bits of the row in a key
-    uint32_t fbits;  // tiled: value bits of a tile word
-    uint32_t cap;    // tiled: search steps before the envelope fallback
 };
 
 // Whole-line windowed search: 8 lines per workgroup (a wave covers 8 rows
@@ -236,7 +238,7 @@ int run(Request &r) {
             const bool offsets_fit =
                 (uint64_t(n) * inner * 2 + uint64_t(n) * kPairLines) * 4 < (uint64_t(1) << 31);
             if (n <= 256 && vmax + n + 4 < uint64_t(kNone16) && tp + 1024 <= kLdsBytes && offsets_fit &&
-                total / n + kPairLines < (uint64_t(1) << 32)) {
+                total / n + kPairLines < (uint64_t(1) << 32) && total / n >= kPairMinLines) {
                 p.tiled16 = true;
                 p.lds = tp;
                 const uint32_t n2 = r.shape[nd - 1];
@@ -268,11 +270,6 @@ int run(Request &r) {
             eb = p.pack ? 4 : 8;
         }
         p.lpw = lanes_for(n, eb);
-        // Tiled pass: 64 lines x n int32 words in LDS, each word holding the
-        // value in its low fbits bits and (during a fallback) an envelope
-        // apex above them.  "No site" is coded as the all-ones value, which
-        // must exceed every real value plus the square of the farthest step
-        // a search takes (cap + 3).
         if (!index_path && r.unit) {
             // Paired 16-bit tile: every value plus the square of any distance
             // within the line stays below the "no site" code, the tile (with
@@ -284,6 +281,7 @@ int run(Request &r) {
             const bool offsets_fit =
                 (uint64_t(n) * inner * 2 + uint64_t(n) * kPairLines) * 4 < (uint64_t(1) << 31);
             if (n <= 256 && fmax + uint64_t(n + 4) * (n + 4) < uint64_t(kNone16) && tp + 1024 <= kLdsBytes &&
+                total / n >= kPairMinLines &&
                 offsets_fit && total / n + kPairLines < (uint64_t(1) << 32)) {
                 p.tiled16 = true;
                 p.lds = tp;
@@ -305,23 +303,9 @@ int run(Request &r) {
                 continue;
             }
         }
-        if (!index_path && r.unit && n > 256 && plan_line_search(p, n, total, false)) continue;
-        if (!index_path && r.unit && n <= 256) {
-            const uint32_t cap = n - 1 < 64 ? n - 1 : 64;
-            int vbits = bits_for(n - 1);
-            if (vbits < 1) vbits = 1;
-            const int fbits = 32 - vbits < 30 ? 32 - vbits : 30;
-            const uint64_t fmask = (uint64_t(1) << fbits) - 1;
-            const size_t tile = size_t(n) * kWave * 4;
-            if (tile + 2048 <= kLdsBytes && fmax + uint64_t(n - 1) * (n - 1) < (uint64_t(1) << 30) &&
-                fmask > fmax + uint64_t(cap + 4) * (cap + 4)) {
-                p.tiled = true;
-                p.fbits = uint32_t(fbits);
-                p.cap = cap;
-                p.lds = tile;
-                continue;
-            }
-        }
+        // Otherwise, unit sampling without indices: whole lines in LDS with
+        // the windowed search (32-bit tile) while they fit.
+        if (!index_path && r.unit && plan_line_search(p, n, total, false)) continue;
         // Index carrier, lines up to 256 rows: tiled windowed search.  Unit
         // sampling packs (value, row) into one key below 2^31.
         if (index_path && n <= 256) {
@@ -557,24 +541,6 @@ int run(Request &r) {
             else if (p.ls_w16) rc = fin ? TM_LS(kLinf, true, true) : TM_LS(kLinf, false, true);
             else rc = fin ? TM_LS(kLinf, true, false) : TM_LS(kLinf, false, false);
 #undef TM_LS
-        } else if (p.tiled) {
-            TileArgs tg{};
-            tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
-            tg.lines = lines;
-            tg.n = n;
-            tg.inner = uint32_t(inner);
-            tg.cap = p.cap;
-            tg.fbits = p.fbits;
-            tg.dist = r.dist;
-            tg.sq = r.sq;
-            tg.ndim = nd;
-            for (int b = 0; b < nd; ++b) {
-                tg.shape[b] = r.shape[b];
-                tg.wall[b] = r.w[b];
-            }
-            const dim3 tgrid(uint32_t((lines + kWave - 1) / kWave)), tblock(kWave * kTileWaves);
-            rc = fin ? launch("tile_field_final", k_tile_field<true>, tgrid, tblock, p.lds, r.stream, tg)
-                     : launch("tile_field", k_tile_field<false>, tgrid, tblock, p.lds, r.stream, tg);
         } else if (!index_path) {
             FieldArgs f{};
             f.buf = r.dist ? static_cast<void *>(r.dist) : static_cast<void *>(r.sq);

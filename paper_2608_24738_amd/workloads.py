@@ -32,6 +32,8 @@ batches:
   8  2-D  8x1x256x256,      background = union of 20 discs,
                             r ~ U[2.5, 30]                         (chamfer)
   9  2-D  8x1x1024x1024,    as 7                                   (EDT, dist)
+ 10  2-D  8x1x256x256,      as 8                                   (EDT, dist)
+ 11  3-D  8x1x64^3,         as 3 with r ~ U[2, 15]                 (EDT, dist)
 
 Smaller twins keep the generator and scale ball radii with the smallest
 extent, so parity tests can cover the same structure at sizes the oracle
@@ -87,6 +89,10 @@ WORKLOADS = {
                 {"count": 20, "r_min": 2.5, "r_max": 30.0}),
     9: Workload(9, "edt2d_8x1024x1024_discs", 8, (1024, 1024), "discs_bg",
                 {"count": 20, "r_min": 10.0, "r_max": 120.0}),
+    10: Workload(10, "edt2d_8x256x256_discs", 8, (256, 256), "discs_bg",
+                 {"count": 20, "r_min": 2.5, "r_max": 30.0}),
+    11: Workload(11, "edt3d_8x64x64x64_balls", 8, (64, 64, 64), "balls_fg",
+                 {"count": 30, "r_min": 2.0, "r_max": 15.0}),
 }
 
 

@@ -46,28 +46,40 @@ def check(mask, ndim, metric, tag=""):
                              % (tag, metric, mask.shape, len(bad), k, got[k], want[k]))
 
 
-# (batch, spatial, background fraction): one case per kernel path
+# (batch, spatial, background fraction).  Passes of fewer than 32768 lines
+# take the whole-line search; larger batches below take the paired tile.
 SHAPES = [
     (3, (1,), 0.0),                 # rank 1, one element, no background
     (2, (37,), 0.1),                # rank 1, span scan
     (4, (128,), 0.03),              # rank 1, word scan
     (2, (1500,), 0.002),            # rank 1, long scan
-    (2, (70, 45), 0.02),            # paired tile, odd last extent
-    (2, (100, 64), 0.02),           # mask-reading paired pass
-    (3, (256, 256), 0.001),         # mask-reading, longest paired line
+    (2, (70, 45), 0.02),            # odd last extent
+    (2, (100, 64), 0.02),
+    (3, (256, 256), 0.001),
     (1, (200, 96), 0.01),
-    (2, (129, 33), 0.05),           # 16-row blocks past 8
-    (2, (20, 16, 128), 0.002),      # 16-bit hand-over between paired passes
+    (2, (129, 33), 0.05),
+    (2, (20, 16, 128), 0.002),
     (2, (9, 33, 17), 0.03),
-    (1, (300, 5), 0.01),            # whole-line pass, final
-    (2, (600, 40, 3), 0.003),       # paired, then a whole-line final pass
-    (1, (3, 400, 8), 0.002),        # whole-line pass feeding a paired final pass
+    (1, (300, 5), 0.01),
+    (2, (600, 40, 3), 0.003),
+    (1, (3, 400, 8), 0.002),
     (1, (5, 6, 7, 8), 0.01),
     (2, (3, 4, 3, 4, 5), 0.02),
     (1, (2, 2, 2, 2, 2, 2, 2, 3), 0.05),
     (2, (1, 1), 0.0),
     (1, (1, 50), 0.05),
     (1, (50, 1), 0.05),
+]
+
+# Batches large enough for the paired tile on every strided pass, with the
+# kernel names it must report: the mask-reading first pass, 16-row blocks
+# past 8, and the 16-bit hand-over between paired passes.
+PAIRED = [
+    (513, (50, 64), 0.02, ("cdt_plane_final",)),
+    (1000, (129, 33), 0.05, ("cdt_pair_final",)),
+    (13, (33, 20, 128), 0.005, ("cdt_plane.o16", "cdt_pair_final.i16")),
+    (43, (3, 4, 7, 64), 0.1, ("cdt_plane", "cdt_pair", "cdt_pair_final")),
+    (60, (600, 40, 3), 0.003, ("cdt_pair", "cdt_line_final")),
 ]
 
 
@@ -77,6 +89,23 @@ SHAPES = [
 def test_parity(metric, batch, spatial, p):
     mask = rand_mask((batch, 1) + spatial, p, 1000 * len(spatial) + sum(spatial))
     check(mask, len(spatial), metric, "shape")
+
+
+@pytest.mark.parametrize("metric", CHAMFER)
+@pytest.mark.parametrize("batch,spatial,p,kernels", PAIRED,
+                         ids=["b%d-%s" % (b, "x".join(map(str, s))) for b, s, _, _ in PAIRED])
+def test_paired_tile(metric, batch, spatial, p, kernels):
+    from paper_2608_24738_amd import binding
+    mask = rand_mask((batch, 1) + spatial, p, 77 + sum(spatial))
+    mask[0] = 1                                   # a sample without background
+    binding.prof_enable(64)
+    try:
+        check(mask, len(spatial), metric, "paired")
+        names = {n for n, _ in binding.prof_read()}
+    finally:
+        binding.prof_enable(0)
+    for k in kernels:
+        assert k in names, (k, names)
 
 
 @pytest.mark.parametrize("metric", CHAMFER)

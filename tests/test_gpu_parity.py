@@ -185,12 +185,14 @@ def test_sqrt_is_correctly_rounded():
         assert np.array_equal(res["dist"][0], np.sqrt(d2.astype(np.float64)).astype(np.float32))
 
 
+# The paired tile takes passes of at least 32768 lines (fewer go to the
+# whole-line search), so batches are sized to reach that on every pass.
 FUSED = [
-    ((7, 50, 64), 2, 0.05),        # final pass reads the mask; 3.5 workgroups
-    ((3, 33, 192), 2, 0.01),       # workgroups straddle planes; zeros several words apart
-    ((2, 9, 21, 128), 3, 0.2),
-    ((1, 5, 160, 64), 3, 0.002),   # long lines, mostly empty rows
-    ((2, 3, 4, 7, 64), 4, 0.5),
+    ((513, 50, 64), 2, 0.05),      # final pass reads the mask; 256.5 workgroups
+    ((171, 33, 192), 2, 0.01),     # workgroups straddle planes; zeros several words apart
+    ((29, 9, 21, 128), 3, 0.2),
+    ((103, 5, 160, 64), 3, 0.002), # long lines, mostly empty rows
+    ((43, 3, 4, 7, 64), 4, 0.5),
 ]
 
 
@@ -216,9 +218,9 @@ def test_pass_reading_the_mask(shape, ndim, p_bg):
 
 
 SEG = [
-    ((3, 33, 20, 128), 3, 0.03),     # fused pass hands 16-bit runs to the final pass
-    ((2, 6, 10, 4, 64), 4, 0.1),     # axis-1 pass writes 16-bit runs (its input is 32-bit)
-    ((2, 5, 6, 7, 128), 4, 0.004),   # a middle pass both reads and writes 16-bit runs
+    ((13, 33, 20, 128), 3, 0.03),    # fused pass hands 16-bit runs to the final pass
+    ((22, 6, 10, 4, 64), 4, 0.1),    # axis-1 pass writes 16-bit runs (its input is 32-bit)
+    ((9, 5, 6, 7, 128), 4, 0.004),   # a middle pass both reads and writes 16-bit runs
 ]
 
 
@@ -226,8 +228,15 @@ SEG = [
 def test_half_width_intermediates(shape, ndim, p_bg):
     """Strides that are multiples of 128: consecutive paired passes keep the
     field as 16-bit values in the first half of each 128-element run."""
+    from paper_2608_24738_amd import binding
     mask = rand_mask(shape, p_bg, 7 + len(shape))
-    parity(mask, ndim, None, dist=True, idx=False, tag="half-width")
+    binding.prof_enable(64)
+    try:
+        parity(mask, ndim, None, dist=True, idx=False, tag="half-width")
+        names = {n for n, _ in binding.prof_read()}
+    finally:
+        binding.prof_enable(0)
+    assert any(".o16" in n for n in names) and any(".i16" in n for n in names), names
     mask[0] = 1                                   # a sample with no background
     mask[-1] = 0                                  # and one that is all background
     parity(mask, ndim, None, dist=True, idx=False, tag="half-width extremes")
