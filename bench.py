@@ -13,6 +13,7 @@ HIP-event-timed average duration), and the CPU oracle's throughput on a
 bounded sample on this host.
 """
 import argparse
+import glob
 import hashlib
 import json
 import os
@@ -23,8 +24,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E peak, GB/s
-SOURCES = ["paper_2608_24738_amd/csrc/edt_common.h", "paper_2608_24738_amd/csrc/edt_fh.h",
-           "paper_2608_24738_amd/csrc/edt_scan.h", "paper_2608_24738_amd/csrc/edt_host.hip"]
+SOURCES = sorted(os.path.relpath(p, ROOT) for p in
+                 glob.glob(os.path.join(ROOT, "paper_2608_24738_amd", "csrc", "*.h")) +
+                 glob.glob(os.path.join(ROOT, "paper_2608_24738_amd", "csrc", "*.hip")))
 
 
 def log(msg):
@@ -187,7 +189,7 @@ def bench_cdt(args, dev, stream):
 
     ms, kernels = time_op(step, args, stream)
     total = int(mask.size)
-    roofline = roofline_of(kernels, args.steps, total, w.ndim, False, w.name)
+    roofline = roofline_of(kernels, args.steps, total, w.ndim, False, "%s_%s" % (w.name, metric))
     print(json.dumps({
         "metric": "chamfer DT inputs/ms (%s), batch %dx1x%s" % (metric, w.batch,
                                                                 "x".join(map(str, w.spatial))),

@@ -136,6 +136,28 @@ int tm_dt_bf(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch
              const double *sampling, float *out_dist, int32_t *out_idx, hipStream_t stream);
 
 /*
+ * tm_edt_signed -- signed Euclidean distance transform, EDT(M) - EDT(not M)
+ * (paper, Sections 1 and 2.3.2: the distance field behind boundary-aware
+ * losses, which recompute it every training step).
+ *
+ * For every element of each sample: on foreground (nonzero) elements the
+ * distance to the nearest background element, positive; on background
+ * elements minus the distance to the nearest foreground element.  Each term
+ * follows tm_edt, so a sample holding one class only measures from the
+ * virtual element (-1, 0, ..., 0) with that class's sign.  No element is
+ * zero.  Unit sampling; float32 results, each the correctly rounded square
+ * root of the exact integer squared distance with its sign.  The mask is
+ * read once: one field carries +F on foreground and -F on background, and
+ * every pass lets an element's own class offer values and the other class
+ * offer sites.  in_u8, ndim, shape, batch as for tm_edt; out_dist: device
+ * float32 [batch][shape...], written completely.  Errors: as tm_edt (no
+ * sampling argument), and TM_ERR_UNSUPPORTED for lines longer than about
+ * 10000 elements along an axis other than the last.
+ */
+int tm_edt_signed(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
+                  float *out_dist, hipStream_t stream);
+
+/*
  * tm_cdt -- chamfer distance transform (paper, Section 2.3.2 and Table 1:
  * the taxicab and chessboard transforms, with no sampling argument).
  *

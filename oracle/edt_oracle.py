@@ -160,6 +160,18 @@ class Oracle:
         return out.astype(np.int32).reshape(mask.shape)
 
 
+def signed_edt(mask: np.ndarray, ndim: int | None = None, *, nthreads: int = 1) -> np.ndarray:
+    """Signed transform EDT(M) - EDT(not M) (the distance field of boundary
+    losses the paper's introduction and Section 2.3.2 motivate): the exact
+    transform of the mask minus that of its complement, float32, unit
+    sampling.  Exactly one of the two terms is nonzero at every element."""
+    mask = np.ascontiguousarray(mask)
+    inv = (mask == 0).astype(np.uint8)
+    pos = edt(mask, ndim, None, want_sq=False, want_idx=False, nthreads=nthreads)["dist"]
+    neg = edt(inv, ndim, None, want_sq=False, want_idx=False, nthreads=nthreads)["dist"]
+    return (pos - neg).astype(np.float32)
+
+
 def metric_dt_at(sample: np.ndarray, metric: str, points: np.ndarray) -> np.ndarray:
     """The metric value (euclidean: squared distance) from each of `points`
     (k x ndim integer coordinates) to the nearest background element of one

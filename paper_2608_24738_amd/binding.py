@@ -5,11 +5,11 @@ turns torch tensors into device pointers, shapes and the current HIP stream,
 and turns status codes into exceptions.  There is no fallback: if the library
 is missing, every call raises.
 
-Entry points with the C names (``tm_edt``, ``tm_edt_sq``, ``tm_dt_bf``,
-``tm_cdt``, ``tm_strerror``) plus ``scipy.ndimage``-style wrappers
-(``distance_transform_edt``, ``distance_transform_bf``,
-``distance_transform_cdt``) over (B, C, *spatial) tensors (paper, Section
-2.2.1).
+Entry points with the C names (``tm_edt``, ``tm_edt_sq``, ``tm_edt_signed``,
+``tm_dt_bf``, ``tm_cdt``, ``tm_strerror``) plus ``scipy.ndimage``-style
+wrappers (``distance_transform_edt``, ``distance_transform_bf``,
+``distance_transform_cdt``, ``signed_distance_transform``) over
+(B, C, *spatial) tensors (paper, Section 2.2.1).
 """
 from __future__ import annotations
 
@@ -50,6 +50,8 @@ def load() -> ctypes.CDLL:
             lib.tm_edt_sq.argtypes = [vp, i32, vp, i64, vp, vp, vp]
             lib.tm_dt_bf.restype = i32
             lib.tm_dt_bf.argtypes = [vp, i32, vp, i64, i32, vp, vp, vp, vp]
+            lib.tm_edt_signed.restype = i32
+            lib.tm_edt_signed.argtypes = [vp, i32, vp, i64, vp, vp]
             lib.tm_cdt.restype = i32
             lib.tm_cdt.argtypes = [vp, i32, vp, i64, i32, vp, vp]
             lib.tm_strerror.restype = ctypes.c_char_p
@@ -165,6 +167,20 @@ def tm_dt_bf(in_u8: torch.Tensor, ndim: int, metric: int, sampling=None, out_dis
                              _ptr(out_idx), ctypes.c_void_p(st))
     if rc != TM_OK:
         raise TMError(rc, "tm_dt_bf")
+
+
+def tm_edt_signed(in_u8: torch.Tensor, ndim: int, out_dist, stream=None) -> None:
+    """Calls tm_edt_signed (EDT(M) - EDT(not M), unit sampling, float32)."""
+    _check_mask(in_u8)
+    spatial, batch = _shape_args(in_u8, ndim)
+    vox = in_u8.numel() // max(batch, 1)
+    _check_out(out_dist, torch.float32, batch * vox, "out_dist", in_u8.device)
+    shape = (ctypes.c_int64 * ndim)(*spatial)
+    with torch.cuda.device(in_u8.device):
+        st = _stream_handle(stream)
+        rc = load().tm_edt_signed(_ptr(in_u8), ndim, shape, batch, _ptr(out_dist), ctypes.c_void_p(st))
+    if rc != TM_OK:
+        raise TMError(rc, "tm_edt_signed")
 
 
 def tm_cdt(in_u8: torch.Tensor, ndim: int, metric: int, out_dist, stream=None) -> None:
@@ -295,6 +311,25 @@ def distance_transform_cdt(input: torch.Tensor, metric: str = "chessboard", dist
     else:
         out = torch.empty(mask.shape, dtype=torch.int32, device=mask.device)
     tm_cdt(mask, ndim, METRICS[metric], out)
+    return None if distances is not None else out
+
+
+def signed_distance_transform(input: torch.Tensor, distances=None):
+    """EDT(M) - EDT(not M) of a (B, C, *spatial) batch: positive distance to
+    the background on foreground elements, minus the distance to the
+    foreground on background elements (float32, unit sampling).  A
+    pre-allocated ``distances`` is filled in place and not returned."""
+    if input.dim() < 3:
+        raise ValueError("input must be (B, C, *spatial) with 1 to 8 spatial dimensions")
+    ndim = input.dim() - 2
+    mask = _as_mask(input)
+    if distances is not None:
+        if distances.shape != mask.shape or distances.dtype != torch.float32:
+            raise RuntimeError("distances array has wrong shape or type")
+        out = distances
+    else:
+        out = torch.empty(mask.shape, dtype=torch.float32, device=mask.device)
+    tm_edt_signed(mask, ndim, out)
     return None if distances is not None else out
 
 

@@ -132,6 +132,7 @@ struct Request {
     int32_t *idx;
     hipStream_t stream;
     int metric;      // kL2 (exact transform) or kL1 / kLinf (chamfer; output in sq)
+    bool sgn;        // signed transform EDT(M) - EDT(not M) (kL2, unit, output in dist)
 };
 
 int validate(const uint8_t *in, int ndim, const int64_t *shape, int64_t batch,
@@ -225,6 +226,11 @@ int run(Request &r) {
         uint64_t fmax = 0;
         for (int b = a + 1; b < nd; ++b) fmax += uint64_t(r.shape[b] - 1) * (r.shape[b] - 1);
         FhPlan &p = fh[a];
+        if (r.sgn) {
+            // signed transform: whole-line search over the signed field
+            if (!plan_line_search(p, n, total, false)) return TM_ERR_UNSUPPORTED;
+            continue;
+        }
         if (r.metric != kL2) {
             // Chamfer transforms: the paired tile with the metric's largest
             // value plus any in-line distance below "no site", else whole
@@ -346,7 +352,23 @@ int run(Request &r) {
     int rc;
     // ---- pass over the last axis: nearest zero in each contiguous line ----
     // (computed by the next pass itself when that one reads the mask)
-    if (!(nd >= 2 && fh[nd - 2].from_mask)) {
+    if (r.sgn) {
+        SignedScanArgs s{};
+        s.in = r.in;
+        s.field = reinterpret_cast<int32_t *>(r.dist);
+        s.dist = r.dist;
+        s.n = nlast;
+        s.lines = uint32_t(total / nlast);
+        const dim3 grid(uint32_t((uint64_t(s.lines) + 3) / 4)), block(256);
+        const bool lng = (nlast + kWave - 1) / kWave > uint32_t(kSignedRegChunks);
+        if (nd == 1)
+            rc = lng ? launch("scan_signed_final", k_scan_signed<true, true>, grid, block, 0, r.stream, s)
+                     : launch("scan_signed_final", k_scan_signed<false, true>, grid, block, 0, r.stream, s);
+        else
+            rc = lng ? launch("scan_signed", k_scan_signed<true, false>, grid, block, 0, r.stream, s)
+                     : launch("scan_signed", k_scan_signed<false, false>, grid, block, 0, r.stream, s);
+        if (rc != TM_OK) return rc;
+    } else if (!(nd >= 2 && fh[nd - 2].from_mask)) {
         ScanArgs s{};
         s.in = r.in;
         s.n = nlast;
@@ -535,7 +557,14 @@ int run(Request &r) {
 #define TM_LS(M, F, W)                                                                                  \
     (p.ls_lpw == 8 ? launch(nm, k_line_search<M, F, W, 8>, lgrid, lblock, p.lds, r.stream, la)         \
                    : launch(nm, k_line_search<M, F, W, 4>, lgrid, lblock, p.lds, r.stream, la))
-            if (r.metric == kL2) rc = fin ? TM_LS(kL2, true, false) : TM_LS(kL2, false, false);
+            if (r.sgn) {
+                nm = fin ? "line_search_signed_final" : "line_search_signed";
+                rc = p.ls_lpw == 8
+                         ? (fin ? launch(nm, k_line_search<kL2, true, false, 8, true>, lgrid, lblock, p.lds, r.stream, la)
+                                : launch(nm, k_line_search<kL2, false, false, 8, true>, lgrid, lblock, p.lds, r.stream, la))
+                         : (fin ? launch(nm, k_line_search<kL2, true, false, 4, true>, lgrid, lblock, p.lds, r.stream, la)
+                                : launch(nm, k_line_search<kL2, false, false, 4, true>, lgrid, lblock, p.lds, r.stream, la));
+            } else if (r.metric == kL2) rc = fin ? TM_LS(kL2, true, false) : TM_LS(kL2, false, false);
             else if (r.metric == kL1 && p.ls_w16) rc = fin ? TM_LS(kL1, true, true) : TM_LS(kL1, false, true);
             else if (r.metric == kL1) rc = fin ? TM_LS(kL1, true, false) : TM_LS(kL1, false, false);
             else if (p.ls_w16) rc = fin ? TM_LS(kLinf, true, true) : TM_LS(kLinf, false, true);
@@ -692,6 +721,19 @@ extern "C" int tm_dt_bf(const uint8_t *in_u8, int ndim, const int64_t *shape, in
     else rc = samp ? TM_BF(2, true) : TM_BF(2, false);
 #undef TM_BF
     return rc;
+}
+
+extern "C" int tm_edt_signed(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
+                             float *out_dist, hipStream_t stream) {
+    Request r{};
+    int rc = validate(in_u8, ndim, shape, batch, nullptr, out_dist, nullptr, nullptr, r);
+    if (rc != TM_OK) return rc;
+    r.dist = out_dist;
+    r.sq = nullptr;
+    r.idx = nullptr;
+    r.stream = stream;
+    r.sgn = true;
+    return run(r);
 }
 
 extern "C" int tm_cdt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, int metric,

@@ -67,8 +67,17 @@ __device__ __forceinline__ bool ls_stop(uint32_t best, int d) {
     else return best <= uint32_t(d);
 }
 
-template <int METRIC, bool FINAL, bool W16, int LPW>
+// SIGNED (euclidean, 32-bit tile): the field is the signed transform's, +F
+// on foreground and -F on background (see k_scan_signed).  The tile keeps
+// the class in bit 31 above |F|; for an element of class c, rows of its own
+// class offer their value and rows of the other class are sites (value 0):
+// with t = word ^ (c << 31), the offer is max(int(t), 0).  The guard rows
+// repeat the end rows of the line (a repeated row read at a larger distance
+// than its own only overestimates), since no single word reads as "no site"
+// for both classes.
+template <int METRIC, bool FINAL, bool W16, int LPW, bool SIGNED = false>
 __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs a) {
+    static_assert(!SIGNED || (METRIC == kL2 && !W16), "signed transform: euclidean, 32-bit tile");
     using T = typename std::conditional<W16, uint16_t, uint32_t>::type;
     constexpr uint32_t NONE = W16 ? 0xffffu : 0xffffffffu;
     constexpr int RPW = kWave / LPW;                 // rows per wave and step
@@ -89,9 +98,11 @@ __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs
     int32_t *line = a.buf + base;
     T *row0 = tile + kLsGuard * LPW;
 
-    for (int k = t; k < kLsGuard * LPW; k += kWave * kLsWaves) {
-        tile[k] = T(NONE);
-        row0[n * LPW + k] = T(NONE);
+    if (!SIGNED) {
+        for (int k = t; k < kLsGuard * LPW; k += kWave * kLsWaves) {
+            tile[k] = T(NONE);
+            row0[n * LPW + k] = T(NONE);
+        }
     }
     if (t < LPW) has_site[t] = 0u;
     __syncthreads();
@@ -111,21 +122,31 @@ __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs
         for (int s = 0; s < SB; ++s) {
             const int q = q0 + s * STEP;
             if (q < n) {
-                row0[q * LPW + j] = v[s] == kInfI ? T(NONE) : T(v[s]);
+                if (SIGNED) row0[q * LPW + j] = v[s] < 0 ? (0x80000000u | uint32_t(-v[s])) : uint32_t(v[s]);
+                else row0[q * LPW + j] = v[s] == kInfI ? T(NONE) : T(v[s]);
                 seen |= v[s] != kInfI ? 1u : 0u;
             }
         }
     }
     if (seen) atomicOr(&has_site[j], 1u);
     __syncthreads();
-    const bool has = has_site[j] != 0u;
+    if (SIGNED) {
+        for (int k = t; k < kLsGuard * LPW; k += kWave * kLsWaves) {
+            tile[k] = row0[k % LPW];
+            row0[n * LPW + k] = row0[(n - 1) * LPW + k % LPW];
+        }
+        __syncthreads();
+    }
+    const bool has = SIGNED || has_site[j] != 0u;
 
     // ---- search and output --------------------------------------------------
     for (int qw = wv * RPW; qw < n; qw += STEP) {      // wave-uniform
         const int q = qw + sub;
         const bool mine = live && q < n;
         const int qc = min(q, n - 1);
-        uint32_t best = (mine && has) ? uint32_t(row0[qc * LPW + j]) : 0u;
+        const uint32_t own = uint32_t(row0[qc * LPW + j]);
+        const uint32_t cq = SIGNED ? (own & 0x80000000u) : 0u;     // class of the element
+        uint32_t best = (mine && has) ? (SIGNED ? own & 0x7fffffffu : own) : 0u;
         // Steps d .. d+7 read rows q-d-7 .. q-d and q+d .. q+d+7 at fixed
         // offsets from two bases.  A base moves into the guard rows only
         // when every row it stands for is beyond the line, so the reads stay
@@ -142,9 +163,11 @@ __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs
                 w[s] = ph[s * LPW];
             }
         };
+        auto offer = [&](uint32_t x) { return SIGNED ? uint32_t(max(int32_t(x ^ cq), 0)) : x; };
         auto fold = [&](int d, const uint32_t (&u)[kLsUnroll], const uint32_t (&w)[kLsUnroll]) {
 #pragma unroll
-            for (int s = 0; s < kLsUnroll; ++s) best = min(best, ls_cand<METRIC, W16>(min(u[s], w[s]), d + s));
+            for (int s = 0; s < kLsUnroll; ++s)
+                best = min(best, ls_cand<METRIC, W16>(min(offer(u[s]), offer(w[s])), d + s));
         };
         uint32_t ua[kLsUnroll], wa[kLsUnroll], ub[kLsUnroll], wb[kLsUnroll];
         int d = 1;
@@ -162,7 +185,17 @@ __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs
         }
         if (!mine) continue;
         const uint64_t e = base + uint64_t(q) * a.inner;
-        if (!FINAL) {
+        if (SIGNED) {
+            const bool none = best >= uint32_t(kInfI);     // one class in the whole sample
+            if (!FINAL) {
+                const int32_t v = none ? kInfI : int32_t(best);
+                a.buf[e] = cq ? -v : v;
+            } else {
+                const int64_t v = none ? virtual_sq<int64_t>(q, i, a.ndim, a.shape, a.wall) : int64_t(best);
+                const float dv = v < (int64_t(1) << 24) ? sqrt_rn_int(uint32_t(v)) : float(sqrt(double(v)));
+                a.dist[e] = cq ? -dv : dv;
+            }
+        } else if (!FINAL) {
             a.buf[e] = has ? int32_t(best) : kInfI;
         } else if (METRIC != kL2) {
             a.buf[e] = has ? int32_t(best) : -1;       // chamfer: nothing reachable

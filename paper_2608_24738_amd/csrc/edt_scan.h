@@ -443,3 +443,114 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
 }
 
 }  // namespace tmedt
+
+namespace tmedt {
+
+// ---------------------------------------------------------------------------
+// First pass of the signed transform EDT(M) - EDT(not M): every element
+// measures to the nearest element of the other class along its line, and
+// the field keeps one signed squared distance per element, +F for
+// foreground (distance to background) and -F for background (distance to
+// foreground), +-kInfI when the line has no element of the other class.
+// Zero never occurs, since an element is never a site of its own field.
+//
+// One wavefront per line, in 64-position chunks: two ballots mark the
+// chunk's background and foreground positions; a forward sweep carries the
+// last position of each class, a backward sweep the next one.  Lines of up
+// to kSignedRegChunks chunks keep the ballots and left candidates in
+// registers; longer lines park the left candidate in the output between the
+// sweeps (each lane rereads only what it wrote).
+// Rank 1 (FINAL): the line is the sample; the outputs are float distances
+// with the class sign, from the virtual element (-1) when the sample holds
+// one class only.
+// ---------------------------------------------------------------------------
+constexpr int kSignedRegChunks = 16;
+
+struct SignedScanArgs {
+    const uint8_t *in;
+    int32_t *field;        // signed squared distances (intermediate output)
+    float *dist;           // rank 1: signed distances
+    uint32_t n;            // line length
+    uint32_t lines;
+};
+
+template <bool LONG, bool FINAL>
+__global__ void __launch_bounds__(256) k_scan_signed(SignedScanArgs a) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const uint32_t line = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    if (line >= a.lines) return;                       // whole wavefront exits together
+    const int n = int(a.n);
+    const uint8_t *src = a.in + uint64_t(line) * a.n;
+    int32_t *fld = a.field + uint64_t(line) * a.n;
+    constexpr int kFar = 1 << 30;
+    const int nc = (n + kWave - 1) / kWave;
+    const uint64_t le = lane == kWave - 1 ? ~0ull : (2ull << lane) - 1ull;   // positions <= lane
+    constexpr int RC = LONG ? 1 : kSignedRegChunks;
+    uint64_t zs[RC], os[RC];
+    int lcand[RC];
+    auto chunk = [&](int c, uint64_t &z, uint64_t &o, bool &fg) {
+        const int pos = c * kWave + lane;
+        const bool valid = pos < n;
+        const uint8_t b = valid ? src[pos] : 0;
+        z = __ballot(valid && b == 0);
+        o = __ballot(valid && b != 0);
+        fg = valid && b != 0;
+    };
+    // ---- forward: last element of the other class at or before each position
+    int lz = -kFar, lo = -kFar;                        // last background / foreground so far
+    auto forward = [&](int c, uint64_t &z, uint64_t &o) {
+        bool fg;
+        chunk(c, z, o, fg);
+        const uint64_t opp = (fg ? z : o) & le;
+        const int left = opp ? c * kWave + 63 - __clzll(opp) : (fg ? lz : lo);
+        if (z) lz = c * kWave + 63 - __clzll(z);
+        if (o) lo = c * kWave + 63 - __clzll(o);
+        return left;
+    };
+    if (LONG) {
+        for (int c = 0; c < nc; ++c) {
+            uint64_t z, o;
+            const int left = forward(c, z, o);
+            if (c * kWave + lane < n) fld[c * kWave + lane] = left;
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < RC; ++c)
+            if (c < nc) lcand[c] = forward(c, zs[c], os[c]);
+    }
+    // ---- backward: next element of the other class, then the values
+    int nz = kFar, no = kFar;                          // next background / foreground
+    auto finish = [&](int c, uint64_t z, uint64_t o, int left) {
+        const int pos = c * kWave + lane;
+        const bool fg = (o >> lane) & 1ull;
+        const uint64_t opp = (fg ? z : o) >> lane;
+        const int right = opp ? pos + __ffsll((unsigned long long)opp) - 1 : (fg ? nz : no);
+        if (z) nz = c * kWave + __ffsll((unsigned long long)z) - 1;
+        if (o) no = c * kWave + __ffsll((unsigned long long)o) - 1;
+        if (pos >= n) return;
+        const int dl = left > -kFar ? pos - left : kFar, dr = right < kFar ? right - pos : kFar;
+        const int d = min(dl, dr);
+        if (!FINAL) {
+            const int32_t v = d < kFar ? d * d : kInfI;
+            fld[pos] = fg ? v : -v;
+        } else {
+            const float dv = d < kFar ? float(d) : float(pos + 1);   // virtual element at -1
+            a.dist[uint64_t(line) * a.n + pos] = fg ? dv : -dv;
+        }
+    };
+    if (LONG) {
+        for (int c = nc - 1; c >= 0; --c) {
+            uint64_t z, o;
+            bool fg;
+            chunk(c, z, o, fg);
+            const int left = c * kWave + lane < n ? fld[c * kWave + lane] : 0;
+            finish(c, z, o, left);
+        }
+    } else {
+#pragma unroll
+        for (int c = RC - 1; c >= 0; --c)
+            if (c < nc) finish(c, zs[c], os[c], lcand[c]);
+    }
+}
+
+}  // namespace tmedt

@@ -38,7 +38,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert {"tm_edt", "tm_edt_sq", "tm_dt_bf", "tm_cdt", "tm_strerror"} <= set(names)
+    assert {"tm_edt", "tm_edt_sq", "tm_edt_signed", "tm_dt_bf", "tm_cdt", "tm_strerror"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -170,3 +170,18 @@ def test_chamfer_binding_checks():
         binding.tm_cdt(x, 2, 1, torch.empty(16, dtype=torch.int32))       # not a GPU tensor
     with pytest.raises(RuntimeError):
         binding.distance_transform_cdt(x, distances=torch.empty((1, 1, 4, 4)))
+
+
+def test_signed_argument_checks(lib):
+    def call(shape, batch=1, inp=FAKE_IN, dist=FAKE_OUT, nd=None):
+        sh = (ctypes.c_int64 * len(shape))(*shape)
+        return lib.tm_edt_signed(inp and ctypes.c_void_p(inp), len(shape) if nd is None else nd, sh, batch,
+                                 dist and ctypes.c_void_p(dist), None)
+    assert call([4, 4], dist=0) == TM_ERR_NO_OUTPUT
+    assert call([4, 4], inp=0) == TM_ERR_NULL
+    assert call([4, 4], batch=0) == TM_ERR_BATCH
+    assert call([4, 0]) == TM_ERR_SHAPE
+    assert call([4] * 9) == TM_ERR_NDIM
+    assert call([16, 16], dist=FAKE_IN + 4) == TM_ERR_ALIAS
+    assert call([50000, 2]) == TM_ERR_TOO_LARGE          # sum of n^2 >= 2^31
+    assert call([20000, 3]) == TM_ERR_UNSUPPORTED        # strided line past the LDS tile
