@@ -52,7 +52,7 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
     fout = 2 if "o16" in tags else 4         # field bytes written
     if base.startswith("scan"):
         return total * (1 + 4)
-    if base in ("plane_pair", "cdt_plane"):  # reads the mask, writes the field
+    if base in ("plane_pair", "cdt_plane", "col_scan"):  # reads the mask, writes the field
         return total * (1 + fout)
     if base in ("plane_pair_final", "cdt_plane_final"):
         return total * (1 + out_bytes)
@@ -60,7 +60,7 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
                 "line_search"):
         return total * (fin + fout)
     if base in ("fh_field_final", "tile_pair_final", "cdt_pair_final",
-                "cdt_line_final", "line_search_final"):
+                "cdt_line_final", "line_search_final", "plane_final"):
         return total * (fin + out_bytes)
     if base in ("fh_index", "tile_idx"):
         return total * (4 + 4)

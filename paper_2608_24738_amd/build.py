@@ -1,6 +1,7 @@
 """Builds ``libtm_edt.so`` (the HIP kernels and C-ABI) in place with hipcc for gfx950."""
 from __future__ import annotations
 
+import glob
 import os
 import subprocess
 import sys
@@ -9,7 +10,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libtm_edt.so")
 SOURCES = [os.path.join(PKG, "csrc", "edt_host.hip")]
-DEPS = SOURCES + [os.path.join(PKG, "csrc", f) for f in ("edt_common.h", "edt_fh.h", "edt_scan.h")] + [
+DEPS = SOURCES + sorted(glob.glob(os.path.join(PKG, "csrc", "*.h"))) + [
     os.path.join(ROOT, "include", "tm_edt.h")]
 
 HIPCC_FLAGS = [

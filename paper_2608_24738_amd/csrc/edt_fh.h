@@ -605,9 +605,23 @@ struct PairArgs {
     int32_t in_seg;       // the input field is in the 16-bit segment layout
     int32_t out_seg;      // write the result in the 16-bit segment layout
     int32_t ndim;
+    uint32_t vox;         // PLANE: elements per sample
     uint32_t shape[kMaxDim];
     double wall[kMaxDim];
 };
+
+// Squared distance to the virtual background element (-1, 0, ..., 0) of the
+// element with in-sample flat index e (unit sampling; samples without any
+// background only).
+__device__ inline int64_t virtual_sq_flat(uint32_t e, int ndim, const uint32_t *shape) {
+    int64_t acc = 0;
+    for (int b = ndim - 1; b >= 1; --b) {
+        const uint32_t x = e % shape[b];
+        e /= shape[b];
+        acc += int64_t(x) * x;
+    }
+    return acc + int64_t(e + 1) * (e + 1);
+}
 
 // 16-bit segment layout of an intermediate field: the values of each
 // 128-element aligned run of the buffer are kept as 16-bit numbers (0xffff:
@@ -654,8 +668,16 @@ __device__ __forceinline__ float sqrt_rn_int(uint32_t x) {
 // METRIC (kL2, kL1, kLinf) selects the transform; the taxicab and
 // chessboard ones (chamfer transforms) write int32 distances in the final
 // pass, -1 for samples without background.
-template <bool FINAL, bool FROM_MASK, int MAXRB, int METRIC = kL2>
+// PLANE (final pass over the last two axes, both of extent 128, after every
+// other axis has been processed): the workgroup's 128 lines are one whole
+// plane.  After the search along axis ndim-2 the results are written back
+// transposed (lane pairs swap halves with a DPP row rotation, so each lane
+// writes whole words), the same search runs along axis ndim-1, and the
+// results are transposed back before the final stores.  The field is staged
+// once and the outputs are written once for both axes.
+template <bool FINAL, bool FROM_MASK, int MAXRB, int METRIC = kL2, bool PLANE = false>
 __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile_pair(PairArgs a) {
+    static_assert(!PLANE || (FINAL && !FROM_MASK && METRIC == kL2 && MAXRB == 8), "plane pass: final, unit euclidean, n = 128");
     extern __shared__ __attribute__((aligned(16))) uint32_t tw[];  // rows [-kGuard16, n + kGuard16) x kRowW words
     __shared__ __attribute__((aligned(8))) uint8_t any_site[kWave][kPairWaves];   // [tile word][wave]
     const int t = threadIdx.x;
@@ -860,7 +882,8 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         }
     }
     any_site[lane][wv] = uint8_t(seen);
-    __syncthreads();
+    // any site in the workgroup's lines (PLANE: in the plane)
+    const bool plane_any = __syncthreads_or(int(seen)) != 0;
 
     // ---- windowed exact search over patches ----------------------------------
     // Patches are 16 rows by 16 lines (8 tile words): lane l takes rows
@@ -877,7 +900,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         o |= o >> 8;
         return o & 3u;
     };
-    const uint32_t has = has_of(lane);                 // lines of this lane's stores
+    const uint32_t has = PLANE ? (plane_any ? 3u : 0u) : has_of(lane);   // lines of this lane's stores
     const int pr = lane >> 3;                          // row within the half patch
     // A final pass over a line with no site gives distances to the virtual
     // background element; the wave takes that path only when one of the
@@ -895,7 +918,9 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             vd = __builtin_bit_cast(uint32_t, sqrt_rn_int(uint32_t(d2)));
             vs = uint32_t(d2);
         } else {
-            const int64_t v = virtual_sq<int64_t>(q, ipos, a.ndim, a.shape, a.wall);
+            const int64_t v = PLANE ? virtual_sq_flat(uint32_t((uint64_t(wg_base) + uint32_t(q) * inner + ipos) % a.vox),
+                                                      a.ndim, a.shape)
+                                    : virtual_sq<int64_t>(q, ipos, a.ndim, a.shape, a.wall);
             vd = __builtin_bit_cast(uint32_t, float(sqrt(double(v))));
             vs = uint32_t(v);
         }
@@ -911,15 +936,14 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
     const int nrb = (n + PR - 1) / PR;                 // at most MAXRB (host)
     auto patch_word = [&](int rbk) { return kPatchRows * ((wv + rbk) & (kPairWaves - 1)) + (lane & 7); };
     u16x2 res1[MAXRB], res2[MAXRB];
+    auto search_patches = [&](auto &&searched_of) {
 #pragma unroll
     for (int rbk = 0; rbk < MAXRB; ++rbk) {
         if (rbk >= nrb) break;
         const int cw = patch_word(rbk);
         // Halves whose line is absent or has no site need no search: clearing
         // them keeps them from holding the wave's stop vote open.
-        const uint32_t has_p = has_of(cw);
-        const uint32_t searched = ((L0 + 2u * cw < a.lines && (has_p & 1u)) ? 0xffffu : 0u) |
-                                  ((L0 + 2u * cw + 1u < a.lines && (has_p & 2u)) ? 0xffff0000u : 0u);
+        const uint32_t searched = searched_of(cw);
         const int q0 = PR * rbk;                       // first row of the patch (uniform)
         const int q1 = min(q0 + pr, n - 1), q2 = min(q0 + kPatchRows + pr, n - 1);
         u16x2 best1 = as_pair(row0[q1 * kRowW + cw] & searched);
@@ -954,7 +978,43 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         res1[rbk] = best1;
         res2[rbk] = best2;
     }
+    };
+    auto searched_first = [&](int cw) {
+        const uint32_t has_p = has_of(cw);
+        return ((L0 + 2u * cw < a.lines && (has_p & 1u)) ? 0xffffu : 0u) |
+               ((L0 + 2u * cw + 1u < a.lines && (has_p & 2u)) ? 0xffff0000u : 0u);
+    };
+    search_patches(searched_first);
     __syncthreads();   // every search has read the tile
+    if constexpr (PLANE) {
+        // Transposed write-back: lane l and lane l ^ 8 hold rows q, q ^ 1 of
+        // the same two columns; each builds the word (row q even, row q odd)
+        // of one column and stores it at row = column, word = q / 2.  Halves
+        // that were not searched hold 0 (so that they never held the stop vote
+        // open) and leave as "no site".
+        auto write_transposed = [&](auto &&searched_of) {
+            const uint32_t sel = (pr & 1) ? 0x03020706u : 0x05040100u;
+#pragma unroll
+            for (int rbk = 0; rbk < MAXRB; ++rbk) {
+                const int cw = patch_word(rbk);
+                uint32_t *dst = row0 + (2 * cw + (pr & 1)) * kRowW + kPatchRows * rbk + (pr >> 1);
+                const uint32_t none = ~searched_of(cw);
+                const uint32_t o1 = as_word(res1[rbk]) | none, o2 = as_word(res2[rbk]) | none;
+                const uint32_t p1 = uint32_t(__builtin_amdgcn_mov_dpp(int(o1), 0x128, 0xf, 0xf, false));
+                const uint32_t p2 = uint32_t(__builtin_amdgcn_mov_dpp(int(o2), 0x128, 0xf, 0xf, false));
+                dst[0] = __builtin_amdgcn_perm(p1, o1, sel);
+                dst[kPatchRows / 2] = __builtin_amdgcn_perm(p2, o2, sel);
+            }
+        };
+        write_transposed(searched_first);
+        __syncthreads();
+        // every line of the plane has a site iff the plane had one
+        auto searched_all = [&](int) { return plane_any ? 0xffffffffu : 0u; };
+        search_patches(searched_all);
+        __syncthreads();
+        write_transposed(searched_all);
+        __syncthreads();
+    } else {
 #pragma unroll
     for (int rbk = 0; rbk < MAXRB; ++rbk) {
         if (rbk >= nrb) break;
@@ -964,6 +1024,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         if (q2 < n) row0[q2 * kRowW + cw] = as_word(res2[rbk]);
     }
     __syncthreads();
+    }
 
     // ---- store: wave wv writes rows wv, wv + 8, ..., one 8-byte pair per lane
     // Lanes of absent lines carry the offset kDeadOff, so their stores are

@@ -29,6 +29,7 @@
 #include "edt_fh.h"
 #include "edt_tidx.h"
 #include "edt_scan.h"
+#include "edt_col.h"
 
 using namespace tmedt;
 
@@ -204,6 +205,87 @@ bool plan_line_search(FhPlan &p, uint32_t n, uint64_t total, bool w16) {
     return true;
 }
 
+// Plane order for distance outputs of unit-sampled inputs whose last two
+// extents are 128: the axis-0 nearest-zero scan first (k_col_scan, straight
+// from the mask), then every middle axis, then one workgroup per plane of the
+// last two axes (k_tile_pair with PLANE), all in 16-bit runs.  The order of
+// the axes does not change any distance (each pass is an exact minimum), and
+// no indices are produced on this path.  Returns kNotPlane, before any
+// launch, when the input does not qualify.
+constexpr int kNotPlane = 1;
+
+int run_plane(Request &r, uint64_t total, uint64_t vox) {
+    const int nd = r.ndim;
+    if (nd < 3 || r.shape[nd - 1] != 128 || r.shape[nd - 2] != 128 || r.shape[0] > 128) return kNotPlane;
+    int32_t *buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
+    if (uintptr_t(r.in) % 4 != 0 || uintptr_t(buf) % 16 != 0) return kNotPlane;
+    const uint64_t S = vox / r.shape[0];                 // a multiple of 128 * 128
+    // Every pass keeps the field below "no site" (0xffff): the largest value
+    // before it plus the square of the farthest row it reads, guard rows
+    // included.
+    uint64_t fmax = uint64_t(r.shape[0] - 1) * (r.shape[0] - 1);
+    size_t mid_lds[kMaxDim] = {};
+    for (int a = 1; a <= nd - 3; ++a) {
+        const uint64_t n = r.shape[a];
+        uint64_t inner = 1;
+        for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
+        mid_lds[a] = size_t(n + 2 * kGuard16) * kRowW * 4;
+        if (n > 256 || fmax + (n + 4) * (n + 4) >= uint64_t(kNone16) || mid_lds[a] + 1024 > kLdsBytes ||
+            (n * inner * 2 + n * kPairLines) * 4 >= (uint64_t(1) << 31))
+            return kNotPlane;
+        fmax += (n - 1) * (n - 1);
+    }
+    const uint64_t reach = uint64_t(128 + kGuard16) * (128 + kGuard16);
+    if (fmax + reach >= uint64_t(kNone16) || fmax + 127 * 127 + reach >= uint64_t(kNone16)) return kNotPlane;
+
+    ColArgs c{};
+    c.mask = r.in;
+    c.buf = buf;
+    c.n0 = r.shape[0];
+    c.S = uint32_t(S);
+    c.blocks = uint32_t(S / kColBlock);
+    c.div_blocks = Div32::make(c.blocks);
+    int rc = launch("col_scan.o16", k_col_scan, dim3(uint32_t(total / (uint64_t(c.n0) * kColBlock))),
+                    dim3(kWave * kColWaves), 0, r.stream, c);
+    if (rc != TM_OK) return rc;
+
+    PairArgs tg{};
+    tg.buf = buf;
+    tg.total = uint32_t(total);
+    tg.dist = r.dist;
+    tg.sq = r.sq;
+    tg.ndim = nd;
+    tg.vox = uint32_t(vox);
+    for (int b = 0; b < nd; ++b) {
+        tg.shape[b] = r.shape[b];
+        tg.wall[b] = 1.0;
+    }
+    tg.in_seg = 1;
+    const dim3 tblock(kWave * kPairWaves);
+    for (int a = 1; a <= nd - 3; ++a) {
+        const uint32_t n = r.shape[a];
+        uint64_t inner = 1;
+        for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
+        tg.n = n;
+        tg.inner = uint32_t(inner);
+        tg.div_inner = Div32::make(tg.inner);
+        tg.lines = uint32_t(total / n);
+        tg.out_seg = 1;
+        const dim3 tgrid(uint32_t((total / n + kPairLines - 1) / kPairLines));
+        rc = n <= 128 ? launch("tile_pair.i16.o16", k_tile_pair<false, false, 8>, tgrid, tblock, mid_lds[a], r.stream, tg)
+                      : launch("tile_pair.i16.o16", k_tile_pair<false, false, 16>, tgrid, tblock, mid_lds[a], r.stream, tg);
+        if (rc != TM_OK) return rc;
+    }
+    tg.n = 128;
+    tg.inner = 128;
+    tg.div_inner = Div32::make(128);
+    tg.lines = uint32_t(total / 128);
+    tg.out_seg = 0;
+    const size_t lds = size_t(128 + 2 * kGuard16) * kRowW * 4;
+    return launch("plane_final.i16", k_tile_pair<true, false, 8, kL2, true>, dim3(uint32_t(total / (128 * 128))),
+                  tblock, lds, r.stream, tg);
+}
+
 int run(Request &r) {
     const int nd = r.ndim;
     uint64_t vox = 1;
@@ -218,6 +300,10 @@ int run(Request &r) {
         return TM_ERR_ALIAS;
 
     const bool index_path = r.idx != nullptr;
+    if (!index_path && r.unit && r.metric == kL2 && !r.sgn) {
+        const int rc = run_plane(r, total, vox);
+        if (rc != kNotPlane) return rc;
+    }
 
     // Plan and check every strided pass before launching anything.
     FhPlan fh[kMaxDim] = {};
