@@ -46,10 +46,11 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
     the last-axis scan reads the 1-byte mask and writes the 4-byte field,
     every strided pass reads and writes the field, and the final pass reads
     the field and writes the outputs.  A ".i16" / ".o16" suffix marks a
-    field read / written as 16-bit values (2 bytes per voxel)."""
+    field read / written as 16-bit values (2 bytes per voxel), ".i8" / ".o8"
+    as 8-bit values (1 byte per voxel)."""
     base, *tags = name.split(".")
-    fin = 2 if "i16" in tags else 4          # field bytes read
-    fout = 2 if "o16" in tags else 4         # field bytes written
+    fin = 2 if "i16" in tags else 1 if "i8" in tags else 4     # field bytes read
+    fout = 2 if "o16" in tags else 1 if "o8" in tags else 4    # field bytes written
     if base.startswith("scan"):
         return total * (1 + 4)
     if base in ("plane_pair", "cdt_plane", "col_scan"):  # reads the mask, writes the field

@@ -602,7 +602,7 @@ struct PairArgs {
     Div32 div_n2;         // FROM_MASK: division by n2
     float *dist;          // final pass outputs
     int32_t *sq;
-    int32_t in_seg;       // the input field is in the 16-bit segment layout
+    int32_t in_seg;       // the input field is in the 16-bit segment layout (2: PLANE, 8-bit plane layout)
     int32_t out_seg;      // write the result in the 16-bit segment layout
     int32_t ndim;
     uint32_t vox;         // PLANE: elements per sample
@@ -709,8 +709,18 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
     };
     bool live_a, live_b;
     uint32_t i_a, i_b, voff_a, voff_b;
-    locate(2 * lane, live_a, i_a, voff_a);
-    locate(2 * lane + 1, live_b, i_b, voff_b);
+    if constexpr (PLANE) {
+        // the workgroup's lines are the 128 columns of one plane: plain
+        // functions of the lane, which the compiler recomputes where needed
+        live_a = live_b = true;
+        i_a = 2u * uint32_t(lane);
+        i_b = i_a + 1u;
+        voff_a = 4u * i_a;
+        voff_b = voff_a + 4u;
+    } else {
+        locate(2 * lane, live_a, i_a, voff_a);
+        locate(2 * lane + 1, live_b, i_b, voff_b);
+    }
     uint32_t *row0 = tw + kGuard16 * kRowW;   // row 0 of the lines
     // Even stride: lines 2l and 2l+1 are adjacent, both live or both absent.
     const bool pair_io = (inner & 1u) == 0u;
@@ -831,7 +841,29 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         // once.  With an even stride the lane's two lines are adjacent in
         // memory and one 8-byte access serves both.
         constexpr int SB = 16;
-        if (a.in_seg) {
+        if (PLANE && a.in_seg == 2) {
+            // distances along axis 0 as bytes at the start of the plane's
+            // own 64 KiB (255: no site): 2 bytes per lane and row, squared here
+            const uint32_t vb = 2u * uint32_t(lane);
+            for (int q0 = wv; q0 < n; q0 += kPairWaves * SB) {
+                uint32_t v[SB];
+#pragma unroll
+                for (int j = 0; j < SB; ++j)
+                    v[j] = __builtin_amdgcn_raw_buffer_load_b16(rb, vb, uint32_t(min(q0 + j * kPairWaves, n - 1)) * 128u, 0);
+#pragma unroll
+                for (int j = 0; j < SB; ++j) {
+                    const int q = q0 + j * kPairWaves;
+                    if (q < n) {
+                        const u16x2 d = as_pair(__builtin_amdgcn_perm(0u, v[j], 0x0c010c00u));
+                        // 255 -> 0xffff, else d^2 (d <= 127)
+                        const uint32_t none = as_word((d + splat(1)) >> splat(8)) * 0xffffu;
+                        const uint32_t w = as_word(d * d) | none;
+                        seen |= ((w & 0xffffu) != 0xffffu ? 1u : 0u) | ((w >> 16) != 0xffffu ? 2u : 0u);
+                        row0[q * kRowW + lane] = w;
+                    }
+                }
+            }
+        } else if (a.in_seg) {
             // whole runs: one 4-byte read per lane holds both lines
             const uint32_t vs = seg_offset(voff_a);
             for (int q0 = wv; q0 < n; q0 += kPairWaves * SB) {

@@ -218,8 +218,10 @@ int run_plane(Request &r, uint64_t total, uint64_t vox) {
     const int nd = r.ndim;
     if (nd < 3 || r.shape[nd - 1] != 128 || r.shape[nd - 2] != 128 || r.shape[0] > 128) return kNotPlane;
     int32_t *buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
-    if (uintptr_t(r.in) % 4 != 0 || uintptr_t(buf) % 16 != 0) return kNotPlane;
+    if (uintptr_t(r.in) % 2 != 0 || uintptr_t(buf) % 16 != 0) return kNotPlane;
     const uint64_t S = vox / r.shape[0];                 // a multiple of 128 * 128
+    // the column scan addresses a wave's 16 rows with 32-bit offsets 4 * S * j
+    if (S >= (uint64_t(1) << 25)) return kNotPlane;
     // Every pass keeps the field below "no site" (0xffff): the largest value
     // before it plus the square of the farthest row it reads, guard rows
     // included.
@@ -245,8 +247,11 @@ int run_plane(Request &r, uint64_t total, uint64_t vox) {
     c.S = uint32_t(S);
     c.blocks = uint32_t(S / kColBlock);
     c.div_blocks = Div32::make(c.blocks);
-    int rc = launch("col_scan.o16", k_col_scan, dim3(uint32_t(total / (uint64_t(c.n0) * kColBlock))),
-                    dim3(kWave * kColWaves), 0, r.stream, c);
+    // With no middle axis the plane pass reads the axis-0 distances as bytes.
+    const bool bytes = nd == 3;
+    const dim3 cgrid(uint32_t(total / (uint64_t(c.n0) * kColBlock))), cblock(kWave * kColWaves);
+    int rc = bytes ? launch("col_scan.o8", k_col_scan<true>, cgrid, cblock, 0, r.stream, c)
+                   : launch("col_scan.o16", k_col_scan<false>, cgrid, cblock, 0, r.stream, c);
     if (rc != TM_OK) return rc;
 
     PairArgs tg{};
@@ -281,9 +286,10 @@ int run_plane(Request &r, uint64_t total, uint64_t vox) {
     tg.div_inner = Div32::make(128);
     tg.lines = uint32_t(total / 128);
     tg.out_seg = 0;
+    tg.in_seg = bytes ? 2 : 1;
     const size_t lds = size_t(128 + 2 * kGuard16) * kRowW * 4;
-    return launch("plane_final.i16", k_tile_pair<true, false, 8, kL2, true>, dim3(uint32_t(total / (128 * 128))),
-                  tblock, lds, r.stream, tg);
+    return launch(bytes ? "plane_final.i8" : "plane_final.i16", k_tile_pair<true, false, 8, kL2, true>,
+                  dim3(uint32_t(total / (128 * 128))), tblock, lds, r.stream, tg);
 }
 
 int run(Request &r) {

@@ -35,10 +35,13 @@ def parity_plane(mask, ndim, tag, dist=True, sq=True, expect_plane=True):
     ora = edt_oracle.edt(mask, ndim, None, nthreads=16)
     check_against_oracle(mask, ndim, None, res, ora)
     if expect_plane:
-        assert "col_scan.o16" in names and "plane_final.i16" in names, names
+        # 3-D: the axis-0 distances reach the plane pass as bytes; with middle
+        # axes they travel as 16-bit squares
+        fmt = ("o8", "i8") if ndim == 3 else ("o16", "i16")
+        assert "col_scan." + fmt[0] in names and "plane_final." + fmt[1] in names, names
         assert not any(n.startswith(("plane_pair", "scan_")) for n in names), names
     else:
-        assert "plane_final.i16" not in names, names
+        assert not any(n.startswith("plane_final") for n in names), names
     return names
 
 
