@@ -1043,6 +1043,36 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         // every line of the plane has a site iff the plane had one
         auto searched_all = [&](int) { return plane_any ? 0xffffffffu : 0u; };
         search_patches(searched_all);
+        if (plane_any) {
+            // Every element has a site: swap halves across lane pairs as
+            // above, which leaves each lane two elements of one row (the
+            // rows and columns of the plane in their memory order), and store
+            // them straight from registers.  The tile is not read again.
+            const uint32_t sel = (pr & 1) ? 0x03020706u : 0x05040100u;
+            auto dist_pair = [](uint32_t w) {
+                return u32x2{__builtin_bit_cast(uint32_t, sqrt_rn_int(w & 0xffffu)),
+                             __builtin_bit_cast(uint32_t, sqrt_rn_int(w >> 16))};
+            };
+#pragma unroll
+            for (int rbk = 0; rbk < MAXRB; ++rbk) {
+                const int cw = patch_word(rbk);
+                const uint32_t o1 = as_word(res1[rbk]), o2 = as_word(res2[rbk]);
+                const uint32_t p1 = uint32_t(__builtin_amdgcn_mov_dpp(int(o1), 0x128, 0xf, 0xf, false));
+                const uint32_t p2 = uint32_t(__builtin_amdgcn_mov_dpp(int(o2), 0x128, 0xf, 0xf, false));
+                const uint32_t w1 = __builtin_amdgcn_perm(p1, o1, sel), w2 = __builtin_amdgcn_perm(p2, o2, sel);
+                // row 2 cw + (pr & 1), columns 16 rbk + (pr & ~1) + {0, 1} (+ 8 for w2)
+                const uint32_t off = uint32_t((2 * cw + (pr & 1)) * 128 + PR * rbk + (pr & ~1)) * 4u;
+                if (want_d) {
+                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w1), rd, off, 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w2), rd, off + 4u * kPatchRows, 0, 0);
+                }
+                if (want_s) {
+                    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w1 & 0xffffu, w1 >> 16}, rs, off, 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w2 & 0xffffu, w2 >> 16}, rs, off + 4u * kPatchRows, 0, 0);
+                }
+            }
+            return;
+        }
         __syncthreads();
         write_transposed(searched_all);
         __syncthreads();
