@@ -968,7 +968,9 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
     const int nrb = (n + PR - 1) / PR;                 // at most MAXRB (host)
     auto patch_word = [&](int rbk) { return kPatchRows * ((wv + rbk) & (kPairWaves - 1)) + (lane & 7); };
     u16x2 res1[MAXRB], res2[MAXRB];
-    auto search_patches = [&](auto &&searched_of) {
+    // emit(rbk, best1, best2) receives each patch's results as soon as its
+    // search is done
+    auto search_patches = [&](auto &&searched_of, auto &&emit) {
 #pragma unroll
     for (int rbk = 0; rbk < MAXRB; ++rbk) {
         if (rbk >= nrb) break;
@@ -1007,8 +1009,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             d += 4;
             if (d > n + 4) break;   // every row has been examined
         }
-        res1[rbk] = best1;
-        res2[rbk] = best2;
+        emit(rbk, best1, best2);
     }
     };
     auto searched_first = [&](int cw) {
@@ -1016,9 +1017,16 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         return ((L0 + 2u * cw < a.lines && (has_p & 1u)) ? 0xffffu : 0u) |
                ((L0 + 2u * cw + 1u < a.lines && (has_p & 2u)) ? 0xffff0000u : 0u);
     };
-    search_patches(searched_first);
+    auto keep = [&](int rbk, u16x2 best1, u16x2 best2) {
+        res1[rbk] = best1;
+        res2[rbk] = best2;
+    };
+    // A plane without any site keeps "no site" everywhere: no search, and
+    // the stores below give the virtual background element.
+    if (!PLANE || plane_any) search_patches(searched_first, keep);
     __syncthreads();   // every search has read the tile
     if constexpr (PLANE) {
+      if (plane_any) {
         // Transposed write-back: lane l and lane l ^ 8 hold rows q, q ^ 1 of
         // the same two columns; each builds the word (row q even, row q odd)
         // of one column and stores it at row = column, word = q / 2.  Halves
@@ -1040,42 +1048,35 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         };
         write_transposed(searched_first);
         __syncthreads();
-        // every line of the plane has a site iff the plane had one
-        auto searched_all = [&](int) { return plane_any ? 0xffffffffu : 0u; };
-        search_patches(searched_all);
-        if (plane_any) {
-            // Every element has a site: swap halves across lane pairs as
-            // above, which leaves each lane two elements of one row (the
-            // rows and columns of the plane in their memory order), and store
-            // them straight from registers.  The tile is not read again.
-            const uint32_t sel = (pr & 1) ? 0x03020706u : 0x05040100u;
-            auto dist_pair = [](uint32_t w) {
-                return u32x2{__builtin_bit_cast(uint32_t, sqrt_rn_int(w & 0xffffu)),
-                             __builtin_bit_cast(uint32_t, sqrt_rn_int(w >> 16))};
-            };
-#pragma unroll
-            for (int rbk = 0; rbk < MAXRB; ++rbk) {
-                const int cw = patch_word(rbk);
-                const uint32_t o1 = as_word(res1[rbk]), o2 = as_word(res2[rbk]);
-                const uint32_t p1 = uint32_t(__builtin_amdgcn_mov_dpp(int(o1), 0x128, 0xf, 0xf, false));
-                const uint32_t p2 = uint32_t(__builtin_amdgcn_mov_dpp(int(o2), 0x128, 0xf, 0xf, false));
-                const uint32_t w1 = __builtin_amdgcn_perm(p1, o1, sel), w2 = __builtin_amdgcn_perm(p2, o2, sel);
-                // row 2 cw + (pr & 1), columns 16 rbk + (pr & ~1) + {0, 1} (+ 8 for w2)
-                const uint32_t off = uint32_t((2 * cw + (pr & 1)) * 128 + PR * rbk + (pr & ~1)) * 4u;
-                if (want_d) {
-                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w1), rd, off, 0, 0);
-                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w2), rd, off + 4u * kPatchRows, 0, 0);
-                }
-                if (want_s) {
-                    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w1 & 0xffffu, w1 >> 16}, rs, off, 0, 0);
-                    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w2 & 0xffffu, w2 >> 16}, rs, off + 4u * kPatchRows, 0, 0);
-                }
+        // Every line of the transposed tile has a site.  Each patch's results
+        // are stored as soon as its search is done: swapping halves across
+        // lane pairs as above leaves each lane two elements of one row (rows
+        // and columns of the plane in their memory order), and the tile is
+        // not written again.
+        const uint32_t sel = (pr & 1) ? 0x03020706u : 0x05040100u;
+        auto dist_pair = [](uint32_t w) {
+            return u32x2{__builtin_bit_cast(uint32_t, sqrt_rn_int(w & 0xffffu)),
+                         __builtin_bit_cast(uint32_t, sqrt_rn_int(w >> 16))};
+        };
+        search_patches([](int) { return 0xffffffffu; }, [&](int rbk, u16x2 best1, u16x2 best2) {
+            const int cw = patch_word(rbk);
+            const uint32_t o1 = as_word(best1), o2 = as_word(best2);
+            const uint32_t p1 = uint32_t(__builtin_amdgcn_mov_dpp(int(o1), 0x128, 0xf, 0xf, false));
+            const uint32_t p2 = uint32_t(__builtin_amdgcn_mov_dpp(int(o2), 0x128, 0xf, 0xf, false));
+            const uint32_t w1 = __builtin_amdgcn_perm(p1, o1, sel), w2 = __builtin_amdgcn_perm(p2, o2, sel);
+            // row 2 cw + (pr & 1), columns 16 rbk + (pr & ~1) + {0, 1} (+ 8 for w2)
+            const uint32_t off = uint32_t((2 * cw + (pr & 1)) * 128 + PR * rbk + (pr & ~1)) * 4u;
+            if (want_d) {
+                __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w1), rd, off, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w2), rd, off + 4u * kPatchRows, 0, 0);
             }
-            return;
-        }
-        __syncthreads();
-        write_transposed(searched_all);
-        __syncthreads();
+            if (want_s) {
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{w1 & 0xffffu, w1 >> 16}, rs, off, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{w2 & 0xffffu, w2 >> 16}, rs, off + 4u * kPatchRows, 0, 0);
+            }
+        });
+        return;
+      }
     } else {
 #pragma unroll
     for (int rbk = 0; rbk < MAXRB; ++rbk) {
