@@ -916,6 +916,15 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
     any_site[lane][wv] = uint8_t(seen);
     // any site in the workgroup's lines (PLANE: in the plane)
     const bool plane_any = __syncthreads_or(int(seen)) != 0;
+    // PLANE: the 8 padding words of each tile row (1088 words, never read by
+    // the searches) hold the correctly rounded square roots of 0..1023 for
+    // the final stores: entry i at row i / 8 (counting the guard rows), word
+    // 64 + i % 8.  Read only after the barriers that follow the first search.
+    constexpr int kLut = 1024;
+    if constexpr (PLANE) {
+        for (int i = t; i < kLut; i += kWave * kPairWaves)
+            tw[(i >> 3) * kRowW + kWave + (i & 7)] = __builtin_bit_cast(uint32_t, sqrt_rn_int(uint32_t(i)));
+    }
 
     // ---- windowed exact search over patches ----------------------------------
     // Patches are 16 rows by 16 lines (8 tile words): lane l takes rows
@@ -1058,6 +1067,8 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             return u32x2{__builtin_bit_cast(uint32_t, sqrt_rn_int(w & 0xffffu)),
                          __builtin_bit_cast(uint32_t, sqrt_rn_int(w >> 16))};
         };
+        auto lut = [&](uint32_t v) { return tw[(v >> 3) * kRowW + kWave + (v & 7u)]; };
+        auto dist_pair_lut = [&](uint32_t w) { return u32x2{lut(w & 0xffffu), lut(w >> 16)}; };
         search_patches([](int) { return 0xffffffffu; }, [&](int rbk, u16x2 best1, u16x2 best2) {
             const int cw = patch_word(rbk);
             const uint32_t o1 = as_word(best1), o2 = as_word(best2);
@@ -1067,8 +1078,15 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             // row 2 cw + (pr & 1), columns 16 rbk + (pr & ~1) + {0, 1} (+ 8 for w2)
             const uint32_t off = uint32_t((2 * cw + (pr & 1)) * 128 + PR * rbk + (pr & ~1)) * 4u;
             if (want_d) {
-                __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w1), rd, off, 0, 0);
-                __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w2), rd, off + 4u * kPatchRows, 0, 0);
+                // table lookups when every squared distance of the wave is below 1024
+                const u16x2 m = __builtin_elementwise_max(best1, best2);
+                if (__all(max(uint32_t(m.x), uint32_t(m.y)) < uint32_t(kLut))) {
+                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair_lut(w1), rd, off, 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair_lut(w2), rd, off + 4u * kPatchRows, 0, 0);
+                } else {
+                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w1), rd, off, 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w2), rd, off + 4u * kPatchRows, 0, 0);
+                }
             }
             if (want_s) {
                 __builtin_amdgcn_raw_buffer_store_b64(u32x2{w1 & 0xffffu, w1 >> 16}, rs, off, 0, 0);
