@@ -49,10 +49,42 @@ struct IdxTileArgs {
 // LDS words of the two tile arrays for lines of n rows.
 __host__ __device__ constexpr uint32_t idx_tile_words(uint32_t n) { return (n + 2 * kIdxGuard) * kIdxRowW; }
 
+// Sampled search blocks BLK .. NBLK-1 (four steps each, unrolled at compile
+// time): candidates f(q -+ d) + w d^2 at immediate LDS offsets from `pb`,
+// the word of row q - 4 NBLK (every read stays in the tile).  Keeps the
+// first strictly smaller candidate and its row offset; ends early once every
+// lane of the wave has w d^2 above its best value.
+template <int BLK, int NBLK>
+__device__ __forceinline__ void search_samp(const uint32_t *pb, float w, float &fbest, int &roff, int &dnext) {
+    if constexpr (BLK < NBLK) {
+        constexpr int d = 1 + 4 * BLK;
+        constexpr int R = 4 * NBLK;
+        if (__all(w * float(d * d) > fbest)) return;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const int dd = d + s;
+            const float add = w * float(dd * dd);
+            const float cu = __builtin_bit_cast(float, pb[(R - dd) * kIdxRowW]) + add;
+            const float cv = __builtin_bit_cast(float, pb[(R + dd) * kIdxRowW]) + add;
+            if (cu < fbest) {
+                fbest = cu;
+                roff = -dd;
+            }
+            if (cv < fbest) {
+                fbest = cv;
+                roff = dd;
+            }
+        }
+        dnext = d + 4;
+        search_samp<BLK + 1, NBLK>(pb, w, fbest, roff, dnext);
+    }
+}
+
 template <bool SAMP, bool FINAL>
 __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
     extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
     __shared__ __attribute__((aligned(16))) uint8_t any_site[kWave][kIdxWaves];   // [line][wave]
+    __shared__ uint4 line_info[kWave];     // per line: sample, base of row 0, position i, live
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
@@ -82,30 +114,44 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         l.base = o * a.n * a.inner + l.i;       // in-sample flat of row 0
         return l;
     };
-    // squared distance over the axes after `ax` between position i of the
-    // line and site y (in-sample flat), or "none"
-    auto carried = [&](uint32_t i, int32_t y, uint32_t &key_or_bits, int q) {
+    // Coordinates along the axes after `ax` of the position i of this lane's
+    // line (staging), computed once.
+    int xc[kMaxDim] = {};
+    float wf[kMaxDim] = {};
+    auto line_coords = [&](uint32_t xi) {
+#pragma unroll
+        for (int b = kMaxDim - 1; b >= 0; --b) {
+            if (b > ax && b < nd) {
+                const uint32_t qx = a.div_shape[b].div(xi);
+                xc[b] = int(xi - qx * a.div_shape[b].d);
+                wf[b] = float(a.wall[b]);
+                xi = qx;
+            }
+        }
+    };
+    // squared distance over the axes after `ax` between this lane's line and
+    // site y (in-sample flat), or "none" (sampled: float sum of the exact
+    // integer squares times the squared sampling)
+    auto carried = [&](int32_t y, uint32_t &key_or_bits, int q) {
         if (y < 0) {
             key_or_bits = SAMP ? __builtin_bit_cast(uint32_t, __builtin_inff()) : uint32_t(kInfI);
             return;
         }
         uint32_t yi = a.div_inner.div(uint32_t(y));
         yi = uint32_t(y) - yi * a.inner;               // site position along the later axes
-        uint32_t xi = i;
-        double accd = 0.0;
+        float accf = 0.0f;
         uint32_t acci = 0;
 #pragma unroll
         for (int b = kMaxDim - 1; b >= 0; --b) {
             if (b > ax && b < nd) {
-                const uint32_t qy = a.div_shape[b].div(yi), qx = a.div_shape[b].div(xi);
-                const int dy = int(yi - qy * a.div_shape[b].d) - int(xi - qx * a.div_shape[b].d);
+                const uint32_t qy = a.div_shape[b].div(yi);
+                const int dy = int(yi - qy * a.div_shape[b].d) - xc[b];
                 yi = qy;
-                xi = qx;
-                if (SAMP) accd += a.wall[b] * double(dy) * double(dy);
+                if (SAMP) accf += wf[b] * float(dy * dy);
                 else acci += uint32_t(dy * dy);
             }
         }
-        key_or_bits = SAMP ? __builtin_bit_cast(uint32_t, float(accd)) : ((acci << a.rbits) | uint32_t(q));
+        key_or_bits = SAMP ? __builtin_bit_cast(uint32_t, accf) : ((acci << a.rbits) | uint32_t(q));
     };
 
     // ---- guard rows and staging ---------------------------------------------
@@ -115,6 +161,8 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         val0[n * kIdxRowW + k] = none;
     }
     const Line me = line_of(lane);
+    if (wv == 0) line_info[lane] = uint4{me.s, me.base, me.i, me.live ? 1u : 0u};
+    line_coords(me.i);
     const int32_t *src = a.idx + uint64_t(me.s) * uint32_t(nd) * a.vox + me.base;
     uint32_t seen = 0;
     constexpr int SB = 8;
@@ -128,7 +176,7 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
             if (q < n) {
                 const int32_t yy = me.live ? y[j] : -1;
                 uint32_t v;
-                carried(me.i, yy, v, q);
+                carried(yy, v, q);
                 seen |= yy >= 0 ? 1u : 0u;
                 val0[q * kIdxRowW + lane] = v;
                 site0[q * kIdxRowW + lane] = yy;
@@ -161,7 +209,20 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
             kbest = 0;
             fbest = 0.0f;
         }
-        for (int d = 1;; d += 4) {
+        int d0 = 1;
+        if constexpr (SAMP) {
+            // Unrolled blocks while every read of the patch stays in the tile
+            // (guard rows included); the loop below takes over from d0.
+            const int q_lo = kIdxPatch * rbk, q_hi = min(q_lo + kIdxPatch - 1, n - 1);
+            const int room = min(q_lo + kIdxGuard, n - 1 + kIdxGuard - q_hi);
+            int roff = 0;
+            if (room >= 16) search_samp<0, 4>(col + (q - 16) * kIdxRowW, w, fbest, roff, d0);
+            else if (room >= 12) search_samp<0, 3>(col + (q - 12) * kIdxRowW, w, fbest, roff, d0);
+            else if (room >= 8) search_samp<0, 2>(col + (q - 8) * kIdxRowW, w, fbest, roff, d0);
+            else if (room >= 4) search_samp<0, 1>(col + (q - 4) * kIdxRowW, w, fbest, roff, d0);
+            r_best = q + roff;
+        }
+        for (int d = d0;; d += 4) {
             bool done;
             if (SAMP) done = w * float(d) * float(d) > fbest;
             else done = (uint64_t(uint32_t(d) * uint32_t(d)) << a.rbits) > uint64_t(kbest);
@@ -194,8 +255,12 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         }
         if (qr >= n) continue;
         // ---- output of element (row qr, line ln) ----------------------------
-        const Line l = line_of(ln);
-        if (!l.live) continue;
+        const uint4 li = line_info[ln];
+        if (!li.w) continue;
+        Line l;
+        l.s = li.x;
+        l.base = li.y;
+        l.i = li.z;
         slice0 = a.idx + uint64_t(l.s) * uint32_t(nd) * a.vox;
         const uint64_t e = uint64_t(l.base) + uint64_t(qr) * a.inner;   // in-sample flat
         int32_t site = -1;
