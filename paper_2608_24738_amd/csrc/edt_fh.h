@@ -845,6 +845,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             // distances along axis 0 as bytes at the start of the plane's
             // own 64 KiB (255: no site): 2 bytes per lane and row, squared here
             const uint32_t vb = 2u * uint32_t(lane);
+            u16x2 lo = splat(kNone16);               // per half: smallest value staged
             for (int q0 = wv; q0 < n; q0 += kPairWaves * SB) {
                 uint32_t v[SB];
 #pragma unroll
@@ -856,13 +857,14 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
                     if (q < n) {
                         const u16x2 d = as_pair(__builtin_amdgcn_perm(0u, v[j], 0x0c010c00u));
                         // 255 -> 0xffff, else d^2 (d <= 127)
-                        const uint32_t none = as_word((d + splat(1)) >> splat(8)) * 0xffffu;
+                        const uint32_t none = as_word(splat(0) - (d >> splat(7)));
                         const uint32_t w = as_word(d * d) | none;
-                        seen |= ((w & 0xffffu) != 0xffffu ? 1u : 0u) | ((w >> 16) != 0xffffu ? 2u : 0u);
+                        lo = __builtin_elementwise_min(lo, as_pair(w));
                         row0[q * kRowW + lane] = w;
                     }
                 }
             }
+            seen = (lo.x != kNone16 ? 1u : 0u) | (lo.y != kNone16 ? 2u : 0u);
         } else if (a.in_seg) {
             // whole runs: one 4-byte read per lane holds both lines
             const uint32_t vs = seg_offset(voff_a);
@@ -988,7 +990,8 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         // them keeps them from holding the wave's stop vote open.
         const uint32_t searched = searched_of(cw);
         const int q0 = PR * rbk;                       // first row of the patch (uniform)
-        const int q1 = min(q0 + pr, n - 1), q2 = min(q0 + kPatchRows + pr, n - 1);
+        // (PLANE: 128 rows, every patch row exists)
+        const int q1 = PLANE ? q0 + pr : min(q0 + pr, n - 1), q2 = PLANE ? q1 + kPatchRows : min(q0 + kPatchRows + pr, n - 1);
         u16x2 best1 = as_pair(row0[q1 * kRowW + cw] & searched);
         u16x2 best2 = as_pair(row0[q2 * kRowW + cw] & searched);
         int d = 1;
