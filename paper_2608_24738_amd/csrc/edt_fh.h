@@ -1021,6 +1021,12 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             d += 4;
             if (d > n + 4) break;   // every row has been examined
         }
+        if constexpr (PLANE) {
+            // halves that were not searched hold 0 (so that they never held
+            // the stop vote open) and leave as "no site"
+            best1 = as_pair(as_word(best1) | ~searched);
+            best2 = as_pair(as_word(best2) | ~searched);
+        }
         emit(rbk, best1, best2);
     }
     };
@@ -1041,24 +1047,21 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
       if (plane_any) {
         // Transposed write-back: lane l and lane l ^ 8 hold rows q, q ^ 1 of
         // the same two columns; each builds the word (row q even, row q odd)
-        // of one column and stores it at row = column, word = q / 2.  Halves
-        // that were not searched hold 0 (so that they never held the stop vote
-        // open) and leave as "no site".
-        auto write_transposed = [&](auto &&searched_of) {
+        // of one column and stores it at row = column, word = q / 2.
+        auto write_transposed = [&]() {
             const uint32_t sel = (pr & 1) ? 0x03020706u : 0x05040100u;
 #pragma unroll
             for (int rbk = 0; rbk < MAXRB; ++rbk) {
                 const int cw = patch_word(rbk);
                 uint32_t *dst = row0 + (2 * cw + (pr & 1)) * kRowW + kPatchRows * rbk + (pr >> 1);
-                const uint32_t none = ~searched_of(cw);
-                const uint32_t o1 = as_word(res1[rbk]) | none, o2 = as_word(res2[rbk]) | none;
+                const uint32_t o1 = as_word(res1[rbk]), o2 = as_word(res2[rbk]);
                 const uint32_t p1 = uint32_t(__builtin_amdgcn_mov_dpp(int(o1), 0x128, 0xf, 0xf, false));
                 const uint32_t p2 = uint32_t(__builtin_amdgcn_mov_dpp(int(o2), 0x128, 0xf, 0xf, false));
                 dst[0] = __builtin_amdgcn_perm(p1, o1, sel);
                 dst[kPatchRows / 2] = __builtin_amdgcn_perm(p2, o2, sel);
             }
         };
-        write_transposed(searched_first);
+        write_transposed();
         __syncthreads();
         // Every line of the transposed tile has a site.  Each patch's results
         // are stored as soon as its search is done: swapping halves across
