@@ -668,16 +668,19 @@ __device__ __forceinline__ float sqrt_rn_int(uint32_t x) {
 // METRIC (kL2, kL1, kLinf) selects the transform; the taxicab and
 // chessboard ones (chamfer transforms) write int32 distances in the final
 // pass, -1 for samples without background.
-// PLANE (final pass over the last two axes, both of extent 128, after every
-// other axis has been processed): the workgroup's 128 lines are one whole
-// plane.  After the search along axis ndim-2 the results are written back
-// transposed (lane pairs swap halves with a DPP row rotation, so each lane
-// writes whole words), the same search runs along axis ndim-1, and the
-// results are transposed back before the final stores.  The field is staged
+// PLANE = P (final pass over the last two axes, both of extent P = 128 or
+// 64, after every other axis has been processed): the workgroup's 128 lines
+// are whole planes (one of 128 x 128 or two of 64 x 64, of one sample).
+// After the search along axis ndim-2 the results are written back transposed
+// within each plane (lane pairs swap halves with a DPP row rotation, so each
+// lane writes whole words), the same search runs along axis ndim-1, and each
+// patch's results are stored straight from registers.  The field is staged
 // once and the outputs are written once for both axes.
-template <bool FINAL, bool FROM_MASK, int MAXRB, int METRIC = kL2, bool PLANE = false>
+template <bool FINAL, bool FROM_MASK, int MAXRB, int METRIC = kL2, int PLANE = 0>
 __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile_pair(PairArgs a) {
-    static_assert(!PLANE || (FINAL && !FROM_MASK && METRIC == kL2 && MAXRB == 8), "plane pass: final, unit euclidean, n = 128");
+    static_assert(PLANE == 0 || ((PLANE == 64 || PLANE == 128) && FINAL && !FROM_MASK && METRIC == kL2 && MAXRB == 8),
+                  "plane pass: final, unit euclidean, planes of 64 or 128");
+    constexpr int HP = PLANE / 2;                  // words per plane row (plane extent / 2)
     extern __shared__ __attribute__((aligned(16))) uint32_t tw[];  // rows [-kGuard16, n + kGuard16) x kRowW words
     __shared__ __attribute__((aligned(8))) uint8_t any_site[kWave][kPairWaves];   // [tile word][wave]
     const int t = threadIdx.x;
@@ -710,10 +713,11 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
     bool live_a, live_b;
     uint32_t i_a, i_b, voff_a, voff_b;
     if constexpr (PLANE) {
-        // the workgroup's lines are the 128 columns of one plane: plain
+        // the workgroup's lines are the columns of whole planes: plain
         // functions of the lane, which the compiler recomputes where needed
+        // (ipos counts from the workgroup's first element)
         live_a = live_b = true;
-        i_a = 2u * uint32_t(lane);
+        i_a = uint32_t((2 * lane) / PLANE) * uint32_t(PLANE * PLANE) + uint32_t((2 * lane) % PLANE);
         i_b = i_a + 1u;
         voff_a = 4u * i_a;
         voff_b = voff_a + 4u;
@@ -866,13 +870,16 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             }
             seen = (lo.x != kNone16 ? 1u : 0u) | (lo.y != kNone16 ? 2u : 0u);
         } else if (a.in_seg) {
-            // whole runs: one 4-byte read per lane holds both lines
+            // whole runs: one 4-byte read per lane holds both lines (rows of
+            // 64 x 64 planes are half runs: rows 2k and 2k+1 share run k, the
+            // odd row's values 128 bytes after the even row's)
             const uint32_t vs = seg_offset(voff_a);
+            auto seg_row = [&](uint32_t q) { return PLANE == 64 ? 512u * (q >> 1) + 128u * (q & 1u) : q * row_bytes; };
             for (int q0 = wv; q0 < n; q0 += kPairWaves * SB) {
                 uint32_t v[SB];
 #pragma unroll
                 for (int j = 0; j < SB; ++j) {
-                    const uint32_t so = uint32_t(min(q0 + j * kPairWaves, n - 1)) * row_bytes;
+                    const uint32_t so = seg_row(uint32_t(min(q0 + j * kPairWaves, n - 1)));
                     v[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, vs, so, 0);
                 }
 #pragma unroll
@@ -918,11 +925,12 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
     any_site[lane][wv] = uint8_t(seen);
     // any site in the workgroup's lines (PLANE: in the plane)
     const bool plane_any = __syncthreads_or(int(seen)) != 0;
-    // PLANE: the 8 padding words of each tile row (1088 words, never read by
-    // the searches) hold the correctly rounded square roots of 0..1023 for
-    // the final stores: entry i at row i / 8 (counting the guard rows), word
-    // 64 + i % 8.  Read only after the barriers that follow the first search.
-    constexpr int kLut = 1024;
+    // PLANE: the 8 padding words of each tile row (1088 / 576 words, never
+    // read by the searches) hold the correctly rounded square roots of
+    // 0..1023 (0..511 for 64-row planes) for the final stores: entry i at row
+    // i / 8 (counting the guard rows), word 64 + i % 8.  Read only after the
+    // barriers that follow the first search.
+    constexpr int kLut = PLANE == 64 ? 512 : 1024;
     if constexpr (PLANE) {
         for (int i = t; i < kLut; i += kWave * kPairWaves)
             tw[(i >> 3) * kRowW + kWave + (i & 7)] = __builtin_bit_cast(uint32_t, sqrt_rn_int(uint32_t(i)));
@@ -1046,14 +1054,15 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
     if constexpr (PLANE) {
       if (plane_any) {
         // Transposed write-back: lane l and lane l ^ 8 hold rows q, q ^ 1 of
-        // the same two columns; each builds the word (row q even, row q odd)
-        // of one column and stores it at row = column, word = q / 2.
+        // the same two columns of plane p; each builds the word (row q even,
+        // row q odd) of one column c and stores it at row c, word
+        // p * P / 2 + q / 2.
         auto write_transposed = [&]() {
             const uint32_t sel = (pr & 1) ? 0x03020706u : 0x05040100u;
 #pragma unroll
-            for (int rbk = 0; rbk < MAXRB; ++rbk) {
+            for (int rbk = 0; rbk < PLANE / PR; ++rbk) {
                 const int cw = patch_word(rbk);
-                uint32_t *dst = row0 + (2 * cw + (pr & 1)) * kRowW + kPatchRows * rbk + (pr >> 1);
+                uint32_t *dst = row0 + (2 * (cw % HP) + (pr & 1)) * kRowW + (cw / HP) * HP + kPatchRows * rbk + (pr >> 1);
                 const uint32_t o1 = as_word(res1[rbk]), o2 = as_word(res2[rbk]);
                 const uint32_t p1 = uint32_t(__builtin_amdgcn_mov_dpp(int(o1), 0x128, 0xf, 0xf, false));
                 const uint32_t p2 = uint32_t(__builtin_amdgcn_mov_dpp(int(o2), 0x128, 0xf, 0xf, false));
@@ -1081,10 +1090,12 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             const uint32_t p1 = uint32_t(__builtin_amdgcn_mov_dpp(int(o1), 0x128, 0xf, 0xf, false));
             const uint32_t p2 = uint32_t(__builtin_amdgcn_mov_dpp(int(o2), 0x128, 0xf, 0xf, false));
             const uint32_t w1 = __builtin_amdgcn_perm(p1, o1, sel), w2 = __builtin_amdgcn_perm(p2, o2, sel);
-            // row 2 cw + (pr & 1), columns 16 rbk + (pr & ~1) + {0, 1} (+ 8 for w2)
-            const uint32_t off = uint32_t((2 * cw + (pr & 1)) * 128 + PR * rbk + (pr & ~1)) * 4u;
+            // plane cw / (P/2), row 2 (cw % (P/2)) + (pr & 1), columns
+            // 16 rbk + (pr & ~1) + {0, 1} (+ 8 for w2)
+            const uint32_t off = uint32_t((cw / HP) * PLANE * PLANE + (2 * (cw % HP) + (pr & 1)) * PLANE +
+                                          PR * rbk + (pr & ~1)) * 4u;
             if (want_d) {
-                // table lookups when every squared distance of the wave is below 1024
+                // table lookups when every squared distance of the wave is in the table
                 const u16x2 m = __builtin_elementwise_max(best1, best2);
                 if (__all(max(uint32_t(m.x), uint32_t(m.y)) < uint32_t(kLut))) {
                     __builtin_amdgcn_raw_buffer_store_b64(dist_pair_lut(w1), rd, off, 0, 0);

@@ -205,10 +205,15 @@ bool plan_line_search(FhPlan &p, uint32_t n, uint64_t total, bool w16) {
     return true;
 }
 
-// Plane order for distance outputs of unit-sampled inputs whose last two
-// extents are 128: the axis-0 nearest-zero scan first (k_col_scan, straight
-// from the mask), then every middle axis, then one workgroup per plane of the
-// last two axes (k_tile_pair with PLANE), all in 16-bit runs.  The order of
+// Plane order for distance outputs of unit-sampled rank-3 inputs whose last
+// two extents are both 128, or both 64 with an even number of planes per
+// sample: the axis-0 nearest-zero scan first (k_col_scan, straight from the
+// mask), then one workgroup per 128 lines of the last two axes (one
+// 128 x 128 plane or two 64 x 64 planes; k_tile_pair with PLANE).  Axis-0
+// distances reach 128 x 128 planes as bytes, 64 x 64 planes as 16-bit
+// squares.  (Rank 4 would put the middle axes between the two kernels; on a
+// sparse 4-D input that order measured slower than the last-axis-first one,
+// whose early passes see fewer empty lines.)  The order of
 // the axes does not change any distance (each pass is an exact minimum), and
 // no indices are produced on this path.  Returns kNotPlane, before any
 // launch, when the input does not qualify.
@@ -216,29 +221,22 @@ constexpr int kNotPlane = 1;
 
 int run_plane(Request &r, uint64_t total, uint64_t vox) {
     const int nd = r.ndim;
-    if (nd < 3 || r.shape[nd - 1] != 128 || r.shape[nd - 2] != 128 || r.shape[0] > 128) return kNotPlane;
+    const uint32_t P = r.shape[nd - 1];
+    if (nd != 3 || (P != 128 && P != 64) || r.shape[nd - 2] != P || r.shape[0] > 128) return kNotPlane;
+    // 64 x 64 planes: a workgroup takes two planes of one sample
+    if (P == 64 && (vox / (64 * 64)) % 2 != 0) return kNotPlane;
     int32_t *buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
     if (uintptr_t(r.in) % 2 != 0 || uintptr_t(buf) % 16 != 0) return kNotPlane;
     const uint64_t S = vox / r.shape[0];                 // a multiple of 128 * 128
     // the column scan addresses a wave's 16 rows with 32-bit offsets 4 * S * j
     if (S >= (uint64_t(1) << 25)) return kNotPlane;
-    // Every pass keeps the field below "no site" (0xffff): the largest value
-    // before it plus the square of the farthest row it reads, guard rows
-    // included.
-    uint64_t fmax = uint64_t(r.shape[0] - 1) * (r.shape[0] - 1);
-    size_t mid_lds[kMaxDim] = {};
-    for (int a = 1; a <= nd - 3; ++a) {
-        const uint64_t n = r.shape[a];
-        uint64_t inner = 1;
-        for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
-        mid_lds[a] = size_t(n + 2 * kGuard16) * kRowW * 4;
-        if (n > 256 || fmax + (n + 4) * (n + 4) >= uint64_t(kNone16) || mid_lds[a] + 1024 > kLdsBytes ||
-            (n * inner * 2 + n * kPairLines) * 4 >= (uint64_t(1) << 31))
-            return kNotPlane;
-        fmax += (n - 1) * (n - 1);
-    }
-    const uint64_t reach = uint64_t(128 + kGuard16) * (128 + kGuard16);
-    if (fmax + reach >= uint64_t(kNone16) || fmax + 127 * 127 + reach >= uint64_t(kNone16)) return kNotPlane;
+    // Both searches keep the field below "no site" (0xffff): the largest
+    // value before a search plus the square of the farthest row it reads,
+    // guard rows included.
+    const uint64_t fmax = uint64_t(r.shape[0] - 1) * (r.shape[0] - 1);
+    const uint64_t reach = uint64_t(P + kGuard16) * (P + kGuard16);
+    if (fmax + reach >= uint64_t(kNone16) || fmax + uint64_t(P - 1) * (P - 1) + reach >= uint64_t(kNone16))
+        return kNotPlane;
 
     ColArgs c{};
     c.mask = r.in;
@@ -247,8 +245,8 @@ int run_plane(Request &r, uint64_t total, uint64_t vox) {
     c.S = uint32_t(S);
     c.blocks = uint32_t(S / kColBlock);
     c.div_blocks = Div32::make(c.blocks);
-    // With no middle axis the plane pass reads the axis-0 distances as bytes.
-    const bool bytes = nd == 3;
+    // A 128 x 128 plane pass reads the axis-0 distances as bytes.
+    const bool bytes = P == 128;
     const dim3 cgrid(uint32_t(total / (uint64_t(c.n0) * kColBlock))), cblock(kWave * kColWaves);
     int rc = bytes ? launch("col_scan.o8", k_col_scan<true>, cgrid, cblock, 0, r.stream, c)
                    : launch("col_scan.o16", k_col_scan<false>, cgrid, cblock, 0, r.stream, c);
@@ -265,31 +263,19 @@ int run_plane(Request &r, uint64_t total, uint64_t vox) {
         tg.shape[b] = r.shape[b];
         tg.wall[b] = 1.0;
     }
-    tg.in_seg = 1;
     const dim3 tblock(kWave * kPairWaves);
-    for (int a = 1; a <= nd - 3; ++a) {
-        const uint32_t n = r.shape[a];
-        uint64_t inner = 1;
-        for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
-        tg.n = n;
-        tg.inner = uint32_t(inner);
-        tg.div_inner = Div32::make(tg.inner);
-        tg.lines = uint32_t(total / n);
-        tg.out_seg = 1;
-        const dim3 tgrid(uint32_t((total / n + kPairLines - 1) / kPairLines));
-        rc = n <= 128 ? launch("tile_pair.i16.o16", k_tile_pair<false, false, 8>, tgrid, tblock, mid_lds[a], r.stream, tg)
-                      : launch("tile_pair.i16.o16", k_tile_pair<false, false, 16>, tgrid, tblock, mid_lds[a], r.stream, tg);
-        if (rc != TM_OK) return rc;
-    }
-    tg.n = 128;
-    tg.inner = 128;
-    tg.div_inner = Div32::make(128);
-    tg.lines = uint32_t(total / 128);
+    tg.n = P;
+    tg.inner = P;
+    tg.div_inner = Div32::make(P);
+    tg.lines = uint32_t(total / P);
     tg.out_seg = 0;
     tg.in_seg = bytes ? 2 : 1;
-    const size_t lds = size_t(128 + 2 * kGuard16) * kRowW * 4;
-    return launch(bytes ? "plane_final.i8" : "plane_final.i16", k_tile_pair<true, false, 8, kL2, true>,
-                  dim3(uint32_t(total / (128 * 128))), tblock, lds, r.stream, tg);
+    const size_t lds = size_t(P + 2 * kGuard16) * kRowW * 4;
+    const dim3 pgrid(uint32_t(total / P / kPairLines));
+    if (P == 64)
+        return launch("plane_final.i16", k_tile_pair<true, false, 8, kL2, 64>, pgrid, tblock, lds, r.stream, tg);
+    return launch(bytes ? "plane_final.i8" : "plane_final.i16", k_tile_pair<true, false, 8, kL2, 128>, pgrid, tblock,
+                  lds, r.stream, tg);
 }
 
 int run(Request &r) {

@@ -1,6 +1,7 @@
 """GPU parity of the plane-ordered path (unit sampling, distance outputs,
-last two extents 128): axis-0 nearest-zero scan from the mask, middle axes,
-then one workgroup per plane of the last two axes.  Squared distances and
+rank 3 with the last two extents both 128, or both 64 with an even number of
+planes per sample): axis-0 nearest-zero scan from the mask, then one
+workgroup per 128 x 128 plane or pair of 64 x 64 planes.  Squared distances and
 distances must equal the oracle's bit for bit; the kernel names the library
 reports show which path ran."""
 import numpy as np
@@ -37,7 +38,7 @@ def parity_plane(mask, ndim, tag, dist=True, sq=True, expect_plane=True):
     if expect_plane:
         # 3-D: the axis-0 distances reach the plane pass as bytes; with middle
         # axes they travel as 16-bit squares
-        fmt = ("o8", "i8") if ndim == 3 else ("o16", "i16")
+        fmt = ("o8", "i8") if mask.shape[-1] == 128 else ("o16", "i16")
         assert "col_scan." + fmt[0] in names and "plane_final." + fmt[1] in names, names
         assert not any(n.startswith(("plane_pair", "scan_")) for n in names), names
     else:
@@ -84,14 +85,10 @@ def test_degenerate_samples():
     parity_plane(mask, 3, "degenerate")
 
 
-def test_four_dims_middle_axis():
-    """4-D: the axis-1 pass runs between the scan and the plane pass on
-    16-bit runs."""
-    mask = rand_mask((2, 9, 5, 128, 128), 0.003, 44)
-    names = parity_plane(mask, 4, "4-D")
-    assert "tile_pair.i16.o16" in names, names
-    mask = workloads.make_mask(5, (6, 3, 128, 128), 2)
-    parity_plane(mask, 4, "4-D sparse")
+def test_four_dims_keep_the_other_path():
+    """Rank 4 with 128 x 128 planes runs the last-axis-first order."""
+    parity_plane(rand_mask((2, 9, 5, 128, 128), 0.003, 44), 4, "4-D", expect_plane=False)
+    parity_plane(workloads.make_mask(5, (6, 3, 128, 128), 2), 4, "4-D sparse", expect_plane=False)
 
 
 def test_fallbacks_keep_the_other_path():
@@ -104,3 +101,28 @@ def test_full_headline_with_squares():
     """8 x 128^3 balls: exact squared distances and distances in one call."""
     mask = workloads.make_mask(3)
     parity_plane(mask, 3, "headline")
+
+
+# ---- 64 x 64 planes (two per workgroup, 16-bit runs of half-run rows) -------
+@pytest.mark.parametrize("n0", [2, 6, 64, 128])
+def test_planes_64(n0):
+    mask = rand_mask((3, n0, 64, 64), 0.01, 200 + n0)
+    parity_plane(mask, 3, "64 n0=%d" % n0)
+
+
+def test_planes_64_structures():
+    parity_plane(workloads.make_mask(11), 3, "8x64^3 balls")
+    parity_plane(workloads.make_mask(5, (24, 64, 64), 2), 3, "sparse background")
+
+
+def test_planes_64_degenerate_and_odd():
+    shape = (4, 8, 64, 64)
+    mask = np.ones(shape, np.uint8)
+    mask[0] = 0                               # all background
+    # mask[1]: no background (virtual element)
+    mask[2, 7, 63, 0] = 0
+    mask[3, :, 31, 32] = 0
+    parity_plane(mask, 3, "64 degenerate")
+    # an odd number of planes per sample keeps the other path
+    parity_plane(rand_mask((2, 5, 64, 64), 0.02, 9), 3, "64 odd planes", expect_plane=False)
+
