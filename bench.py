@@ -57,11 +57,13 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
         return total * (1 + fout)
     if base in ("plane_pair_final", "cdt_plane_final"):
         return total * (1 + out_bytes)
+    if base == "scan_signed":                # mask in, signed field out
+        return total * (1 + 4)
     if base in ("fh_field", "tile_pair", "cdt_pair", "cdt_line", "cdt_none",
-                "line_search"):
+                "line_search", "line_search_signed"):
         return total * (fin + fout)
     if base in ("fh_field_final", "tile_pair_final", "cdt_pair_final",
-                "cdt_line_final", "line_search_final", "plane_final"):
+                "cdt_line_final", "line_search_final", "plane_final", "line_search_signed_final"):
         return total * (fin + out_bytes)
     if base in ("fh_index", "tile_idx"):
         return total * (4 + 4)
@@ -205,6 +207,37 @@ def bench_cdt(args, dev, stream):
         "source_digest": source_digest()}), flush=True)
 
 
+def bench_signed(args, dev, stream):
+    """Signed transform EDT(M) - EDT(not M) (the boundary-loss field) of an
+    EDT workload (default: the 8 x 1 x 128^3 balls); float32 output."""
+    import torch
+
+    from paper_2608_24738_amd import binding, workloads
+    key = args.workload
+    w = workloads.WORKLOADS[key]
+    log("generating %s" % w.name)
+    mask = workloads.make_mask(key)
+    x = torch.from_numpy(mask).to(dev)
+    out = torch.empty(mask.shape, dtype=torch.float32, device=dev)
+
+    def step():
+        binding.tm_edt_signed(x, w.ndim, out, stream=stream)
+
+    ms, kernels = time_op(step, args, stream)
+    total = int(mask.size)
+    roofline = roofline_of(kernels, args.steps, total, w.ndim, False, "%s_signed" % w.name)
+    print(json.dumps({
+        "metric": "signed EDT voxels/sec, %s" % w.name,
+        "value": total / (ms * 1e-3), "unit": "voxels/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "int32", "data": "synthetic",
+        "config": {"workload": w.name, "outputs": "float32 signed distances",
+                   "mask_sha256": workloads.mask_digest(mask)[:16]},
+        "roofline": roofline,
+        "kernels": kernels,
+        "source_digest": source_digest()}), flush=True)
+
+
 def bench_bf(args, dev, stream):
     """Brute-force transform: 8 x 256^2 images whose background is a seeded
     1 % Bernoulli sample (the paper times its brute-force transform on 256^2
@@ -256,9 +289,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run only a plain 256 MiB device copy (counter calibration)")
-    ap.add_argument("--op", default="edt", choices=["edt", "bf", "cdt"],
+    ap.add_argument("--op", default="edt", choices=["edt", "bf", "cdt", "signed"],
                     help="edt: the exact transform (headline); bf: the brute-force transform; "
-                         "cdt: the chamfer transform (workload 7 or 8)")
+                         "cdt: the chamfer transform (workload 7 or 8); signed: EDT(M) - EDT(not M)")
     ap.add_argument("--metric", default="euclidean", choices=["euclidean", "taxicab", "chessboard"],
                     help="metric of --op bf / cdt (cdt: euclidean means chessboard)")
     args = ap.parse_args()
@@ -294,6 +327,8 @@ def main():
         return bench_bf(args, dev, stream)
     if args.op == "cdt":
         return bench_cdt(args, dev, stream)
+    if args.op == "signed":
+        return bench_signed(args, dev, stream)
 
     w = workloads.WORKLOADS[args.workload]
     log("generating %s" % w.name)
