@@ -499,6 +499,14 @@ __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void *p, uint64_t bytes
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, n, 0x00020000);
 }
 
+// LDS byte address of a pointer into workgroup memory, and a 32-bit read at one.
+typedef __attribute__((address_space(3))) uint32_t lds_u32_t;
+__device__ __forceinline__ uint32_t lds_byte_addr(const uint32_t *p) {
+    return uint32_t(reinterpret_cast<uintptr_t>((const lds_u32_t *)p));
+}
+__device__ __forceinline__ uint32_t lds_word(uint32_t byte_addr) {
+    return *(const lds_u32_t *)(uintptr_t)byte_addr;
+}
 __device__ __forceinline__ u16x2 as_pair(uint32_t v) { return __builtin_bit_cast(u16x2, v); }
 __device__ __forceinline__ uint32_t as_word(u16x2 v) { return __builtin_bit_cast(uint32_t, v); }
 __device__ __forceinline__ u16x2 splat(int v) { return u16x2{uint16_t(v), uint16_t(v)}; }
@@ -683,6 +691,9 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
     constexpr int HP = PLANE / 2;                  // words per plane row (plane extent / 2)
     extern __shared__ __attribute__((aligned(16))) uint32_t tw[];  // rows [-kGuard16, n + kGuard16) x kRowW words
     __shared__ __attribute__((aligned(8))) uint8_t any_site[kWave][kPairWaves];   // [tile word][wave]
+    // PLANE: per wave, ballots over the 64 tile words of "line 2w (2w + 1)
+    // has a site in the wave's rows": {even lo, even hi, odd lo, odd hi}
+    __shared__ __attribute__((aligned(16))) uint32_t site_ballot[kPairWaves][4];
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
@@ -922,7 +933,14 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             }
         }
     }
-    any_site[lane][wv] = uint8_t(seen);
+    if constexpr (PLANE) {
+        const uint64_t be = __ballot(seen & 1u), bo = __ballot(seen & 2u);
+        if (lane == 0)
+            *reinterpret_cast<uint4 *>(site_ballot[wv]) =
+                uint4{uint32_t(be), uint32_t(be >> 32), uint32_t(bo), uint32_t(bo >> 32)};
+    } else {
+        any_site[lane][wv] = uint8_t(seen);
+    }
     // any site in the workgroup's lines (PLANE: in the plane)
     const bool plane_any = __syncthreads_or(int(seen)) != 0;
     // PLANE: the 8 padding words of each tile row (1088 / 576 words, never
@@ -996,7 +1014,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         const int cw = patch_word(rbk);
         // Halves whose line is absent or has no site need no search: clearing
         // them keeps them from holding the wave's stop vote open.
-        const uint32_t searched = searched_of(cw);
+        const uint32_t searched = searched_of(cw, (wv + rbk) & (kPairWaves - 1));
         const int q0 = PR * rbk;                       // first row of the patch (uniform)
         // (PLANE: 128 rows, every patch row exists)
         const int q1 = PLANE ? q0 + pr : min(q0 + pr, n - 1), q2 = PLANE ? q1 + kPatchRows : min(q0 + kPatchRows + pr, n - 1);
@@ -1013,16 +1031,26 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         else if (nb == 3) search_pair2<0, 3, METRIC>(row0 + (q1 - 12) * kRowW + cw, best1, best2, d);
         else if (nb == 2) search_pair2<0, 2, METRIC>(row0 + (q1 - 8) * kRowW + cw, best1, best2, d);
         else if (nb == 1) search_pair2<0, 1, METRIC>(row0 + (q1 - 4) * kRowW + cw, best1, best2, d);
-        // Longer searches and rows near the ends: row indices clamp into
-        // the guard rows.
+        // Longer searches and rows near the ends: reads clamp into the
+        // guard rows.  The clamp works on LDS byte addresses, so each read
+        // costs one add and one min / max, against uniform bounds: the first
+        // data word of the first guard row and the last one of the last
+        // guard row.  (A row stride exceeds the data words of a row, so a
+        // read past the guard rows is clamped to one of those two words,
+        // which hold "no site" like the whole guard row.)
+        const uint32_t a1 = lds_byte_addr(row0 + q1 * kRowW + cw), a2 = lds_byte_addr(row0 + q2 * kRowW + cw);
+        const uint32_t a_lo = lds_byte_addr(tw);
+        const uint32_t a_hi = lds_byte_addr(row0 + (n + kGuard16 - 1) * kRowW + (kWave - 1));
         while (!__all(stop_at<METRIC>(__builtin_elementwise_max(best1, best2), d))) {
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
                 const int dd = d + s;
-                const int lo1 = max(q1 - dd, -kGuard16), hi1 = min(q1 + dd, n + kGuard16 - 1);
-                const int lo2 = max(q2 - dd, -kGuard16), hi2 = min(q2 + dd, n + kGuard16 - 1);
-                const u16x2 u = as_pair(row0[lo1 * kRowW + cw]), w = as_pair(row0[hi1 * kRowW + cw]);
-                const u16x2 x = as_pair(row0[lo2 * kRowW + cw]), y = as_pair(row0[hi2 * kRowW + cw]);
+                const uint32_t step = 4u * uint32_t(dd * kRowW);   // uniform
+                // a1 - step may wrap below 0 when dd is large: compare as signed
+                const u16x2 u = as_pair(lds_word(uint32_t(max(int(a1 - step), int(a_lo)))));
+                const u16x2 w = as_pair(lds_word(min(a1 + step, a_hi)));
+                const u16x2 x = as_pair(lds_word(uint32_t(max(int(a2 - step), int(a_lo)))));
+                const u16x2 y = as_pair(lds_word(min(a2 + step, a_hi)));
                 best1 = __builtin_elementwise_min(best1, cand<METRIC>(__builtin_elementwise_min(u, w), dd));
                 best2 = __builtin_elementwise_min(best2, cand<METRIC>(__builtin_elementwise_min(x, y), dd));
             }
@@ -1038,10 +1066,33 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         emit(rbk, best1, best2);
     }
     };
-    auto searched_first = [&](int cw) {
-        const uint32_t has_p = has_of(cw);
-        return ((L0 + 2u * cw < a.lines && (has_p & 1u)) ? 0xffffu : 0u) |
-               ((L0 + 2u * cw + 1u < a.lines && (has_p & 2u)) ? 0xffff0000u : 0u);
+    // PLANE: the OR of the waves' ballots (uniform); every line is live
+    uint32_t sb[4] = {0u, 0u, 0u, 0u};
+    if constexpr (PLANE) {
+#pragma unroll
+        for (int w = 0; w < kPairWaves; ++w) {
+            const uint4 v = *reinterpret_cast<const uint4 *>(site_ballot[w]);
+            sb[0] |= v.x;
+            sb[1] |= v.y;
+            sb[2] |= v.z;
+            sb[3] |= v.w;
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) sb[k] = __builtin_amdgcn_readfirstlane(sb[k]);
+    }
+    auto searched_first = [&](int cw, int cb) -> uint32_t {
+        if constexpr (PLANE) {
+            // word cw = 8 cb + lane % 8: bit cw of the ballots
+            const uint32_t sh = 8u * uint32_t(cb & 3);
+            const uint32_t e = ((cb & 4) ? sb[1] : sb[0]) >> sh, o = ((cb & 4) ? sb[3] : sb[2]) >> sh;
+            const uint32_t lo = uint32_t(__builtin_amdgcn_sbfe(int(e), uint32_t(lane & 7), 1u));
+            const uint32_t hi = uint32_t(__builtin_amdgcn_sbfe(int(o), uint32_t(lane & 7), 1u));
+            return (lo & 0xffffu) | (hi & 0xffff0000u);
+        } else {
+            const uint32_t has_p = has_of(cw);
+            return ((L0 + 2u * cw < a.lines && (has_p & 1u)) ? 0xffffu : 0u) |
+                   ((L0 + 2u * cw + 1u < a.lines && (has_p & 2u)) ? 0xffff0000u : 0u);
+        }
     };
     auto keep = [&](int rbk, u16x2 best1, u16x2 best2) {
         res1[rbk] = best1;
@@ -1082,32 +1133,36 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             return u32x2{__builtin_bit_cast(uint32_t, sqrt_rn_int(w & 0xffffu)),
                          __builtin_bit_cast(uint32_t, sqrt_rn_int(w >> 16))};
         };
-        auto lut = [&](uint32_t v) { return tw[(v >> 3) * kRowW + kWave + (v & 7u)]; };
+        const uint32_t lut_base = lds_byte_addr(tw + kWave);
+        auto lut = [&](uint32_t v) { return lds_word(__umul24(v >> 3, 4u * kRowW) + lut_base + ((v & 7u) << 2)); };
         auto dist_pair_lut = [&](uint32_t w) { return u32x2{lut(w & 0xffffu), lut(w >> 16)}; };
-        search_patches([](int) { return 0xffffffffu; }, [&](int rbk, u16x2 best1, u16x2 best2) {
-            const int cw = patch_word(rbk);
+        // Word cw = 8 cb + lane % 8 of column block cb: plane cw / (P/2), row
+        // 2 (cw % (P/2)) + (pr & 1), columns 16 rbk + (pr & ~1) + {0, 1} (+ 8
+        // for the second row of the patch).  The lane's part of the byte
+        // offset is fixed; the block's part is uniform (scalar offset).
+        constexpr int CBP = HP / 8;                   // column blocks per plane
+        const uint32_t off_l = uint32_t((2 * (lane & 7) + (pr & 1)) * PLANE + (pr & ~1)) * 4u;
+        search_patches([](int, int) { return 0xffffffffu; }, [&](int rbk, u16x2 best1, u16x2 best2) {
+            const int cb = (wv + rbk) & (kPairWaves - 1);
             const uint32_t o1 = as_word(best1), o2 = as_word(best2);
             const uint32_t p1 = uint32_t(__builtin_amdgcn_mov_dpp(int(o1), 0x128, 0xf, 0xf, false));
             const uint32_t p2 = uint32_t(__builtin_amdgcn_mov_dpp(int(o2), 0x128, 0xf, 0xf, false));
             const uint32_t w1 = __builtin_amdgcn_perm(p1, o1, sel), w2 = __builtin_amdgcn_perm(p2, o2, sel);
-            // plane cw / (P/2), row 2 (cw % (P/2)) + (pr & 1), columns
-            // 16 rbk + (pr & ~1) + {0, 1} (+ 8 for w2)
-            const uint32_t off = uint32_t((cw / HP) * PLANE * PLANE + (2 * (cw % HP) + (pr & 1)) * PLANE +
-                                          PR * rbk + (pr & ~1)) * 4u;
+            const uint32_t off = uint32_t((cb / CBP) * PLANE * PLANE + 16 * (cb % CBP) * PLANE + PR * rbk) * 4u;
             if (want_d) {
                 // table lookups when every squared distance of the wave is in the table
                 const u16x2 m = __builtin_elementwise_max(best1, best2);
                 if (__all(max(uint32_t(m.x), uint32_t(m.y)) < uint32_t(kLut))) {
-                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair_lut(w1), rd, off, 0, 0);
-                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair_lut(w2), rd, off + 4u * kPatchRows, 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair_lut(w1), rd, off_l, off, 0);
+                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair_lut(w2), rd, off_l, off + 4u * kPatchRows, 0);
                 } else {
-                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w1), rd, off, 0, 0);
-                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w2), rd, off + 4u * kPatchRows, 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w1), rd, off_l, off, 0);
+                    __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w2), rd, off_l, off + 4u * kPatchRows, 0);
                 }
             }
             if (want_s) {
-                __builtin_amdgcn_raw_buffer_store_b64(u32x2{w1 & 0xffffu, w1 >> 16}, rs, off, 0, 0);
-                __builtin_amdgcn_raw_buffer_store_b64(u32x2{w2 & 0xffffu, w2 >> 16}, rs, off + 4u * kPatchRows, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{w1 & 0xffffu, w1 >> 16}, rs, off_l, off, 0);
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{w2 & 0xffffu, w2 >> 16}, rs, off_l, off + 4u * kPatchRows, 0);
             }
         });
         return;
