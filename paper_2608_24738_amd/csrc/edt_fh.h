@@ -1133,9 +1133,19 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             return u32x2{__builtin_bit_cast(uint32_t, sqrt_rn_int(w & 0xffffu)),
                          __builtin_bit_cast(uint32_t, sqrt_rn_int(w >> 16))};
         };
+        // Table entry v sits at row v / 8, word kWave + v % 8: byte address
+        // base + 288 (v / 8) + 4 (v % 8) = base + 256 (v / 8) + 4 v.  For
+        // v < kLut that is below 2^16 (the tile is under 40 KB), so both
+        // halves of a word get their addresses in packed 16-bit arithmetic.
+        static_assert(PLANE == 0 || (PLANE + 2 * kGuard16) * kRowW * 4 + 1024 < 65536, "table addresses fit 16 bits");
         const uint32_t lut_base = lds_byte_addr(tw + kWave);
-        auto lut = [&](uint32_t v) { return lds_word(__umul24(v >> 3, 4u * kRowW) + lut_base + ((v & 7u) << 2)); };
-        auto dist_pair_lut = [&](uint32_t w) { return u32x2{lut(w & 0xffffu), lut(w >> 16)}; };
+        auto dist_pair_lut = [&](uint32_t w) {
+            const u16x2 v = as_pair(w);
+            const uint32_t ad = as_word((v >> splat(3)) * splat(256) + (v << splat(2)) + splat(int(lut_base)));
+            return u32x2{lds_word(ad & 0xffffu), lds_word(ad >> 16)};
+        };
+        // outputs wanted, as a uniform integer (scalar branches)
+        const int outs = __builtin_amdgcn_readfirstlane((want_d ? 1 : 0) | (want_s ? 2 : 0));
         // Word cw = 8 cb + lane % 8 of column block cb: plane cw / (P/2), row
         // 2 (cw % (P/2)) + (pr & 1), columns 16 rbk + (pr & ~1) + {0, 1} (+ 8
         // for the second row of the patch).  The lane's part of the byte
@@ -1149,7 +1159,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
             const uint32_t p2 = uint32_t(__builtin_amdgcn_mov_dpp(int(o2), 0x128, 0xf, 0xf, false));
             const uint32_t w1 = __builtin_amdgcn_perm(p1, o1, sel), w2 = __builtin_amdgcn_perm(p2, o2, sel);
             const uint32_t off = uint32_t((cb / CBP) * PLANE * PLANE + 16 * (cb % CBP) * PLANE + PR * rbk) * 4u;
-            if (want_d) {
+            if (outs & 1) {
                 // table lookups when every squared distance of the wave is in the table
                 const u16x2 m = __builtin_elementwise_max(best1, best2);
                 if (__all(max(uint32_t(m.x), uint32_t(m.y)) < uint32_t(kLut))) {
@@ -1160,7 +1170,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
                     __builtin_amdgcn_raw_buffer_store_b64(dist_pair(w2), rd, off_l, off + 4u * kPatchRows, 0);
                 }
             }
-            if (want_s) {
+            if (outs & 2) {
                 __builtin_amdgcn_raw_buffer_store_b64(u32x2{w1 & 0xffffu, w1 >> 16}, rs, off_l, off, 0);
                 __builtin_amdgcn_raw_buffer_store_b64(u32x2{w2 & 0xffffu, w2 >> 16}, rs, off_l, off + 4u * kPatchRows, 0);
             }
