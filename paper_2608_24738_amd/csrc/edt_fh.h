@@ -871,15 +871,18 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
                     const int q = q0 + j * kPairWaves;
                     if (q < n) {
                         const u16x2 d = as_pair(__builtin_amdgcn_perm(0u, v[j], 0x0c010c00u));
-                        // 255 -> 0xffff, else d^2 (d <= 127)
-                        const uint32_t none = as_word(splat(0) - (d >> splat(7)));
-                        const uint32_t w = as_word(d * d) | none;
-                        lo = __builtin_elementwise_min(lo, as_pair(w));
-                        row0[q * kRowW + lane] = w;
+                        // d^2; "no site" (255) becomes 65025, above every
+                        // candidate a real site gives in this plane (at most
+                        // 2 * 127^2), so it never wins a minimum in a line
+                        // that has a site.  Lines without one are not
+                        // searched and leave as "no site" (0xffff).
+                        const u16x2 w = d * d;
+                        lo = __builtin_elementwise_min(lo, w);
+                        row0[q * kRowW + lane] = as_word(w);
                     }
                 }
             }
-            seen = (lo.x != kNone16 ? 1u : 0u) | (lo.y != kNone16 ? 2u : 0u);
+            seen = (lo.x < 255u * 255u ? 1u : 0u) | (lo.y < 255u * 255u ? 2u : 0u);
         } else if (a.in_seg) {
             // whole runs: one 4-byte read per lane holds both lines (rows of
             // 64 x 64 planes are half runs: rows 2k and 2k+1 share run k, the
