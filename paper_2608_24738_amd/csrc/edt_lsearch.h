@@ -90,7 +90,19 @@ __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs
     const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
     const int j = lane % LPW, sub = lane / LPW;
     const int n = int(a.n);
-    const uint32_t L = blockIdx.x * uint32_t(LPW) + uint32_t(j);
+    // Workgroups are dealt to the 8 XCDs in turn (workgroup b to XCD b % 8),
+    // and each XCD has its own L2.  Consecutive line groups are adjacent in
+    // memory (four groups of 8 lines fill a 128-byte cache line), so each run
+    // of four consecutive groups goes to the workgroups b, b + 8, b + 16,
+    // b + 24 of one XCD, which run at about the same time and share those
+    // cache lines in its L2.  The last partial set of 32 workgroups keeps the
+    // identity order.
+    uint32_t g = blockIdx.x;
+    if (g < (gridDim.x & ~31u)) {
+        const uint32_t x = g & 7u, i = g >> 3;
+        g = (i >> 2) * 32u + x * 4u + (i & 3u);
+    }
+    const uint32_t L = g * uint32_t(LPW) + uint32_t(j);
     const bool live = L < a.lines;
     const uint32_t o = live ? a.div_inner.div(L) : 0u;
     const uint32_t i = live ? L - o * a.inner : 0u;
