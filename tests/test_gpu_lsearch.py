@@ -1,0 +1,36 @@
+"""GPU parity of the whole-line windowed search (lines longer than the paired
+16-bit tile takes), at grid sizes around the 32-workgroup sets that the
+XCD-aware line-group order permutes: below 32, one full set plus a ragged
+tail, and whole sets.  Squared distances and distances must equal the
+oracle's bit for bit; the kernel names show that the line search ran."""
+import numpy as np
+import pytest
+
+from gpu_util import announce, check_against_oracle, run_gpu
+from oracle import edt_oracle
+
+pytestmark = pytest.mark.gpu
+
+# (spatial, batch): axis 0 longer than 256 rows, batch * extent of axis 1 lines
+CASES = [((300, 24), 1),      # 3 line groups of 8
+         ((300, 264), 1),     # 33 groups: one set of 32 and a tail of 1
+         ((520, 200), 2),     # 50 groups
+         ((600, 512), 1),     # 64 groups: two whole sets
+         ((257, 100), 3)]     # 38 groups, ragged last group
+
+
+@pytest.mark.parametrize("spatial,batch", CASES, ids=["%dx%d_b%d" % (s[0], s[1], b) for s, b in CASES])
+def test_line_search_grids(spatial, batch):
+    from paper_2608_24738_amd import binding
+    rng = np.random.default_rng(spatial[0] * 1000 + spatial[1] + batch)
+    mask = (rng.random((batch,) + spatial) >= 0.003).astype(np.uint8)
+    announce("line search shape=%s" % (mask.shape,))
+    binding.prof_enable(64)
+    try:
+        res = run_gpu(mask, 2, None, dist=True, idx=False, sq=True)
+        names = [n for n, _ in binding.prof_read()]
+    finally:
+        binding.prof_enable(0)
+    assert any(n.startswith("line_search") for n in names), names
+    ora = edt_oracle.edt(mask, 2, None, nthreads=16)
+    check_against_oracle(mask, 2, None, res, ora)
