@@ -525,6 +525,15 @@ __device__ __forceinline__ u16x2 cand(u16x2 m, int d) {
     else if constexpr (METRIC == kL1) return __builtin_elementwise_add_sat(m, splat(d >= kNone16 ? kNone16 : d));
     else return __builtin_elementwise_max(m, splat(d >= kNone16 ? kNone16 : d));
 }
+// The same candidate for a distance d that differs between lanes (d < 256,
+// so d^2 fits 16 bits).
+template <int METRIC>
+__device__ __forceinline__ u16x2 cand_lane(u16x2 m, uint32_t d) {
+    const uint32_t t = METRIC == kL2 ? __umul24(d, d) : d;
+    const u16x2 tt = as_pair(t | (t << 16));
+    if constexpr (METRIC == kLinf) return __builtin_elementwise_max(m, tt);
+    else return __builtin_elementwise_add_sat(m, tt);
+}
 // true when no row at distance >= d can lower either half of `best`
 template <int METRIC>
 __device__ __forceinline__ bool stop_at(u16x2 best, int d) {
@@ -694,6 +703,9 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
     // PLANE: per wave, ballots over the 64 tile words of "line 2w (2w + 1)
     // has a site in the wave's rows": {even lo, even hi, odd lo, odd hi}
     __shared__ __attribute__((aligned(16))) uint32_t site_ballot[kPairWaves][4];
+    // FROM_MASK: per wave, bit j = its j-th staged row (row 8 j + wave) holds a
+    // site in some line of the tile
+    __shared__ uint32_t row_occ[kPairWaves];
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
@@ -745,6 +757,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         row0[(n * kRowW) + k] = 0xffffffffu;
     }
     uint32_t seen = 0;
+    uint32_t occ = 0;
     if constexpr (FROM_MASK) {
         const uint32_t n2 = a.n2;
         const int nw = int(n2 >> 5);                        // mask words per row
@@ -848,6 +861,7 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
                 }
                 seenw = __builtin_elementwise_min(seenw, as_pair(w));
                 row0[q * kRowW + lane] = w;
+                occ |= __ballot(w != 0xffffffffu) != 0 ? (1u << (q >> 3)) : 0u;
             }
         }
         seen = (seenw.x != kNone16 ? 1u : 0u) | (seenw.y != kNone16 ? 2u : 0u);
@@ -943,9 +957,29 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
                 uint4{uint32_t(be), uint32_t(be >> 32), uint32_t(bo), uint32_t(bo >> 32)};
     } else {
         any_site[lane][wv] = uint8_t(seen);
+        if (FROM_MASK && lane == 0) row_occ[wv] = occ;
     }
     // any site in the workgroup's lines (PLANE: in the plane)
     const bool plane_any = __syncthreads_or(int(seen)) != 0;
+    // FROM_MASK: rows holding a site in some line of the tile (uniform), and
+    // their count.  With few of them (a sparse background), every element
+    // takes the minimum over those rows directly instead of searching
+    // outward through the empty ones: the other rows hold "no site" in every
+    // line, so the minimum is the same.
+    // (Lines of at most 128 rows: the longer tile has no registers to spare.)
+    constexpr int kDirectRows = 8;
+    constexpr bool DIRECT = FROM_MASK && MAXRB <= 8;
+    uint32_t occw[kPairWaves] = {};
+    int n_occ = kDirectRows + 1;
+    if constexpr (DIRECT) {
+        n_occ = 0;
+#pragma unroll
+        for (int w = 0; w < kPairWaves; ++w) {
+            occw[w] = __builtin_amdgcn_readfirstlane(row_occ[w]);
+            n_occ += __builtin_popcount(occw[w]);
+        }
+    }
+    const bool direct = DIRECT && n_occ <= kDirectRows;
     // PLANE: the 8 padding words of each tile row (1088 / 576 words, never
     // read by the searches) hold the correctly rounded square roots of
     // 0..1023 (0..511 for 64-row planes) for the final stores: entry i at row
@@ -1024,6 +1058,21 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         u16x2 best1 = as_pair(row0[q1 * kRowW + cw] & searched);
         u16x2 best2 = as_pair(row0[q2 * kRowW + cw] & searched);
         int d = 1;
+        if (DIRECT && direct) {
+            // minimum over the occupied rows (row 8 j + w for bit j of occw[w])
+#pragma unroll
+            for (int w = 0; w < kPairWaves; ++w) {
+                for (uint32_t m = occw[w]; m != 0u; m &= m - 1u) {
+                    const int r = 8 * int(__builtin_ctz(m)) + w;        // uniform
+                    const u16x2 v = as_pair(row0[r * kRowW + cw]);
+                    const uint32_t d1 = uint32_t(abs(q1 - r)), d2 = uint32_t(abs(q2 - r));
+                    best1 = __builtin_elementwise_min(best1, cand_lane<METRIC>(v, d1));
+                    best2 = __builtin_elementwise_min(best2, cand_lane<METRIC>(v, d2));
+                }
+            }
+            emit(rbk, best1, best2);
+            continue;
+        }
         // Unrolled blocks whose reads stay in the tile for every row of the
         // patch: block k reads up to 4 (k + 1) rows away (uniform choice).
         // A patch that runs past the last row (its clamped rows are not 8
