@@ -17,6 +17,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -34,10 +35,16 @@ def log(msg):
 
 
 def source_digest():
+    """Digest of the kernel sources with comments and whitespace removed, so
+    that a profile stays matched to the code it measured across edits of
+    comments only."""
     h = hashlib.sha256()
     for s in SOURCES:
-        with open(os.path.join(ROOT, s), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, s), encoding="utf-8") as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

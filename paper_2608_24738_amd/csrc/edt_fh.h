@@ -473,7 +473,7 @@ namespace tmedt {
 // search unrolled, in blocks of four with literal squared distances and
 // immediate LDS offsets; the kGuard16 rows of "no site" (0xffff) above and
 // below the line keep those reads in the tile.  Other rows, and searches
-// that need more steps, continue with the row index clamped into the guard
+// that need more steps, continue with their reads clamped into the guard
 // rows (every row beyond the line is "no site" anyway), so the result is
 // exact for any input.  Few guard rows keep the tile small enough for four
 // 128-line workgroups per compute unit at n = 128.
