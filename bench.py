@@ -72,6 +72,8 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
     if base in ("fh_field_final", "tile_pair_final", "cdt_pair_final",
                 "cdt_line_final", "line_search_final", "plane_final", "line_search_signed_final"):
         return total * (fin + out_bytes)
+    if base == "small2d":                    # mask in; distances (and indices) out
+        return total * (1 + out_bytes + (4 * ndim if want_idx else 0))
     if base in ("fh_index", "tile_idx"):
         return total * (4 + 4)
     if base in ("fh_index_final", "tile_idx_final"):

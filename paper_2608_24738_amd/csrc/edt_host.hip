@@ -30,6 +30,7 @@
 #include "edt_tidx.h"
 #include "edt_scan.h"
 #include "edt_col.h"
+#include "edt_small.h"
 
 using namespace tmedt;
 
@@ -292,6 +293,19 @@ int run(Request &r) {
         return TM_ERR_ALIAS;
 
     const bool index_path = r.idx != nullptr;
+    // Small 2-D samples (both extents at most 64): one workgroup per sample
+    // runs both passes in LDS, in one launch.
+    if (nd == 2 && r.unit && r.metric == kL2 && !r.sgn && r.shape[0] <= uint32_t(kSmallMax) &&
+        r.shape[1] <= uint32_t(kSmallMax) && r.batch < (uint64_t(1) << 31)) {
+        SmallArgs sa{};
+        sa.mask = r.in;
+        sa.dist = r.dist;
+        sa.sq = r.sq;
+        sa.idx = r.idx;
+        sa.n0 = r.shape[0];
+        sa.n1 = r.shape[1];
+        return launch("small2d", k_small2d, dim3(uint32_t(r.batch)), dim3(kWave * kSmallWaves), 0, r.stream, sa);
+    }
     if (!index_path && r.unit && r.metric == kL2 && !r.sgn) {
         const int rc = run_plane(r, total, vox);
         if (rc != kNotPlane) return rc;

@@ -188,7 +188,7 @@ def test_sqrt_is_correctly_rounded():
 # The paired tile takes passes of at least 32768 lines (fewer go to the
 # whole-line search), so batches are sized to reach that on every pass.
 FUSED = [
-    ((513, 50, 64), 2, 0.05),      # final pass reads the mask; 256.5 workgroups
+    ((513, 65, 64), 2, 0.05),      # final pass reads the mask; 256.5 workgroups (65 rows: past the one-launch small path)
     ((171, 33, 192), 2, 0.01),     # workgroups straddle planes; zeros several words apart
     ((29, 9, 21, 128), 3, 0.2),
     ((103, 5, 160, 64), 3, 0.002), # long lines, mostly empty rows
