@@ -412,22 +412,54 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
             out[p] = none ? -1 : y;   // kScanFinal: the line is the sample
         }
     }
-    if (!live) return;
-
     // ---- stores -------------------------------------------------------------
-    if (MODE == kScanFieldInt || MODE == kScanFieldL1 || MODE == kScanFieldFlt) {
-        int4 *dst = reinterpret_cast<int4 *>(MODE != kScanFieldFlt ? a.field_i
-                                                                  : reinterpret_cast<int32_t *>(a.field_f)) +
-                    pos0 / 4;
+    if (MODE != kScanFinal) {
+        // A lane's 64 results are 256 contiguous bytes.  Written straight from
+        // registers, each store instruction of the wave would touch 64
+        // separate 16-byte pieces; instead they pass through LDS in two
+        // halves, so that each store instruction writes 8 whole 128-byte
+        // segments (half a lane's results each).  The destinations of the
+        // lanes' results go through LDS as well: index slices of different
+        // samples are not adjacent.
+        constexpr int kPad = 9;                                   // int4 per lane row: 8 + 1 pad
+        __shared__ int4 stage[256 / kWave][kWave * kPad];
+        __shared__ uint64_t dest[256 / kWave][kWave];
+        int4 *st = stage[threadIdx.x / kWave];
+        uint64_t *ds = dest[threadIdx.x / kWave];
+        int32_t *db;
+        uint64_t own;
+        if (MODE == kScanIndex) {
+            const uint64_t s = line / a.lps;
+            db = a.idx;
+            own = s * uint64_t(a.ndim) * a.vox + (line - s * a.lps) * a.n + uint64_t(w) * 64;
+        } else {
+            db = MODE == kScanFieldFlt ? reinterpret_cast<int32_t *>(a.field_f) : a.field_i;
+            own = pos0;
+        }
+        ds[lane] = live ? own : ~0ull;
+        const int src = lane >> 3, piece = lane & 7;
 #pragma unroll
-        for (int k = 0; k < 16; ++k) dst[k] = make_int4(out[4 * k], out[4 * k + 1], out[4 * k + 2], out[4 * k + 3]);
-    } else if (MODE == kScanIndex) {
-        const uint64_t s = line / a.lps;
-        const uint64_t off = s * uint64_t(a.ndim) * a.vox + (line - s * a.lps) * a.n + uint64_t(w) * 64;
-        int4 *dst = reinterpret_cast<int4 *>(a.idx + off);
+        for (int h = 0; h < 2; ++h) {
 #pragma unroll
-        for (int k = 0; k < 16; ++k) dst[k] = make_int4(out[4 * k], out[4 * k + 1], out[4 * k + 2], out[4 * k + 3]);
+            for (int i = 0; i < 8; ++i)
+                st[lane * kPad + i] = make_int4(out[32 * h + 4 * i], out[32 * h + 4 * i + 1],
+                                                out[32 * h + 4 * i + 2], out[32 * h + 4 * i + 3]);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int sl = 8 * k + src;                       // source lane
+                const uint64_t o = ds[sl];
+                const int4 v = st[sl * kPad + piece];
+                if (o != ~0ull) *reinterpret_cast<int4 *>(db + o + 32 * h + 4 * piece) = v;
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        }
     } else {
+        if (!live) return;
         // rank 1: a line without any zero measures from the virtual zero at -1
 #pragma unroll
         for (int p = 0; p < 64; ++p) {
