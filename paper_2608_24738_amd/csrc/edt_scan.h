@@ -334,6 +334,10 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
     const uint64_t line = wave * a.lpw + lw;
     const bool live = lw < int(a.lpw) && line < a.lines;
     if (wave * a.lpw >= a.lines) return;      // whole wavefront exits together
+    // kScanIndex: sample of the line and the line's first in-sample position
+    // (the 64-bit division runs here, while few registers are live)
+    const uint64_t smp = MODE == kScanIndex ? line / a.lps : 0;
+    const uint32_t local = MODE == kScanIndex ? uint32_t(line - smp * a.lps) * a.n : 0;
 
     // ---- zero mask of this lane's 64 positions ---------------------------
     const uint64_t pos0 = line * a.n + uint64_t(w) * 64;   // batch-flat first position
@@ -405,8 +409,6 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
             out[p] = none ? __builtin_bit_cast(int32_t, __builtin_inff())
                           : __builtin_bit_cast(int32_t, float(a.w * (df * df)));
         } else if (MODE == kScanIndex) {
-            const uint64_t s = line / a.lps;
-            const uint32_t local = uint32_t(line - s * a.lps) * a.n;
             out[p] = none ? kNoIdx : int32_t(local + y);
         } else {
             out[p] = none ? -1 : y;   // kScanFinal: the line is the sample
@@ -429,9 +431,8 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
         int32_t *db;
         uint64_t own;
         if (MODE == kScanIndex) {
-            const uint64_t s = line / a.lps;
             db = a.idx;
-            own = s * uint64_t(a.ndim) * a.vox + (line - s * a.lps) * a.n + uint64_t(w) * 64;
+            own = smp * uint64_t(a.ndim) * a.vox + local + uint64_t(w) * 64;
         } else {
             db = MODE == kScanFieldFlt ? reinterpret_cast<int32_t *>(a.field_f) : a.field_i;
             own = pos0;
@@ -439,7 +440,7 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
         ds[lane] = live ? own : ~0ull;
         const int src = lane >> 3, piece = lane & 7;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
+        for (int h = 1; h >= 0; --h) {                          // the later half is ready first
 #pragma unroll
             for (int i = 0; i < 8; ++i)
                 st[lane * kPad + i] = make_int4(out[32 * h + 4 * i], out[32 * h + 4 * i + 1],
