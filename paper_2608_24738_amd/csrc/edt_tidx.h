@@ -297,7 +297,12 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
             slice0[e] = -1;
             for (int b = 1; b < nd; ++b) slice0[uint64_t(b) * a.vox + e] = 0;
         }
-        const float dist = (!SAMP && d2 < 16777216.0) ? sqrt_rn_int(uint32_t(d2)) : float(sqrt(d2));
+        // A found site's sampled value is a float, and its correctly rounded
+        // float root (sqrtf) equals the double root rounded to float, since
+        // 53 >= 2 * 24 + 2; the virtual element's value takes the double root.
+        const float dist = (SAMP && site >= 0)                ? sqrtf(fbest)
+                           : (!SAMP && d2 < 16777216.0) ? sqrt_rn_int(uint32_t(d2))
+                                                        : float(sqrt(d2));
         if (a.dist) a.dist[uint64_t(l.s) * a.vox + e] = dist;
         if (a.sq) a.sq[uint64_t(l.s) * a.vox + e] = int32_t(d2);
     }
