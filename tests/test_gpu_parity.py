@@ -240,3 +240,33 @@ def test_half_width_intermediates(shape, ndim, p_bg):
     mask[0] = 1                                   # a sample with no background
     mask[-1] = 0                                  # and one that is all background
     parity(mask, ndim, None, dist=True, idx=False, tag="half-width extremes")
+
+
+# Last-axis word scan: a wavefront holds 64 / (n / 64) whole lines and its
+# stores pass through LDS.  Line lengths 192 and 320 leave idle lanes at the
+# end of each wavefront; samples of 3 or 5 lines put several samples in one
+# wavefront, so the index slices of its lines are not adjacent in memory.
+WORD = [
+    ((7, 3, 192), 2, None, True),
+    ((11, 5, 320), 2, (1.5, 0.7), True),
+    ((4, 5, 3, 192), 3, None, True),
+    ((9, 3, 192), 2, None, False),
+    ((6, 5, 320), 2, (0.9, 2.0), False),
+    ((2, 6, 5, 4096), 2, None, True),
+]
+
+
+@pytest.mark.parametrize("shape,ndim,samp,idx", WORD,
+                         ids=["x".join(map(str, s)) + ("-s" if m else "") + ("-i" if i else "")
+                              for s, _, m, i in WORD])
+def test_word_scan_lanes_and_samples(shape, ndim, samp, idx):
+    from paper_2608_24738_amd import binding
+    for p_bg, seed in ((0.02, 1), (0.3, 2)):
+        mask = rand_mask(shape, p_bg, 100 + seed + len(shape))
+        binding.prof_enable(64)
+        try:
+            parity(mask, ndim, samp, dist=True, idx=idx, tag="word scan p=%g" % p_bg)
+            names = {n for n, _ in binding.prof_read()}
+        finally:
+            binding.prof_enable(0)
+        assert "scan_word" in names, names
