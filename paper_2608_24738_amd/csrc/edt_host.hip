@@ -220,6 +220,11 @@ bool plan_line_search(FhPlan &p, uint32_t n, uint64_t total, bool w16) {
 // launch, when the input does not qualify.
 constexpr int kNotPlane = 1;
 
+// Wavefronts below which the last-axis word scan takes 32-position words
+// (one per SIMD).  Measured: 8 x 256^2 6.8 against 8.2 us; at 2048 wavefronts
+// (32 x 512^2, 8 x 1024^2) 64-position words stay faster (16.7 against 18.0 us).
+constexpr uint64_t kWord32Waves = 1024;
+
 int run_plane(Request &r, uint64_t total, uint64_t vox) {
     const int nd = r.ndim;
     const uint32_t P = r.shape[nd - 1];
@@ -502,9 +507,14 @@ int run(Request &r) {
             WordScanArgs ws{};
             ws.in = r.in;
             ws.n = nlast;
-            ws.nw = nlast / kWave;
-            ws.lpw = kWave / ws.nw;
+            // 32-position words when 64-position words would leave fewer than
+            // kWord32Waves wavefronts: twice the wavefronts, and so twice the
+            // loads and stores, in flight.
             ws.lines = total / nlast;
+            const uint64_t lpw64 = kWave / (nlast / kWave);
+            const bool w32 = nlast <= uint32_t(32 * kWave) && (ws.lines + lpw64 - 1) / lpw64 < kWord32Waves;
+            ws.nw = nlast / (w32 ? 32 : 64);
+            ws.lpw = kWave / ws.nw;
             ws.lps = uint32_t(vox / nlast);
             ws.vox = uint32_t(vox);
             ws.ndim = nd;
@@ -516,13 +526,17 @@ int run(Request &r) {
             ws.sq = s.sq;
             const uint64_t waves = (ws.lines + ws.lpw - 1) / ws.lpw;
             const dim3 grid(uint32_t((waves + 3) / 4)), block(256);
+#define TM_WORD(M)                                                                            \
+    (w32 ? launch("scan_word", k_scan_word<M, 32>, grid, block, 0, r.stream, ws)                  \
+         : launch("scan_word", k_scan_word<M, 64>, grid, block, 0, r.stream, ws))
             switch (mode) {
-                case kScanFieldInt: rc = launch("scan_word", k_scan_word<kScanFieldInt>, grid, block, 0, r.stream, ws); break;
-                case kScanFieldL1: rc = launch("scan_word", k_scan_word<kScanFieldL1>, grid, block, 0, r.stream, ws); break;
-                case kScanFieldFlt: rc = launch("scan_word", k_scan_word<kScanFieldFlt>, grid, block, 0, r.stream, ws); break;
-                case kScanIndex: rc = launch("scan_word", k_scan_word<kScanIndex>, grid, block, 0, r.stream, ws); break;
-                default: rc = launch("scan_word", k_scan_word<kScanFinal>, grid, block, 0, r.stream, ws); break;
+                case kScanFieldInt: rc = TM_WORD(kScanFieldInt); break;
+                case kScanFieldL1: rc = TM_WORD(kScanFieldL1); break;
+                case kScanFieldFlt: rc = TM_WORD(kScanFieldFlt); break;
+                case kScanIndex: rc = TM_WORD(kScanIndex); break;
+                default: rc = TM_WORD(kScanFinal); break;
             }
+#undef TM_WORD
         } else if (nlast <= uint32_t(kSpan)) {
             s.span_lines = uint32_t(kSpan) / nlast;
             const uint64_t waves = (uint64_t(s.lines) + s.span_lines - 1) / s.span_lines;

@@ -299,18 +299,19 @@ __global__ void __launch_bounds__(64) k_scan_long(ScanArgs a) {
 namespace tmedt {
 
 // ---------------------------------------------------------------------------
-// Lines whose length is a multiple of 64: one lane per 64-position word.
-// A wavefront holds 64 / words-per-line whole lines (lanes past them idle).
-// Each lane loads its 64 mask bytes (four 16-byte loads), builds the 64-bit
-// zero mask, takes the last zero of the earlier words and the first zero of
-// the later words of its line from two segmented wave scans, then walks its
-// 64 positions left to right (distance to the last zero) and right to left
-// (distance to the next zero), keeping the left zero on ties.
+// Lines whose length is a multiple of WB (64, or 32 to run twice as many
+// wavefronts on short batches): one lane per WB-position word.  A wavefront
+// holds 64 / words-per-line whole lines (lanes past them idle).  Each lane
+// loads its WB mask bytes (16-byte loads), builds the zero mask, takes the
+// last zero of the earlier words and the first zero of the later words of
+// its line from two segmented wave scans, then walks its WB positions left
+// to right (distance to the last zero) and right to left (distance to the
+// next zero), keeping the left zero on ties.
 // ---------------------------------------------------------------------------
 struct WordScanArgs {
     const uint8_t *in;
-    uint32_t n;            // line length, a multiple of 64
-    uint32_t nw;           // words per line = n / 64 (<= 64)
+    uint32_t n;            // line length, a multiple of the word size WB
+    uint32_t nw;           // words per line = n / WB (<= 64)
     uint32_t lpw;          // whole lines per wavefront = 64 / nw
     uint64_t lines;        // lines in the batch
     uint32_t lps;          // lines per sample
@@ -324,8 +325,9 @@ struct WordScanArgs {
     int32_t *sq;
 };
 
-template <int MODE>
+template <int MODE, int WB>
 __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
+    static_assert(WB == 32 || WB == 64, "a word holds 32 or 64 positions");
     const int lane = threadIdx.x & (kWave - 1);
     const uint64_t wave = uint64_t(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
     const int nw = int(a.nw);
@@ -339,16 +341,16 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
     const uint64_t smp = MODE == kScanIndex ? line / a.lps : 0;
     const uint32_t local = MODE == kScanIndex ? uint32_t(line - smp * a.lps) * a.n : 0;
 
-    // ---- zero mask of this lane's 64 positions ---------------------------
-    const uint64_t pos0 = line * a.n + uint64_t(w) * 64;   // batch-flat first position
+    // ---- zero mask of this lane's WB positions ---------------------------
+    const uint64_t pos0 = line * a.n + uint64_t(w) * WB;   // batch-flat first position
     uint64_t mask = 0;
     if (live) {
         const uint4 *src = reinterpret_cast<const uint4 *>(a.in + pos0);
-        uint4 v[4];
+        uint4 v[WB / 16];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) v[k] = src[k];
+        for (int k = 0; k < WB / 16; ++k) v[k] = src[k];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
+        for (int k = 0; k < WB / 16; ++k) {
             const uint32_t d4[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
@@ -365,7 +367,7 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
     // ---- nearest zero in the other words of the line ---------------------
     // Keys carry the line within the wavefront in their high bits so that a
     // plain wave-wide max / min never mixes two lines.
-    const int base = w * 64;
+    const int base = w * WB;
     const uint32_t hi = uint32_t(lw) << 16;
     const uint32_t own_last = mask ? hi | uint32_t(base + 63 - __clzll(mask) + 1) : hi;
     const uint32_t own_first = mask ? hi | uint32_t(base + __ffsll((unsigned long long)mask) - 1) : hi | 0xffffu;
@@ -386,15 +388,15 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
     int next = (after & 0xffffu) != 0xffffu ? int(after & 0xffffu) : kFar;
 
     // ---- per-position distances -------------------------------------------
-    int dl[64];
+    int dl[WB];
 #pragma unroll
-    for (int p = 0; p < 64; ++p) {
+    for (int p = 0; p < WB; ++p) {
         if ((mask >> p) & 1ull) last = base + p;
         dl[p] = last;             // last zero at or before base + p
     }
-    int32_t out[64];
+    int32_t out[WB];
 #pragma unroll
-    for (int p = 63; p >= 0; --p) {
+    for (int p = WB - 1; p >= 0; --p) {
         if ((mask >> p) & 1ull) next = base + p;
         const int x = base + p;
         const int l = x - dl[p], r = next - x;   // l, r >= 0
@@ -416,11 +418,11 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
     }
     // ---- stores -------------------------------------------------------------
     if (MODE != kScanFinal) {
-        // A lane's 64 results are 256 contiguous bytes.  Written straight from
-        // registers, each store instruction of the wave would touch 64
-        // separate 16-byte pieces; instead they pass through LDS in two
-        // halves, so that each store instruction writes 8 whole 128-byte
-        // segments (half a lane's results each).  The destinations of the
+        // A lane's WB results are 4 WB contiguous bytes.  Written straight
+        // from registers, each store instruction of the wave would touch 64
+        // separate 16-byte pieces; instead they pass through LDS in halves
+        // of 32 results, so that each store instruction writes 8 whole
+        // 128-byte segments (a half of each of 8 lanes).  The destinations of the
         // lanes' results go through LDS as well: index slices of different
         // samples are not adjacent.
         constexpr int kPad = 9;                                   // int4 per lane row: 8 + 1 pad
@@ -432,7 +434,7 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
         uint64_t own;
         if (MODE == kScanIndex) {
             db = a.idx;
-            own = smp * uint64_t(a.ndim) * a.vox + local + uint64_t(w) * 64;
+            own = smp * uint64_t(a.ndim) * a.vox + local + uint64_t(w) * WB;
         } else {
             db = MODE == kScanFieldFlt ? reinterpret_cast<int32_t *>(a.field_f) : a.field_i;
             own = pos0;
@@ -440,7 +442,7 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
         ds[lane] = live ? own : ~0ull;
         const int src = lane >> 3, piece = lane & 7;
 #pragma unroll
-        for (int h = 1; h >= 0; --h) {                          // the later half is ready first
+        for (int h = WB / 32 - 1; h >= 0; --h) {                // the later half is ready first
 #pragma unroll
             for (int i = 0; i < 8; ++i)
                 st[lane * kPad + i] = make_int4(out[32 * h + 4 * i], out[32 * h + 4 * i + 1],
@@ -463,7 +465,7 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
         if (!live) return;
         // rank 1: a line without any zero measures from the virtual zero at -1
 #pragma unroll
-        for (int p = 0; p < 64; ++p) {
+        for (int p = 0; p < WB; ++p) {
             const int x = base + p;
             const int y = out[p];
             const int64_t dd = y >= 0 ? int64_t(x - y) : int64_t(x + 1);
