@@ -307,7 +307,7 @@ def main():
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only; --gpus %d is not supported (the EDT shards "
-              "by batch with no exchange, see DESIGN.md)" % args.gpus, file=sys.stderr)
+              "by batch with no exchange between GPUs)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
