@@ -60,7 +60,8 @@ typedef enum {
     TM_ERR_ALIAS = -8,       /* two of the buffers overlap */
     TM_ERR_UNSUPPORTED = -9, /* a line is longer than the envelope kernels hold in LDS */
     TM_ERR_HIP = -10,        /* the HIP runtime reported an error while enqueuing */
-    TM_ERR_METRIC = -11      /* metric is not one of tm_metric */
+    TM_ERR_METRIC = -11,     /* metric is not one of tm_metric */
+    TM_ERR_DTYPE = -12       /* dtype is not one of tm_dtype */
 } tm_status;
 
 /*
@@ -177,6 +178,45 @@ int tm_edt_signed(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t 
  */
 int tm_cdt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, int metric,
            int32_t *out_dist, hipStream_t stream);
+
+/* Element types the foreground predicate reads. */
+typedef enum {
+    TM_DTYPE_U8 = 0,     /* 1-byte integers: uint8, int8, bool */
+    TM_DTYPE_I16 = 1,    /* 2-byte integers */
+    TM_DTYPE_I32 = 2,    /* 4-byte integers */
+    TM_DTYPE_I64 = 3,    /* 8-byte integers */
+    TM_DTYPE_F16 = 4,    /* IEEE binary16 */
+    TM_DTYPE_BF16 = 5,   /* bfloat16 */
+    TM_DTYPE_F32 = 6,    /* IEEE binary32 */
+    TM_DTYPE_F64 = 7,    /* IEEE binary64 */
+    TM_DTYPE_F8 = 8      /* 1-byte floats (E4M3, E5M2): the top bit is the sign */
+} tm_dtype;
+
+/*
+ * tm_mask_nonzero -- the byte mask the transforms read, from an input of any
+ * element type and any layout (paper, Section 2.2.1: the operators accept
+ * what their SciPy counterparts accept, and SciPy counts every nonzero
+ * element as foreground, NaN included).
+ *
+ *   in        DEVICE pointer to the first element of a strided view.
+ *   dtype     one of tm_dtype.  Integers are foreground when nonzero;
+ *             floating-point values when any bit other than the sign is set,
+ *             so +0 and -0 are background and NaN, infinities and subnormals
+ *             are foreground.  The test is on bit patterns (no arithmetic).
+ *   ndim      dimensions of the view, 1 to 16; shape: HOST pointer to the
+ *             extents (each >= 1), outermost first.
+ *   strides   HOST pointer to ndim strides in BYTES (each >= 0), or NULL for
+ *             a C-contiguous view.
+ *   out_u8    DEVICE pointer to prod(shape) bytes, written C-contiguous with
+ *             1 for foreground and 0 for background; owned by the caller and
+ *             not overlapping the input's footprint.
+ * Enqueued on `stream` like the transforms; allocates nothing.  Errors:
+ * TM_ERR_NDIM, TM_ERR_SHAPE (NULL shape, an extent < 1 or a negative
+ * stride), TM_ERR_NULL (in), TM_ERR_NO_OUTPUT (out_u8), TM_ERR_DTYPE,
+ * TM_ERR_TOO_LARGE (2^32 elements or more), TM_ERR_ALIAS, TM_ERR_HIP.
+ */
+int tm_mask_nonzero(const void *in, int dtype, int ndim, const int64_t *shape,
+                    const int64_t *strides, uint8_t *out_u8, hipStream_t stream);
 
 /*
  * tm_selftest_host -- checks the host-side planning arithmetic (the

@@ -6,7 +6,7 @@ and turns status codes into exceptions.  There is no fallback: if the library
 is missing, every call raises.
 
 Entry points with the C names (``tm_edt``, ``tm_edt_sq``, ``tm_edt_signed``,
-``tm_dt_bf``, ``tm_cdt``, ``tm_strerror``) plus ``scipy.ndimage``-style
+``tm_dt_bf``, ``tm_cdt``, ``tm_mask_nonzero``, ``tm_strerror``) plus ``scipy.ndimage``-style
 wrappers (``distance_transform_edt``, ``distance_transform_bf``,
 ``distance_transform_cdt``, ``signed_distance_transform``) over
 (B, C, *spatial) tensors (paper, Section 2.2.1).
@@ -65,6 +65,8 @@ def load() -> ctypes.CDLL:
                                          ctypes.POINTER(ctypes.c_float)]
             lib.tm_selftest_host.restype = i32
             lib.tm_selftest_host.argtypes = []
+            lib.tm_mask_nonzero.restype = i32
+            lib.tm_mask_nonzero.argtypes = [vp, i32, i32, vp, vp, vp, vp]
             _lib = lib
     return _lib
 
@@ -93,7 +95,8 @@ def _check_mask(in_u8: torch.Tensor):
     if not in_u8.is_cuda:
         raise ValueError("input must be a ROCm (cuda) tensor")
     if in_u8.dtype not in (torch.uint8, torch.bool):
-        raise TypeError("input must be uint8 or bool (nonzero = foreground); got %s" % in_u8.dtype)
+        raise TypeError("the C entry points read a uint8 or bool mask (nonzero = foreground); got %s; "
+                        "the scipy-style wrappers accept any dtype" % in_u8.dtype)
     if not in_u8.is_contiguous():
         raise ValueError("tm_edt needs a contiguous input")
 
@@ -209,22 +212,83 @@ def _normalise_sampling(sampling, ndim):
     return s
 
 
+# tm_dtype codes of the foreground predicate, by torch element type
+_DTYPES = {
+    torch.uint8: 0, torch.int8: 0, torch.bool: 0,
+    torch.int16: 1, torch.int32: 2, torch.int64: 3,
+    torch.float16: 4, torch.bfloat16: 5, torch.float32: 6, torch.float64: 7,
+}
+for _name in ("uint16", "uint32", "uint64"):
+    if hasattr(torch, _name):
+        _DTYPES[getattr(torch, _name)] = {"uint16": 1, "uint32": 2, "uint64": 3}[_name]
+# 1-byte floats with a negative zero ignore the sign bit; the "fnuz" formats
+# have no negative zero (0x80 is their NaN), so every nonzero byte counts
+for _name, _code in (("float8_e4m3fn", 8), ("float8_e5m2", 8), ("float8_e4m3fnuz", 0),
+                     ("float8_e5m2fnuz", 0)):
+    if hasattr(torch, _name):
+        _DTYPES[getattr(torch, _name)] = _code
+
+
+def tm_mask_nonzero(x: torch.Tensor, out_u8: torch.Tensor, stream=None) -> None:
+    """Calls tm_mask_nonzero: ``out_u8`` (contiguous, x.numel() bytes) gets 1
+    where ``x`` is nonzero (NaN included, -0.0 excluded), read through x's strides."""
+    if not x.is_cuda:
+        raise ValueError("input must be a ROCm (cuda) tensor")
+    if x.dtype not in _DTYPES:
+        raise TypeError("input dtype %s has no nonzero test here" % x.dtype)
+    _check_out(out_u8, torch.uint8, x.numel(), "out_u8", x.device)
+    nd = max(x.dim(), 1)
+    shape = (ctypes.c_int64 * nd)(*(x.shape if x.dim() else (1,)))
+    strides = (ctypes.c_int64 * nd)(*[st * x.element_size() for st in (x.stride() if x.dim() else (1,))])
+    with torch.cuda.device(x.device):
+        st = _stream_handle(stream)
+        rc = load().tm_mask_nonzero(_ptr(x), _DTYPES[x.dtype], nd, shape, strides, _ptr(out_u8),
+                                    ctypes.c_void_p(st))
+    if rc != TM_OK:
+        raise TMError(rc, "tm_mask_nonzero")
+
+
 def _as_mask(input: torch.Tensor) -> torch.Tensor:
-    if input.dtype == torch.bool:
-        input = input.view(torch.uint8)
-    elif input.dtype != torch.uint8:
-        raise TypeError("input must be uint8 or bool (nonzero = foreground); convert other "
-                        "dtypes with (x != 0) first; got %s" % input.dtype)
-    return input.contiguous()
+    """The contiguous byte mask of ``input``: uint8 / bool contiguous tensors are
+    used as they are; any other dtype or layout goes through tm_mask_nonzero."""
+    if input.dtype not in _DTYPES:
+        raise TypeError("input dtype %s has no nonzero test here" % input.dtype)
+    if not input.is_cuda:
+        raise ValueError("input must be a ROCm (cuda) tensor")
+    if input.dtype in (torch.uint8, torch.bool) and input.is_contiguous():
+        return input.view(torch.uint8)
+    mask = torch.empty(input.shape, dtype=torch.uint8, device=input.device)
+    tm_mask_nonzero(input, mask)
+    return mask
+
+
+def _out_buffer(given, shape, dtype, dev, what):
+    """(buffer the library writes, tensor to copy it into afterwards or None).
+    A pre-allocated output of the right shape and dtype is written directly
+    when it is contiguous, else through a contiguous buffer (scipy fills
+    any layout)."""
+    if given is None:
+        return torch.empty(shape, dtype=dtype, device=dev), None
+    if tuple(given.shape) != tuple(shape) or given.dtype != dtype:
+        raise RuntimeError("%s array has wrong shape or type" % what)
+    if given.device != dev:
+        raise RuntimeError("%s array is on %s, the input on %s" % (what, given.device, dev))
+    if given.is_contiguous():
+        return given, None
+    return torch.empty(shape, dtype=dtype, device=dev), given
 
 
 def distance_transform_edt(input: torch.Tensor, sampling=None, return_distances: bool = True,
                            return_indices: bool = False, distances=None, indices=None):
     """``scipy.ndimage.distance_transform_edt`` over a (B, C, *spatial) batch.
 
+    ``input`` may have any element type and any strides: nonzero elements
+    (NaN included) are foreground, as in scipy; anything but a contiguous
+    uint8 / bool tensor is turned into the byte mask by tm_mask_nonzero.
     Returns float32 distances (B, C, *S) and/or int32 indices (B, C, len(S), *S),
     like scipy (a tuple when both are requested).  Pre-allocated ``distances`` /
-    ``indices`` are filled in place and not returned.  Distances are float32.
+    ``indices`` (any strides) are filled in place and not returned.  Distances
+    are float32.
     """
     if input.dim() < 3:
         raise ValueError("input must be (B, C, *spatial) with 1 to 8 spatial dimensions")
@@ -238,24 +302,16 @@ def distance_transform_edt(input: torch.Tensor, sampling=None, return_distances:
     lead = tuple(mask.shape[:2])
     spatial = tuple(mask.shape[2:])
     dev = mask.device
-    dist_out = None
+    dist_out = dist_back = idx_out = idx_back = None
     if return_distances:
-        if distances is not None:
-            if distances.shape != mask.shape or distances.dtype != torch.float32:
-                raise RuntimeError("distances array has wrong shape or type")
-            dist_out = distances
-        else:
-            dist_out = torch.empty(mask.shape, dtype=torch.float32, device=dev)
-    idx_out = None
+        dist_out, dist_back = _out_buffer(distances, mask.shape, torch.float32, dev, "distances")
     if return_indices:
-        want = lead + (ndim,) + spatial
-        if indices is not None:
-            if tuple(indices.shape) != want or indices.dtype != torch.int32:
-                raise RuntimeError("indices array has wrong shape or type")
-            idx_out = indices
-        else:
-            idx_out = torch.empty(want, dtype=torch.int32, device=dev)
+        idx_out, idx_back = _out_buffer(indices, lead + (ndim,) + spatial, torch.int32, dev, "indices")
     tm_edt(mask, ndim, samp, dist_out, idx_out)
+    if dist_back is not None:
+        dist_back.copy_(dist_out)
+    if idx_back is not None:
+        idx_back.copy_(idx_out)
     result = []
     if return_distances and distances is None:
         result.append(dist_out)
@@ -304,13 +360,10 @@ def distance_transform_cdt(input: torch.Tensor, metric: str = "chessboard", dist
     if metric not in ("chessboard", "taxicab"):
         raise ValueError("metric must be 'chessboard' or 'taxicab'")
     mask = _as_mask(input)
-    if distances is not None:
-        if distances.shape != mask.shape or distances.dtype != torch.int32:
-            raise RuntimeError("distances array has wrong shape or type")
-        out = distances
-    else:
-        out = torch.empty(mask.shape, dtype=torch.int32, device=mask.device)
+    out, back = _out_buffer(distances, mask.shape, torch.int32, mask.device, "distances")
     tm_cdt(mask, ndim, METRICS[metric], out)
+    if back is not None:
+        back.copy_(out)
     return None if distances is not None else out
 
 
@@ -323,13 +376,10 @@ def signed_distance_transform(input: torch.Tensor, distances=None):
         raise ValueError("input must be (B, C, *spatial) with 1 to 8 spatial dimensions")
     ndim = input.dim() - 2
     mask = _as_mask(input)
-    if distances is not None:
-        if distances.shape != mask.shape or distances.dtype != torch.float32:
-            raise RuntimeError("distances array has wrong shape or type")
-        out = distances
-    else:
-        out = torch.empty(mask.shape, dtype=torch.float32, device=mask.device)
+    out, back = _out_buffer(distances, mask.shape, torch.float32, mask.device, "distances")
     tm_edt_signed(mask, ndim, out)
+    if back is not None:
+        back.copy_(out)
     return None if distances is not None else out
 
 

@@ -31,6 +31,7 @@
 #include "edt_scan.h"
 #include "edt_col.h"
 #include "edt_small.h"
+#include "edt_mask.h"
 
 using namespace tmedt;
 
@@ -856,6 +857,59 @@ extern "C" int tm_cdt(const uint8_t *in_u8, int ndim, const int64_t *shape, int6
     return run(r);
 }
 
+extern "C" int tm_mask_nonzero(const void *in, int dtype, int ndim, const int64_t *shape,
+                               const int64_t *strides, uint8_t *out_u8, hipStream_t stream) {
+    if (ndim < 1 || ndim > kMaskMaxDim) return TM_ERR_NDIM;
+    if (!shape) return TM_ERR_SHAPE;
+    if (!in) return TM_ERR_NULL;
+    if (!out_u8) return TM_ERR_NO_OUTPUT;
+    if (dtype < TM_DTYPE_U8 || dtype > TM_DTYPE_F8) return TM_ERR_DTYPE;
+    static const int esize[] = {1, 2, 4, 8, 2, 2, 4, 8, 1};
+    const int E = esize[dtype];
+    const bool flt = dtype >= TM_DTYPE_F16;
+    uint64_t n = 1, span = uint64_t(E);   // elements, and bytes from `in` to the end of the last one
+    bool contig = true;
+    uint64_t want = uint64_t(E);          // C-order stride of the current axis
+    for (int b = ndim - 1; b >= 0; --b) {
+        if (shape[b] < 1) return TM_ERR_SHAPE;
+        const int64_t st = strides ? strides[b] : int64_t(want);
+        if (st < 0) return TM_ERR_SHAPE;
+        if (uint64_t(shape[b]) >= (uint64_t(1) << 32)) return TM_ERR_TOO_LARGE;
+        n *= uint64_t(shape[b]);
+        if (n >= (uint64_t(1) << 32)) return TM_ERR_TOO_LARGE;
+        if (shape[b] > 1 && uint64_t(st) != want) contig = false;
+        span += uint64_t(shape[b] - 1) * uint64_t(st);
+        if (span >= (uint64_t(1) << 62)) return TM_ERR_TOO_LARGE;
+        want *= uint64_t(shape[b]);
+    }
+    if (overlaps(in, span, out_u8, n)) return TM_ERR_ALIAS;
+    MaskArgs m{};
+    m.in = static_cast<const uint8_t *>(in);
+    m.out = out_u8;
+    m.n = uint32_t(n);
+    m.ndim = ndim;
+    for (int b = 0; b < ndim; ++b) {
+        m.div_shape[b] = Div32::make(uint32_t(shape[b]));
+        m.stride[b] = strides ? strides[b] : 0;
+    }
+    const uint64_t per = uint64_t(kMaskThreads) * kMaskPer;
+    const dim3 grid(uint32_t((n + per - 1) / per)), block(kMaskThreads);
+#define TM_MASK(EB, F)                                                                                  \
+    (contig ? launch("mask_nonzero", k_mask_nonzero<EB, F, true>, grid, block, 0, stream, m)            \
+            : launch("mask_nonzero", k_mask_nonzero<EB, F, false>, grid, block, 0, stream, m))
+    switch (E * 2 + (flt ? 1 : 0)) {
+        case 2: return TM_MASK(1, false);
+        case 3: return TM_MASK(1, true);
+        case 4: return TM_MASK(2, false);
+        case 5: return TM_MASK(2, true);
+        case 8: return TM_MASK(4, false);
+        case 9: return TM_MASK(4, true);
+        case 16: return TM_MASK(8, false);
+        default: return TM_MASK(8, true);
+    }
+#undef TM_MASK
+}
+
 extern "C" const char *tm_strerror(int status) {
     switch (status) {
         case TM_OK: return "success";
@@ -870,6 +924,7 @@ extern "C" const char *tm_strerror(int status) {
         case TM_ERR_UNSUPPORTED: return "a line is longer than the envelope stack held in LDS";
         case TM_ERR_HIP: return "HIP runtime error while enqueuing kernels";
         case TM_ERR_METRIC: return "metric must be euclidean, taxicab or chessboard";
+        case TM_ERR_DTYPE: return "element type is not one of tm_dtype";
         default: return "unknown status";
     }
 }

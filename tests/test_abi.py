@@ -14,7 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 TM_OK, TM_ERR_NDIM, TM_ERR_SHAPE, TM_ERR_BATCH, TM_ERR_NULL = 0, -1, -2, -3, -4
 TM_ERR_NO_OUTPUT, TM_ERR_SAMPLING, TM_ERR_TOO_LARGE, TM_ERR_ALIAS = -5, -6, -7, -8
-TM_ERR_UNSUPPORTED, TM_ERR_HIP, TM_ERR_METRIC = -9, -10, -11
+TM_ERR_UNSUPPORTED, TM_ERR_HIP, TM_ERR_METRIC, TM_ERR_DTYPE = -9, -10, -11, -12
 
 FAKE_IN = 0x100000           # never dereferenced: every call below fails validation
 FAKE_OUT = 0x40000000
@@ -38,7 +38,8 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert {"tm_edt", "tm_edt_sq", "tm_edt_signed", "tm_dt_bf", "tm_cdt", "tm_strerror"} <= set(names)
+    assert {"tm_edt", "tm_edt_sq", "tm_edt_signed", "tm_dt_bf", "tm_cdt", "tm_mask_nonzero",
+            "tm_strerror"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -48,7 +49,7 @@ def test_host_division_constants(lib):
 
 
 def test_strerror_covers_every_status(lib):
-    for s in range(0, -12, -1):
+    for s in range(0, -13, -1):
         msg = binding.tm_strerror(s)
         assert msg and msg != "unknown status", s
     assert binding.tm_strerror(-99) == "unknown status"
@@ -117,8 +118,10 @@ def test_binding_rejects_bad_python_arguments():
         binding.distance_transform_edt(x, return_distances=False, return_indices=False)
     with pytest.raises(RuntimeError):
         binding.distance_transform_edt(x, sampling=[1.0, 2.0, 3.0])
+    with pytest.raises(ValueError):
+        binding.distance_transform_edt(x.float())                         # any dtype, but on the GPU
     with pytest.raises(TypeError):
-        binding.distance_transform_edt(x.float())
+        binding._as_mask(torch.zeros((1, 1, 4, 4), dtype=torch.complex64, device="meta"))
     with pytest.raises(ValueError):
         binding.distance_transform_edt(torch.zeros((4, 4), dtype=torch.uint8))
 
@@ -168,8 +171,14 @@ def test_chamfer_binding_checks():
         binding.distance_transform_cdt(x, metric="euclidean")
     with pytest.raises(ValueError):
         binding.tm_cdt(x, 2, 1, torch.empty(16, dtype=torch.int32))       # not a GPU tensor
+    with pytest.raises(ValueError):
+        binding.distance_transform_cdt(x, distances=torch.empty((1, 1, 4, 4)))   # CPU input
+    # pre-allocated outputs of the wrong dtype or shape: scipy's RuntimeError
     with pytest.raises(RuntimeError):
-        binding.distance_transform_cdt(x, distances=torch.empty((1, 1, 4, 4)))
+        binding._out_buffer(torch.empty((1, 1, 4, 4)), (1, 1, 4, 4), torch.int32, x.device, "distances")
+    with pytest.raises(RuntimeError):
+        binding._out_buffer(torch.empty((1, 1, 4, 5), dtype=torch.int32), (1, 1, 4, 4), torch.int32,
+                            x.device, "distances")
 
 
 def test_signed_argument_checks(lib):
@@ -185,3 +194,27 @@ def test_signed_argument_checks(lib):
     assert call([16, 16], dist=FAKE_IN + 4) == TM_ERR_ALIAS
     assert call([50000, 2]) == TM_ERR_TOO_LARGE          # sum of n^2 >= 2^31
     assert call([20000, 3]) == TM_ERR_UNSUPPORTED        # strided line past the LDS tile
+
+
+def call_mask(lib, shape, dtype=6, strides=None, inp=FAKE_IN, out=FAKE_OUT, ndim=None):
+    nd = len(shape) if ndim is None else ndim
+    sh = (ctypes.c_int64 * max(len(shape), 1))(*shape) if shape is not None else None
+    st = (ctypes.c_int64 * len(strides))(*strides) if strides is not None else None
+    return lib.tm_mask_nonzero(inp and ctypes.c_void_p(inp), dtype, nd, sh, st,
+                               out and ctypes.c_void_p(out), None)
+
+
+def test_mask_predicate_argument_checks(lib):
+    assert call_mask(lib, [4, 4], dtype=9) == TM_ERR_DTYPE
+    assert call_mask(lib, [4, 4], dtype=-1) == TM_ERR_DTYPE
+    assert call_mask(lib, [4] * 17) == TM_ERR_NDIM
+    assert call_mask(lib, [4], ndim=0) == TM_ERR_NDIM
+    assert call_mask(lib, None, ndim=2) == TM_ERR_SHAPE
+    assert call_mask(lib, [4, 0]) == TM_ERR_SHAPE
+    assert call_mask(lib, [4, 4], strides=[16, -4]) == TM_ERR_SHAPE
+    assert call_mask(lib, [4, 4], inp=0) == TM_ERR_NULL
+    assert call_mask(lib, [4, 4], out=0) == TM_ERR_NO_OUTPUT
+    assert call_mask(lib, [1 << 16, 1 << 16], dtype=0) == TM_ERR_TOO_LARGE
+    # the output may not overlap the bytes the strided view reads
+    assert call_mask(lib, [4, 4], dtype=6, out=FAKE_IN + 60) == TM_ERR_ALIAS
+    assert call_mask(lib, [4, 4], dtype=6, strides=[64, 4], out=FAKE_IN + 200) == TM_ERR_ALIAS
