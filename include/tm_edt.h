@@ -56,9 +56,10 @@ typedef enum {
     TM_ERR_NO_OUTPUT = -5,   /* every output pointer is NULL */
     TM_ERR_SAMPLING = -6,    /* a sampling entry is not finite or not > 0 */
     TM_ERR_TOO_LARGE = -7,   /* >= 2^31 elements per sample, batch * elements overflows,
-                                or (unit sampling) squared distances may exceed int32 */
+                                or (tm_edt_sq, tm_edt_signed, tm_dt_bf) squared distances
+                                may exceed int32 */
     TM_ERR_ALIAS = -8,       /* two of the buffers overlap */
-    TM_ERR_UNSUPPORTED = -9, /* a line is longer than the envelope kernels hold in LDS */
+    TM_ERR_UNSUPPORTED = -9, /* a line is longer than the signed or chessboard kernels hold */
     TM_ERR_HIP = -10,        /* the HIP runtime reported an error while enqueuing */
     TM_ERR_METRIC = -11,     /* metric is not one of tm_metric */
     TM_ERR_DTYPE = -12       /* dtype is not one of tm_dtype */
@@ -69,9 +70,13 @@ typedef enum {
  *
  *   sampling  NULL, or ndim spacings (all finite and > 0).  NULL or all 1.0
  *             runs the exact integer path (squared distances are exact
- *             integers; out_dist is the correctly rounded float sqrt).  Other
- *             spacings run with float32 storage and double breakpoint tests;
- *             distances then agree with an exact evaluation to ~1e-6 relative.
+ *             integers, of any size the shape allows; out_dist is the
+ *             correctly rounded float sqrt).  Other spacings run with float32
+ *             storage and double breakpoint tests; distances then agree with
+ *             an exact evaluation to ~1e-6 relative.
+ * Lines of any length along any axis (paper, Section 2.3.2: lines longer
+ * than on-chip memory keep their envelope in device memory; here it lives
+ * inside the line's own output storage, so nothing is allocated).
  *   out_dist  NULL, or [batch][shape...] float32 distances.
  *   out_idx   NULL, or [batch][ndim][shape...] int32 coordinates of the
  *             nearest background element.
@@ -153,7 +158,9 @@ int tm_dt_bf(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch
  * offer sites.  in_u8, ndim, shape, batch as for tm_edt; out_dist: device
  * float32 [batch][shape...], written completely.  Errors: as tm_edt (no
  * sampling argument), and TM_ERR_UNSUPPORTED for lines longer than about
- * 10000 elements along an axis other than the last.
+ * 40 700 elements along an axis other than the last (one whole 32-bit line
+ * per workgroup in LDS; squared distances in int32 already cap the extents
+ * at 46 340).
  */
 int tm_edt_signed(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
                   float *out_dist, hipStream_t stream);
@@ -171,10 +178,11 @@ int tm_edt_signed(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t 
  * is reachable).  in_u8, ndim, shape, batch as for tm_edt.  out_dist:
  * device int32 [batch][shape...], written completely, not aliasing in_u8.
  * Errors: as tm_edt_sq (TM_ERR_NO_OUTPUT for a NULL out_dist), plus
- * TM_ERR_METRIC for TM_METRIC_EUCLIDEAN or an unknown metric, and
- * TM_ERR_UNSUPPORTED for lines longer than the kernels take along an axis
- * other than the last (about 20000 elements while every distance fits 16
- * bits, else about 10000).
+ * TM_ERR_METRIC for TM_METRIC_EUCLIDEAN or an unknown metric.  Taxicab
+ * lines of any length are taken; chessboard lines along an axis other than
+ * the last are held whole in LDS, which takes up to about 81 400 elements
+ * while every distance fits 16 bits and about 40 700 otherwise: longer ones
+ * give TM_ERR_UNSUPPORTED.
  */
 int tm_cdt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, int metric,
            int32_t *out_dist, hipStream_t stream);

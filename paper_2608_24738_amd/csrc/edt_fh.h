@@ -246,7 +246,10 @@ __global__ void __launch_bounds__(64) k_fh_field(FieldArgs a) {
 // of the index output; squared distances are recomputed from it exactly.
 // ---------------------------------------------------------------------------
 struct IndexArgs {
-    int32_t *idx;            // [batch][ndim][vox]
+    int32_t *idx;            // the carrier: slice 0 of [batch][ndim][vox], or a distance
+                             // output holding flat indices (cstride = vox)
+    uint64_t cstride;        // carrier elements per sample
+    int32_t coords;          // final pass: write the ndim coordinate slices at idx
     uint64_t lines;          // batch * lps
     uint32_t lps;            // lines per sample
     uint32_t n;              // line length
@@ -279,7 +282,7 @@ __global__ void __launch_bounds__(64) k_fh_index(IndexArgs a) {
     const uint32_t o = a.div_inner.div(r);
     const uint32_t i = r - o * a.inner;
     const uint32_t base = o * uint32_t(n) * a.inner;  // in-sample flat of (outer, 0, 0..)
-    int32_t *slice0 = a.idx + s * uint64_t(nd) * a.vox;
+    int32_t *slice0 = a.idx + s * a.cstride;
     int32_t *line = slice0 + base + i;
     const uint64_t inner = a.inner;
     const uint32_t stride = a.lpw;
@@ -403,8 +406,10 @@ __global__ void __launch_bounds__(64) k_fh_index(IndexArgs a) {
                 else acc += A(q + 1) * A(q + 1);
                 if (a.dist) a.dist[s * vox + loc] = float(sqrt(double(acc)));
                 if (a.sq) a.sq[s * vox + loc] = int32_t(acc);
-                slice0[loc] = -1;
-                for (int b = 1; b < nd; ++b) slice0[uint64_t(b) * vox + loc] = 0;
+                if (a.coords) {
+                    slice0[loc] = -1;
+                    for (int b = 1; b < nd; ++b) slice0[uint64_t(b) * vox + loc] = 0;
+                }
             }
         }
         return;
@@ -451,10 +456,12 @@ __global__ void __launch_bounds__(64) k_fh_index(IndexArgs a) {
             const uint64_t loc = base + i + e;
             if (a.dist) a.dist[s * vox + loc] = float(sqrt(double(d2)));
             if (a.sq) a.sq[s * vox + loc] = int32_t(d2);
-            slice0[loc] = vc;
+            if (a.coords) {
+                slice0[loc] = vc;
 #pragma unroll
-            for (int b = 1; b < kMaxDim; ++b)
-                if (b < nd) slice0[uint64_t(b) * vox + loc] = cc[b];
+                for (int b = 1; b < kMaxDim; ++b)
+                    if (b < nd) slice0[uint64_t(b) * vox + loc] = cc[b];
+            }
         }
     }
 }

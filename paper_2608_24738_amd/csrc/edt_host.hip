@@ -32,6 +32,7 @@
 #include "edt_col.h"
 #include "edt_small.h"
 #include "edt_mask.h"
+#include "edt_long.h"
 
 using namespace tmedt;
 
@@ -136,6 +137,7 @@ struct Request {
     hipStream_t stream;
     int metric;      // kL2 (exact transform) or kL1 / kLinf (chamfer; output in sq)
     bool sgn;        // signed transform EDT(M) - EDT(not M) (kL2, unit, output in dist)
+    bool big;        // unit sampling with squared distances that may pass int32
 };
 
 int validate(const uint8_t *in, int ndim, const int64_t *shape, int64_t batch,
@@ -164,7 +166,8 @@ int validate(const uint8_t *in, int ndim, const int64_t *shape, int64_t batch,
         r.shape[a] = uint32_t(shape[a]);
     }
     if (uint64_t(batch) >= (uint64_t(1) << 32) / vox) return TM_ERR_TOO_LARGE;
-    if (squared && r.unit && sumsq >= (uint64_t(1) << 31) - 1) return TM_ERR_TOO_LARGE;
+    r.big = r.unit && sumsq >= (uint64_t(1) << 31) - 1;
+    if (squared && r.big) return TM_ERR_TOO_LARGE;
     r.in = in;
     r.ndim = ndim;
     r.batch = uint64_t(batch);
@@ -185,19 +188,21 @@ struct FhPlan {
     bool tiled16;    // paired 16-bit tile with guard rows (k_tile_pair)
     bool from_mask;  // tiled16 on axis ndim-2, computing the last-axis pass itself
     bool tidx;       // tiled pass on the index carrier (k_tile_idx)
-    int ls_lpw;      // whole lines in LDS, windowed search (k_line_search): lines per workgroup (8 or 4), 0 = not
+    int ls_lpw;      // whole lines in LDS, windowed search (k_line_search): lines per workgroup (8, 4, 2, 1), 0 = not
     bool ls_w16;     //   with a 16-bit tile
     uint32_t rbits;  // tidx, unit sampling: bits of the row in a key
+    bool lng;        // index carrier, envelope in the line's own storage (k_fh_long)
+    bool l1long;     // taxicab, two running minima in place (k_cdt_l1_long)
 };
 
 // Whole-line windowed search: 8 lines per workgroup (a wave covers 8 rows
 // of 8 lines, whose search lengths vary less than those of 64 lines of one
-// row), or 4 when the tile of 8 does not fit LDS.
-bool plan_line_search(FhPlan &p, uint32_t n, uint64_t total, bool w16) {
+// row), or fewer (down to min_lpw) when the tile of 8 does not fit LDS.
+bool plan_line_search(FhPlan &p, uint32_t n, uint64_t total, bool w16, int min_lpw = 4) {
     const int tb = w16 ? 2 : 4;
     const uint64_t lines = total / n;
     int lpw = 0;
-    for (int c = 8; c >= 4 && !lpw; c /= 2)
+    for (int c = 8; c >= min_lpw && !lpw; c /= 2)
         if (line_search_lds(n, c, tb) + 1024 <= kLdsBytes) lpw = c;
     if (!lpw || lines + uint64_t(lpw) >= (uint64_t(1) << 32) || (lines + lpw - 1) / lpw >= (uint64_t(1) << 31))
         return false;
@@ -285,40 +290,13 @@ int run_plane(Request &r, uint64_t total, uint64_t vox) {
                   lds, r.stream, tg);
 }
 
-int run(Request &r) {
+// Plan of every strided pass, axis nd-2 down to 0, before anything is
+// launched.  index_path: the index carrier (flat index of the nearest
+// background element); otherwise the field carrier (unit squared distances).
+// Returns TM_ERR_UNSUPPORTED when a pass has no kernel for its lines.
+int plan_passes(const Request &r, uint64_t total, bool index_path, FhPlan *fh) {
     const int nd = r.ndim;
-    uint64_t vox = 1;
-    for (int a = 0; a < nd; ++a) vox *= r.shape[a];
-    const uint64_t total = r.batch * vox;
-
-    // Buffers must not overlap.
-    const uint64_t nin = total, nf = 4 * total, ni = 4 * total * uint64_t(nd);
-    if (overlaps(r.in, nin, r.dist, nf) || overlaps(r.in, nin, r.sq, nf) ||
-        overlaps(r.in, nin, r.idx, ni) || overlaps(r.dist, nf, r.sq, nf) ||
-        overlaps(r.dist, nf, r.idx, ni) || overlaps(r.sq, nf, r.idx, ni))
-        return TM_ERR_ALIAS;
-
-    const bool index_path = r.idx != nullptr;
-    // Small 2-D samples (both extents at most 64): one workgroup per sample
-    // runs both passes in LDS, in one launch.
-    if (nd == 2 && r.unit && r.metric == kL2 && !r.sgn && r.shape[0] <= uint32_t(kSmallMax) &&
-        r.shape[1] <= uint32_t(kSmallMax) && r.batch < (uint64_t(1) << 31)) {
-        SmallArgs sa{};
-        sa.mask = r.in;
-        sa.dist = r.dist;
-        sa.sq = r.sq;
-        sa.idx = r.idx;
-        sa.n0 = r.shape[0];
-        sa.n1 = r.shape[1];
-        return launch("small2d", k_small2d, dim3(uint32_t(r.batch)), dim3(kWave * kSmallWaves), 0, r.stream, sa);
-    }
-    if (!index_path && r.unit && r.metric == kL2 && !r.sgn) {
-        const int rc = run_plane(r, total, vox);
-        if (rc != kNotPlane) return rc;
-    }
-
-    // Plan and check every strided pass before launching anything.
-    FhPlan fh[kMaxDim] = {};
+    for (int a = 0; a < kMaxDim; ++a) fh[a] = FhPlan{};
     for (int a = nd - 2; a >= 0; --a) {
         const uint32_t n = r.shape[a];
         uint64_t fmax = 0;
@@ -326,7 +304,7 @@ int run(Request &r) {
         FhPlan &p = fh[a];
         if (r.sgn) {
             // signed transform: whole-line search over the signed field
-            if (!plan_line_search(p, n, total, false)) return TM_ERR_UNSUPPORTED;
+            if (!plan_line_search(p, n, total, false, 1)) return TM_ERR_UNSUPPORTED;
             continue;
         }
         if (r.metric != kL2) {
@@ -359,8 +337,13 @@ int run(Request &r) {
                 continue;
             }
             const uint64_t cmax = r.metric == kL1 ? vmax + n + 4 : std::max<uint64_t>(vmax, n + 4);
-            if (!plan_line_search(p, n, total, cmax < uint64_t(kNone16))) return TM_ERR_UNSUPPORTED;
-            continue;
+            if (plan_line_search(p, n, total, cmax < uint64_t(kNone16), 1)) continue;
+            // taxicab lines of any length: two running minima in place
+            if (r.metric == kL1) {
+                p.l1long = true;
+                continue;
+            }
+            return TM_ERR_UNSUPPORTED;
         }
         p.acc = !r.unit ? 3 : int24_safe(fmax, n) ? 0 : int32_safe(fmax, n) ? 1 : 2;
         uint32_t eb;
@@ -416,8 +399,9 @@ int run(Request &r) {
             const size_t tb = size_t(2) * idx_tile_words(n) * 4;
             int rb = bits_for(n - 1);
             if (rb < 1) rb = 1;
-            const bool keys_fit = !r.unit || (rb < 31 &&
-                ((fmax + uint64_t(n - 1) * (n - 1)) << rb | uint64_t(n - 1)) < (uint64_t(1) << 31));
+            const uint64_t kv = fmax + uint64_t(n - 1) * (n - 1);
+            const bool keys_fit = !r.unit || (rb < 31 && kv < (uint64_t(1) << 31) &&
+                                              ((kv << rb) | uint64_t(n - 1)) < (uint64_t(1) << 31));
             if (tb + 1024 <= kLdsBytes && keys_fit && total / n + kWave < (uint64_t(1) << 32)) {
                 p.tidx = true;
                 p.rbits = uint32_t(rb);
@@ -425,11 +409,73 @@ int run(Request &r) {
                 continue;
             }
         }
-        if (p.lpw == 0) return TM_ERR_UNSUPPORTED;
         const uint64_t lines = total / n;
-        if ((lines + p.lpw - 1) / p.lpw >= (uint64_t(1) << 31)) return TM_ERR_UNSUPPORTED;
+        if (p.lpw == 0 || (lines + p.lpw - 1) / p.lpw >= (uint64_t(1) << 31)) {
+            // the field carrier has no kernel for this line; the index
+            // carrier keeps the envelope in the line's own storage
+            if (!index_path) return TM_ERR_UNSUPPORTED;
+            p.lpw = 0;
+            p.lng = true;
+            continue;
+        }
         p.lds = size_t(n) * p.lpw * eb;
     }
+    return TM_OK;
+}
+
+int run(Request &r) {
+    const int nd = r.ndim;
+    uint64_t vox = 1;
+    for (int a = 0; a < nd; ++a) vox *= r.shape[a];
+    const uint64_t total = r.batch * vox;
+
+    // Buffers must not overlap.
+    const uint64_t nin = total, nf = 4 * total, ni = 4 * total * uint64_t(nd);
+    if (overlaps(r.in, nin, r.dist, nf) || overlaps(r.in, nin, r.sq, nf) ||
+        overlaps(r.in, nin, r.idx, ni) || overlaps(r.dist, nf, r.sq, nf) ||
+        overlaps(r.dist, nf, r.idx, ni) || overlaps(r.sq, nf, r.idx, ni))
+        return TM_ERR_ALIAS;
+
+    // Small 2-D samples (both extents at most 64): one workgroup per sample
+    // runs both passes in LDS, in one launch.
+    if (nd == 2 && r.unit && r.metric == kL2 && !r.sgn && r.shape[0] <= uint32_t(kSmallMax) &&
+        r.shape[1] <= uint32_t(kSmallMax) && r.batch < (uint64_t(1) << 31)) {
+        SmallArgs sa{};
+        sa.mask = r.in;
+        sa.dist = r.dist;
+        sa.sq = r.sq;
+        sa.idx = r.idx;
+        sa.n0 = r.shape[0];
+        sa.n1 = r.shape[1];
+        return launch("small2d", k_small2d, dim3(uint32_t(r.batch)), dim3(kWave * kSmallWaves), 0, r.stream, sa);
+    }
+    if (!r.idx && r.unit && !r.big && r.metric == kL2 && !r.sgn) {
+        const int rc = run_plane(r, total, vox);
+        if (rc != kNotPlane) return rc;
+    }
+
+    // The carrier between passes.  With indices: the flat index of the
+    // nearest background element, in slice 0 of out_idx.  Distances only,
+    // unit sampling: the squared distance itself, in the output.  Distances
+    // only otherwise (sampled, squared distances that may pass int32, or a
+    // line no field kernel holds): the flat index again, inside the 32-bit
+    // distance output, which the final pass overwrites with the distances.
+    FhPlan fh[kMaxDim];
+    bool index_path = r.idx != nullptr;
+    int prc = TM_OK;
+    if (!index_path && r.metric == kL2 && !r.sgn) {
+        if (r.unit && !r.big) prc = plan_passes(r, total, false, fh);
+        if (!r.unit || r.big || prc != TM_OK) {
+            index_path = true;
+            prc = plan_passes(r, total, true, fh);
+        }
+    } else {
+        prc = plan_passes(r, total, index_path, fh);
+    }
+    if (prc != TM_OK) return prc;
+    int32_t *const cidx = r.idx ? r.idx : r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
+    const uint64_t cstride = r.idx ? uint64_t(nd) * vox : vox;
+    const int coords = r.idx ? 1 : 0;
     // Consecutive paired passes whose rows are whole 128-element runs hand
     // their field over in the 16-bit segment layout.
     bool out_seg[kMaxDim] = {};
@@ -443,9 +489,6 @@ int run(Request &r) {
         for (int a = nd - 2; a >= 1; --a) out_seg[a] = seg_ok[a] && seg_ok[a - 1];
     }
     const uint32_t nlast = r.shape[nd - 1];
-    if (nlast > uint32_t(kSpan) &&
-        (uint64_t(nlast + kSpan - 1) / kSpan + 1) * 4 > kLdsBytes)
-        return TM_ERR_UNSUPPORTED;
 
     int rc;
     // ---- pass over the last axis: nearest zero in each contiguous line ----
@@ -491,8 +534,9 @@ int run(Request &r) {
             out = nullptr;   // scalar stores: no alignment needed
         } else if (index_path) {
             mode = kScanIndex;
-            s.idx = r.idx;
-            out = r.idx;
+            s.idx = cidx;
+            s.cstride = cstride;
+            out = cidx;
         } else if (r.unit) {
             mode = kScanFieldInt;
             s.field_i = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
@@ -523,6 +567,7 @@ int run(Request &r) {
             ws.field_i = s.field_i;
             ws.field_f = s.field_f;
             ws.idx = s.idx;
+            ws.cstride = s.cstride;
             ws.dist = s.dist;
             ws.sq = s.sq;
             const uint64_t waves = (ws.lines + ws.lpw - 1) / ws.lpw;
@@ -558,7 +603,7 @@ int run(Request &r) {
         } else {
             s.span_lines = 1;
             const dim3 grid(s.lines), block(kWave);
-            const size_t lds = size_t(nlast / kSpan + 2) * 4;
+            const size_t lds = 0;
             switch (mode) {
                 case kScanFieldInt: rc = launch("scan_long", k_scan_long<kScanFieldInt>, grid, block, lds, r.stream, s); break;
                 case kScanFieldL1: rc = launch("scan_long", k_scan_long<kScanFieldL1>, grid, block, lds, r.stream, s); break;
@@ -586,7 +631,17 @@ int run(Request &r) {
         const uint32_t lpw = p.lpw ? p.lpw : 1;     // lines per wave of the envelope kernels
         const dim3 grid(uint32_t((lines + lpw - 1) / lpw)), block(kWave);
         const bool fin = a == 0;
-        if (p.tiled16) {
+        if (p.l1long) {
+            L1LongArgs la{};
+            la.buf = r.sq;
+            la.lines = lines;
+            la.n = n;
+            la.inner = uint32_t(inner);
+            la.div_inner = Div32::make(la.inner);
+            const dim3 lgrid(uint32_t((lines + kWave - 1) / kWave)), lblock(kWave);
+            rc = fin ? launch("cdt_l1_long_final", k_cdt_l1_long<true>, lgrid, lblock, 0, r.stream, la)
+                     : launch("cdt_l1_long", k_cdt_l1_long<false>, lgrid, lblock, 0, r.stream, la);
+        } else if (p.tiled16) {
             PairArgs tg{};
             tg.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
             tg.mask = r.in;
@@ -661,22 +716,26 @@ int run(Request &r) {
             const dim3 lgrid(uint32_t((lines + p.ls_lpw - 1) / p.ls_lpw)), lblock(kWave * kLsWaves);
             const char *nm = r.metric == kL2 ? (fin ? "line_search_final" : "line_search")
                                              : (fin ? "cdt_line_final" : "cdt_line");
+#define TM_LS4(M, F, W, S)                                                                                 \
+    (p.ls_lpw == 8   ? launch(nm, k_line_search<M, F, W, 8, S>, lgrid, lblock, p.lds, r.stream, la)          \
+     : p.ls_lpw == 4 ? launch(nm, k_line_search<M, F, W, 4, S>, lgrid, lblock, p.lds, r.stream, la)          \
+     : p.ls_lpw == 2 ? launch(nm, k_line_search<M, F, W, 2, S>, lgrid, lblock, p.lds, r.stream, la)          \
+                     : launch(nm, k_line_search<M, F, W, 1, S>, lgrid, lblock, p.lds, r.stream, la))
+            // lines of the exact transform keep to 8 or 4 per workgroup (the
+            // planner sends longer ones to the envelope kernels)
 #define TM_LS(M, F, W)                                                                                  \
     (p.ls_lpw == 8 ? launch(nm, k_line_search<M, F, W, 8>, lgrid, lblock, p.lds, r.stream, la)         \
                    : launch(nm, k_line_search<M, F, W, 4>, lgrid, lblock, p.lds, r.stream, la))
             if (r.sgn) {
                 nm = fin ? "line_search_signed_final" : "line_search_signed";
-                rc = p.ls_lpw == 8
-                         ? (fin ? launch(nm, k_line_search<kL2, true, false, 8, true>, lgrid, lblock, p.lds, r.stream, la)
-                                : launch(nm, k_line_search<kL2, false, false, 8, true>, lgrid, lblock, p.lds, r.stream, la))
-                         : (fin ? launch(nm, k_line_search<kL2, true, false, 4, true>, lgrid, lblock, p.lds, r.stream, la)
-                                : launch(nm, k_line_search<kL2, false, false, 4, true>, lgrid, lblock, p.lds, r.stream, la));
+                rc = fin ? TM_LS4(kL2, true, false, true) : TM_LS4(kL2, false, false, true);
             } else if (r.metric == kL2) rc = fin ? TM_LS(kL2, true, false) : TM_LS(kL2, false, false);
-            else if (r.metric == kL1 && p.ls_w16) rc = fin ? TM_LS(kL1, true, true) : TM_LS(kL1, false, true);
-            else if (r.metric == kL1) rc = fin ? TM_LS(kL1, true, false) : TM_LS(kL1, false, false);
-            else if (p.ls_w16) rc = fin ? TM_LS(kLinf, true, true) : TM_LS(kLinf, false, true);
-            else rc = fin ? TM_LS(kLinf, true, false) : TM_LS(kLinf, false, false);
+            else if (r.metric == kL1 && p.ls_w16) rc = fin ? TM_LS4(kL1, true, true, false) : TM_LS4(kL1, false, true, false);
+            else if (r.metric == kL1) rc = fin ? TM_LS4(kL1, true, false, false) : TM_LS4(kL1, false, false, false);
+            else if (p.ls_w16) rc = fin ? TM_LS4(kLinf, true, true, false) : TM_LS4(kLinf, false, true, false);
+            else rc = fin ? TM_LS4(kLinf, true, false, false) : TM_LS4(kLinf, false, false, false);
 #undef TM_LS
+#undef TM_LS4
         } else if (!index_path) {
             FieldArgs f{};
             f.buf = r.dist ? static_cast<void *>(r.dist) : static_cast<void *>(r.sq);
@@ -696,8 +755,7 @@ int run(Request &r) {
             }
             const char *nm = fin ? "fh_field_final" : "fh_field";
 #define TM_FIELD(M, PK, FN) launch(nm, k_fh_field<M, PK, FN>, grid, block, p.lds, r.stream, f)
-            if (p.acc == 3) rc = fin ? TM_FIELD(ArF64, false, true) : TM_FIELD(ArF64, false, false);
-            else if (p.acc == 0 && p.pack) rc = fin ? TM_FIELD(ArI24, true, true) : TM_FIELD(ArI24, true, false);
+            if (p.acc == 0 && p.pack) rc = fin ? TM_FIELD(ArI24, true, true) : TM_FIELD(ArI24, true, false);
             else if (p.acc == 0) rc = fin ? TM_FIELD(ArI24, false, true) : TM_FIELD(ArI24, false, false);
             else if (p.acc == 1 && p.pack) rc = fin ? TM_FIELD(ArI32, true, true) : TM_FIELD(ArI32, true, false);
             else if (p.acc == 1) rc = fin ? TM_FIELD(ArI32, false, true) : TM_FIELD(ArI32, false, false);
@@ -706,7 +764,9 @@ int run(Request &r) {
 #undef TM_FIELD
         } else if (p.tidx) {
             IdxTileArgs x{};
-            x.idx = r.idx;
+            x.idx = cidx;
+            x.cstride = cstride;
+            x.coords = coords;
             x.lines = uint32_t(lines);
             x.lps = uint32_t(vox / n);
             x.n = n;
@@ -733,7 +793,9 @@ int run(Request &r) {
                          : launch("tile_idx", k_tile_idx<true, false>, igrid, iblock, p.lds, r.stream, x);
         } else {
             IndexArgs x{};
-            x.idx = r.idx;
+            x.idx = cidx;
+            x.cstride = cstride;
+            x.coords = coords;
             x.lines = lines;
             x.lps = uint32_t(vox / n);
             x.n = n;
@@ -749,6 +811,18 @@ int run(Request &r) {
             }
             x.dist = fin ? r.dist : nullptr;
             x.sq = fin ? r.sq : nullptr;
+            if (p.lng) {
+                const dim3 lgrid(uint32_t((lines + kWave - 1) / kWave)), lblock(kWave);
+                const char *ln = fin ? "fh_long_final" : "fh_long";
+                if (r.unit)
+                    rc = fin ? launch(ln, k_fh_long<false, true>, lgrid, lblock, 0, r.stream, x)
+                             : launch(ln, k_fh_long<false, false>, lgrid, lblock, 0, r.stream, x);
+                else
+                    rc = fin ? launch(ln, k_fh_long<true, true>, lgrid, lblock, 0, r.stream, x)
+                             : launch(ln, k_fh_long<true, false>, lgrid, lblock, 0, r.stream, x);
+                if (rc != TM_OK) return rc;
+                continue;
+            }
             const char *nm = fin ? "fh_index_final" : "fh_index";
 #define TM_INDEX(M, FN) launch(nm, k_fh_index<M, FN>, grid, block, p.lds, r.stream, x)
             if (p.acc == 3) rc = fin ? TM_INDEX(ArF64, true) : TM_INDEX(ArF64, false);
@@ -771,7 +845,9 @@ extern "C" int tm_edt(const uint8_t *in_u8, int ndim, const int64_t *shape, int6
                       const double *sampling, float *out_dist, int32_t *out_idx,
                       hipStream_t stream) {
     Request r{};
-    int rc = validate(in_u8, ndim, shape, batch, sampling, out_dist, out_idx, nullptr, r);
+    // float outputs: exact squared distances of any size are carried in
+    // 64-bit arithmetic (flat-index carrier), so no int32 bound applies
+    int rc = validate(in_u8, ndim, shape, batch, sampling, out_dist, out_idx, nullptr, r, false);
     if (rc != TM_OK) return rc;
     r.dist = out_dist;
     r.sq = nullptr;
@@ -921,7 +997,7 @@ extern "C" const char *tm_strerror(int status) {
         case TM_ERR_SAMPLING: return "sampling entries must be finite and positive";
         case TM_ERR_TOO_LARGE: return "input too large for 32-bit indices or int32 squared distances";
         case TM_ERR_ALIAS: return "input and output buffers overlap";
-        case TM_ERR_UNSUPPORTED: return "a line is longer than the envelope stack held in LDS";
+        case TM_ERR_UNSUPPORTED: return "a line is longer than the signed or chessboard kernels hold in LDS";
         case TM_ERR_HIP: return "HIP runtime error while enqueuing kernels";
         case TM_ERR_METRIC: return "metric must be euclidean, taxicab or chessboard";
         case TM_ERR_DTYPE: return "element type is not one of tm_dtype";

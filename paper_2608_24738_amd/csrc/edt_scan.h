@@ -37,7 +37,10 @@ struct ScanArgs {
     double w;              // squared sampling of the last axis
     int32_t *field_i;      // kScanFieldInt output (batch-flat)
     float *field_f;        // kScanFieldFlt output (batch-flat)
-    int32_t *idx;          // kScanIndex: [batch][ndim][vox] (slice 0 written); kScanFinal: coords
+    int32_t *idx;          // kScanIndex: the carrier, cstride elements per sample (slice 0 of
+                           // [batch][ndim][vox], or a distance output holding flat indices);
+                           // kScanFinal: coords
+    uint64_t cstride;      // kScanIndex: carrier elements per sample
     float *dist;           // kScanFinal outputs (each may be null)
     int32_t *sq;
 };
@@ -156,7 +159,7 @@ __device__ inline void scan_store4(const ScanArgs &a, uint32_t gline, int x0, co
         int32_t v[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) v[j] = y[j] >= 0 ? int32_t(local + y[j]) : kNoIdx;
-        int32_t *o = a.idx + uint64_t(s) * a.ndim * a.vox + local + x0;
+        int32_t *o = a.idx + uint64_t(s) * a.cstride + local + x0;
         if (VEC) {
             *reinterpret_cast<int4 *>(o) = make_int4(v[0], v[1], v[2], v[3]);
         } else {
@@ -229,19 +232,37 @@ __global__ void __launch_bounds__(256) k_scan_span(ScanArgs a) {
     }
 }
 
+// The 32-bit output word of position x of line `gline` (the first output
+// present in the rank-1 case).
+template <int MODE>
+__device__ inline uint32_t *scan_slot(const ScanArgs &a, uint32_t gline, int x) {
+    const uint64_t lbase = uint64_t(gline) * a.n;
+    if (MODE == kScanFieldInt || MODE == kScanFieldL1) return reinterpret_cast<uint32_t *>(a.field_i + lbase + x);
+    if (MODE == kScanFieldFlt) return reinterpret_cast<uint32_t *>(a.field_f + lbase + x);
+    if (MODE == kScanIndex) {
+        const uint32_t s = a.div_lps.div(gline);
+        const uint64_t local = uint64_t(gline - s * a.lps) * a.n;
+        return reinterpret_cast<uint32_t *>(a.idx + uint64_t(s) * a.cstride + local + x);
+    }
+    if (a.dist) return reinterpret_cast<uint32_t *>(a.dist + lbase + x);
+    if (a.sq) return reinterpret_cast<uint32_t *>(a.sq + lbase + x);
+    return reinterpret_cast<uint32_t *>(a.idx + lbase + x);
+}
+
 // Lines longer than 1024: one wavefront per line, two sweeps over 1024-
-// position chunks.  The first (right to left) stores, per chunk, the first
-// zero at or after the chunk start in LDS; the second (left to right) carries
-// the last zero seen and reads the right carry from LDS.
+// position chunks.  The first (right to left) finds, per chunk, the first
+// zero at or after the chunk start and parks it in the output word of the
+// chunk's first position (every lane writes the same value there, and reads
+// it back itself); the second (left to right) carries the last zero seen and
+// reads the right carry of the next chunk before this chunk's results are
+// stored.  Lines of any length, no workspace.
 template <int MODE>
 __global__ void __launch_bounds__(64) k_scan_long(ScanArgs a) {
-    extern __shared__ int first_from[];  // [chunks + 1]
     const int lane = threadIdx.x;
     const uint32_t gline = blockIdx.x;
     const uint8_t *src = a.in + uint64_t(gline) * a.n;
     const int n = int(a.n);
     const int chunks = (n + kSpan - 1) / kSpan;
-    if (lane == 0) first_from[chunks] = kBig;
     int carry = kBig;
     for (int c = chunks - 1; c >= 0; --c) {
         const int valid = min(kSpan, n - c * kSpan);
@@ -254,9 +275,8 @@ __global__ void __launch_bounds__(64) k_scan_long(ScanArgs a) {
 #pragma unroll
         for (int d = 32; d >= 1; d >>= 1) m = min(m, __shfl_xor(m, d, kWave));
         carry = min(carry, m);
-        if (lane == 0) first_from[c] = carry;
+        if (c >= 1) *scan_slot<MODE>(a, gline, c * kSpan) = uint32_t(carry);
     }
-    __syncthreads();
     int last = -kBig;  // last zero before the current chunk (line-relative)
     for (int c = 0; c < chunks; ++c) {
         const int valid = min(kSpan, n - c * kSpan);
@@ -264,7 +284,7 @@ __global__ void __launch_bounds__(64) k_scan_long(ScanArgs a) {
         uint32_t zb[4];
         load_zero_bits<false>(src + off, valid, lane, zb);
         const int cl = last == -kBig ? -kBig : last - off;
-        const int nxt = first_from[c + 1];
+        const int nxt = c + 1 < chunks ? int(*scan_slot<MODE>(a, gline, (c + 1) * kSpan)) : kBig;
         const int cr = nxt == kBig ? kBig : nxt - off;
         int left[4][4], right[4][4];
         chunk_candidates(zb, cl, cr, lane, left, right);
@@ -320,7 +340,8 @@ struct WordScanArgs {
     double w;              // squared sampling of the last axis
     int32_t *field_i;      // kScanFieldInt output
     float *field_f;        // kScanFieldFlt output
-    int32_t *idx;          // kScanIndex: slice 0 of [batch][ndim][vox]; kScanFinal: coords
+    int32_t *idx;          // kScanIndex: the carrier (see ScanArgs); kScanFinal: coords
+    uint64_t cstride;      // kScanIndex: carrier elements per sample
     float *dist;           // kScanFinal outputs (each may be null)
     int32_t *sq;
 };
@@ -434,7 +455,7 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
         uint64_t own;
         if (MODE == kScanIndex) {
             db = a.idx;
-            own = smp * uint64_t(a.ndim) * a.vox + local + uint64_t(w) * WB;
+            own = smp * a.cstride + local + uint64_t(w) * WB;
         } else {
             db = MODE == kScanFieldFlt ? reinterpret_cast<int32_t *>(a.field_f) : a.field_i;
             own = pos0;

@@ -28,8 +28,11 @@ constexpr int kIdxRowW = kWave + 8;  // padded row stride (words)
 constexpr int kIdxPatch = 8;       // patch: 8 rows x 8 lines
 
 struct IdxTileArgs {
-    int32_t *idx;            // [batch][ndim][vox]; slice 0 carries the sites
-    float *dist;             // final pass outputs (each may be null)
+    int32_t *idx;            // the carrier of the sites: slice 0 of [batch][ndim][vox], or a
+                             // distance output holding flat indices (cstride = vox)
+    uint64_t cstride;        // carrier elements per sample
+    int32_t coords;          // final pass: write the ndim coordinate slices at idx
+    float *dist;             // final pass outputs (each may be null; may be the carrier)
     int32_t *sq;
     uint32_t lines;          // batch * lps
     uint32_t lps;            // lines per sample
@@ -163,7 +166,7 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
     const Line me = line_of(lane);
     if (wv == 0) line_info[lane] = uint4{me.s, me.base, me.i, me.live ? 1u : 0u};
     line_coords(me.i);
-    const int32_t *src = a.idx + uint64_t(me.s) * uint32_t(nd) * a.vox + me.base;
+    const int32_t *src = a.idx + uint64_t(me.s) * a.cstride + me.base;
     uint32_t seen = 0;
     constexpr int SB = 8;
     for (int q0 = wv; q0 < n; q0 += kIdxWaves * SB) {
@@ -261,7 +264,7 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         l.s = li.x;
         l.base = li.y;
         l.i = li.z;
-        slice0 = a.idx + uint64_t(l.s) * uint32_t(nd) * a.vox;
+        slice0 = a.idx + uint64_t(l.s) * a.cstride;
         const uint64_t e = uint64_t(l.base) + uint64_t(qr) * a.inner;   // in-sample flat
         int32_t site = -1;
         if (has) {
@@ -272,21 +275,25 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
             slice0[e] = site;
             continue;
         }
-        // final pass: coordinates, distance, squared distance
+        // final pass: coordinates, distance, squared distance (with the
+        // carrier in a distance output, the distance replaces the carried
+        // site in place: this workgroup staged every row of its lines)
         double d2;
         if (site >= 0) {
             if (SAMP) d2 = double(fbest);
             else d2 = double(kbest >> a.rbits);
-            uint32_t t2 = uint32_t(site);
+            if (a.coords) {
+                uint32_t t2 = uint32_t(site);
 #pragma unroll
-            for (int b = kMaxDim - 1; b >= 0; --b) {
-                if (b < nd) {
-                    if (b > 0) {
-                        const uint32_t qd = a.div_shape[b].div(t2);
-                        slice0[uint64_t(b) * a.vox + e] = int32_t(t2 - qd * a.div_shape[b].d);
-                        t2 = qd;
-                    } else {
-                        slice0[e] = int32_t(t2);
+                for (int b = kMaxDim - 1; b >= 0; --b) {
+                    if (b < nd) {
+                        if (b > 0) {
+                            const uint32_t qd = a.div_shape[b].div(t2);
+                            slice0[uint64_t(b) * a.vox + e] = int32_t(t2 - qd * a.div_shape[b].d);
+                            t2 = qd;
+                        } else {
+                            slice0[e] = int32_t(t2);
+                        }
                     }
                 }
             }
@@ -294,8 +301,10 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
             // no background in the sample: the virtual element (-1, 0, ..., 0)
             d2 = virtual_sq<double>(qr, l.i, nd, a.shape, a.wall);
             if (!SAMP) d2 = double(virtual_sq<int64_t>(qr, l.i, nd, a.shape, a.wall));
-            slice0[e] = -1;
-            for (int b = 1; b < nd; ++b) slice0[uint64_t(b) * a.vox + e] = 0;
+            if (a.coords) {
+                slice0[e] = -1;
+                for (int b = 1; b < nd; ++b) slice0[uint64_t(b) * a.vox + e] = 0;
+            }
         }
         // A found site's sampled value is a float, and its correctly rounded
         // float root (sqrtf) equals the double root rounded to float, since

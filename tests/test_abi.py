@@ -104,9 +104,17 @@ def test_overlapping_buffers(lib):
     assert call_sq(lib, [16, 16], sq=FAKE_OUT, idx=FAKE_OUT + 512) == TM_ERR_ALIAS
 
 
-def test_unsupported_long_strided_line(lib):
-    # 60000-long lines along axis 0 with float stacks exceed the LDS budget
-    assert call_edt(lib, [60000, 2], sampling=[1.5, 1.0]) == TM_ERR_UNSUPPORTED
+def test_remaining_line_length_limits(lib):
+    # The exact transform takes strided lines of any length (the envelope of a
+    # line too long for LDS lives in the line's own storage); the limits left
+    # are the signed transform's whole-line tile (32-bit, one line per
+    # workgroup: about 40 700 elements) and the chessboard chamfer pass past
+    # 16-bit values (about 40 700 elements).  These calls are refused on the
+    # host; nothing is launched.
+    assert call_cdt(lib, [70000, 2], metric=2) == TM_ERR_UNSUPPORTED
+    sh = (ctypes.c_int64 * 2)(45000, 3)
+    assert lib.tm_edt_signed(ctypes.c_void_p(FAKE_IN), 2, sh, 1, ctypes.c_void_p(FAKE_OUT), None) \
+        == TM_ERR_UNSUPPORTED
 
 
 def test_binding_rejects_bad_python_arguments():
@@ -157,11 +165,11 @@ def test_chamfer_argument_checks(lib):
     assert call_cdt(lib, [4] * 9) == TM_ERR_NDIM
     assert call_cdt(lib, [16, 16], dist=FAKE_IN + 8) == TM_ERR_ALIAS
     assert call_cdt(lib, [1 << 16, 1 << 15]) == TM_ERR_TOO_LARGE
-    # no bound on squared extents (values are sums, not squares), but lines
-    # past the whole-line pass's LDS budget along a strided axis are refused
-    for metric in (1, 2):
-        assert call_cdt(lib, [50000, 2], metric=metric) == TM_ERR_UNSUPPORTED
-        assert call_cdt(lib, [30000, 2], metric=metric) == TM_ERR_UNSUPPORTED
+    # no bound on squared extents (values are sums, not squares); taxicab
+    # lines of any length run, chessboard lines past the 16-bit whole-line
+    # tile with values beyond 16 bits (about 40 700 elements) are refused
+    assert call_cdt(lib, [70000, 2], metric=2) == TM_ERR_UNSUPPORTED
+    assert call_cdt(lib, [100000, 3], metric=2) == TM_ERR_UNSUPPORTED
 
 
 def test_chamfer_binding_checks():
@@ -193,7 +201,7 @@ def test_signed_argument_checks(lib):
     assert call([4] * 9) == TM_ERR_NDIM
     assert call([16, 16], dist=FAKE_IN + 4) == TM_ERR_ALIAS
     assert call([50000, 2]) == TM_ERR_TOO_LARGE          # sum of n^2 >= 2^31
-    assert call([20000, 3]) == TM_ERR_UNSUPPORTED        # strided line past the LDS tile
+    assert call([45000, 3]) == TM_ERR_UNSUPPORTED        # strided line past the one-line LDS tile
 
 
 def call_mask(lib, shape, dtype=6, strides=None, inp=FAKE_IN, out=FAKE_OUT, ndim=None):
