@@ -4,13 +4,18 @@
 Default workload: 3-D EDT of 8 x 1 x 128^3 uint8 masks whose foreground is the
 union of 30 random solid balls (radius 4-30 voxels) per volume, unit
 sampling, float32 distances.  One step = one tm_edt call over the whole batch
-(the last-axis scan, the axis-1 envelope pass and the fused axis-0 pass), with
-the mask already resident in HBM and the output preallocated.
+with the mask already resident in HBM and the output preallocated.  On this
+shape the call runs two kernels: the axis-0 nearest-background scan straight
+from the mask, writing one byte per voxel ("col_scan.o8"), and one workgroup
+per 128 x 128 plane doing both remaining axes and the square root
+("plane_final.i8").
 
 Prints one JSON line: voxels/s, per-step time, the dominant kernel's
-achieved HBM bandwidth against the MI355X peak (algorithmic bytes over its
-HIP-event-timed average duration), and the CPU oracle's throughput on a
-bounded sample on this host.
+algorithmic bytes per launch over its HIP-event-timed average duration
+against the MI355X HBM peak, the counter-measured traffic and VALU-issue
+share of that kernel when a rocprofv3 summary taken on the current kernel
+sources is committed under profiles/, and the CPU oracle's throughput on a
+bounded sample on this host (median of three runs).
 """
 import argparse
 import glob
@@ -74,16 +79,19 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
         return total * (fin + out_bytes)
     if base == "small2d":                    # mask in; distances (and indices) out
         return total * (1 + out_bytes + (4 * ndim if want_idx else 0))
-    if base in ("fh_index", "tile_idx"):
+    if base in ("fh_index", "tile_idx", "fh_long"):     # flat-index carrier in and out
         return total * (4 + 4)
-    if base in ("fh_index_final", "tile_idx_final"):
-        return total * (4 + 4 * ndim + (out_bytes if want_idx else 0))
+    if base in ("fh_index_final", "tile_idx_final", "fh_long_final"):
+        # carrier in; coordinates (with indices) and distances out
+        return total * (4 + (4 * ndim if want_idx else 0) + out_bytes)
+    if base in ("cdt_l1_long", "cdt_l1_long_final"):
+        return total * (4 + 4) * 2                       # two sweeps, each reads and writes
     raise KeyError(name)
 
 
-def read_counters(kernel, workload_name):
-    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
-    was taken on the current kernel sources."""
+def read_profile(kernel, workload_name):
+    """The JSON block of a committed rocprofv3 summary of `kernel` on
+    `workload_name`, if it was taken on the current kernel sources."""
     path = os.path.join(ROOT, "profiles", "%s__%s.md" % (kernel, workload_name))
     if not os.path.exists(path):
         return None
@@ -98,34 +106,58 @@ def read_counters(kernel, workload_name):
         return None
     if data.get("source_digest") != source_digest():
         return None
-    return data.get("traffic_bytes_per_launch")
+    return data
 
 
-def cpu_baseline(mask_np, ndim, sampling, budget_s=10.0):
+def cpu_model():
+    """The host CPU's model name (lscpu), or None."""
+    try:
+        import subprocess
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, ValueError):
+        pass
+    return None
+
+
+def cpu_baseline(mask_np, ndim, sampling, want_idx, run_s=3.5):
+    """The oracle on this host's cores: three runs, each repeating the whole
+    batch for about `run_s` seconds, reported as the median rate; beside it
+    the median of three single-thread runs on one volume."""
+    import statistics
+
     from oracle import edt_oracle
     nthreads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or min(16, os.cpu_count() or 1)
     used = edt_oracle.threads_used(nthreads)
     batch = mask_np.shape[0]
     vox_per = int(mask_np[0].size)
-    done_vox, reps = 0, 0
-    t0 = time.perf_counter()
-    while True:
-        edt_oracle.edt(mask_np, ndim, sampling, want_sq=False, want_dist=True, want_idx=False,
-                       nthreads=nthreads)
-        reps += 1
-        done_vox += batch * vox_per
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    dt = time.perf_counter() - t0
-    # single-thread figure on one volume, for the paper's one-core comparison
-    t1 = time.perf_counter()
-    edt_oracle.edt(mask_np[:1], ndim, sampling, want_sq=False, want_dist=True, want_idx=False,
-                   nthreads=1)
-    dt1 = time.perf_counter() - t1
-    return {"value": done_vox / dt, "unit": "voxels/s", "cores": used, "kind": "oracle",
-            "sample": "%d x the whole %d-volume batch (%.1f s wall, %d OpenMP threads)"
-                      % (reps, batch, dt, used),
-            "single_thread_value": vox_per / dt1}
+    rates, reps = [], []
+    for _ in range(3):
+        done, n = 0, 0
+        t0 = time.perf_counter()
+        while True:
+            edt_oracle.edt(mask_np, ndim, sampling, want_sq=False, want_dist=True, want_idx=want_idx,
+                           nthreads=nthreads)
+            n += 1
+            done += batch * vox_per
+            if time.perf_counter() - t0 >= run_s:
+                break
+        rates.append(done / (time.perf_counter() - t0))
+        reps.append(n)
+    singles = []
+    for _ in range(3):
+        t1 = time.perf_counter()
+        edt_oracle.edt(mask_np[:1], ndim, sampling, want_sq=False, want_dist=True, want_idx=want_idx,
+                       nthreads=1)
+        singles.append(vox_per / (time.perf_counter() - t1))
+    return {"value": statistics.median(rates), "unit": "voxels/s", "cores": used, "kind": "oracle",
+            "sample": "median of 3 runs, each %s x the whole %d-volume batch (about %.1f s), %d OpenMP "
+                      "threads" % ("/".join(map(str, reps)), batch, run_s, used),
+            "cpu_model": cpu_model(), "nproc": os.cpu_count(),
+            "runs": [round(r) for r in rates],
+            "single_thread_value": statistics.median(singles)}
 
 
 def time_op(step, args, stream):
@@ -174,10 +206,25 @@ def roofline_of(kernels, steps, total, ndim, want_idx, workload_name, out_bytes=
         v["achieved_GBs"] = round(b / (v["avg_ms"] * 1e-3) / 1e9, 1)
         v["avg_ms"] = round(v["avg_ms"], 5)
         v["launches"] = int(v["launches"] / steps)
-    traffic = read_counters(dom, workload_name)
-    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-            "kernel": dom, "launches_per_step": dom_launches_per_step}
+    prof = read_profile(dom, workload_name) or {}
+    out = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+           "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+           "traffic": prof.get("traffic_bytes_per_launch"),
+           "kernel": dom, "launches_per_step": dom_launches_per_step}
+    # What the counters say limits the kernel: its HBM traffic over its
+    # traced duration against the peak, and its VALU issue time (wave
+    # instructions x waves per SIMD x 4 cycles at 2.4 GHz) over the same
+    # duration.  The byte roofline above stays the bound the method is
+    # judged against; these say how far from it the kernel is and why.
+    if prof.get("traced_us"):
+        t = prof["traced_us"] * 1e-6
+        if prof.get("traffic_bytes_per_launch"):
+            out["traffic_frac"] = round(prof["traffic_bytes_per_launch"] / t / 1e9 / HBM_PEAK_GBS, 4)
+        if prof.get("valu_issue_us"):
+            out["valu_issue_frac"] = round(prof["valu_issue_us"] / prof["traced_us"], 3)
+            out["limiter"] = ("valu-issue" if out["valu_issue_frac"] > out.get("traffic_frac", 0.0)
+                              else "hbm")
+    return out
 
 
 def bench_cdt(args, dev, stream):
@@ -294,7 +341,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=3,
-                    help="workload key: 1-5 and 9 edt (3 = headline), 7-8 cdt")
+                    help="workload key (paper_2608_24738_amd/workloads.py): 1-5, 9-15 edt "
+                         "(3 = headline), 7-8 cdt")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run only a plain 256 MiB device copy (counter calibration)")
@@ -362,7 +410,7 @@ def main():
     cpu = None
     if not args.no_cpu:
         log("timing the CPU oracle")
-        cpu = cpu_baseline(mask_np.reshape((w.batch,) + tuple(w.spatial)), ndim, w.sampling)
+        cpu = cpu_baseline(mask_np.reshape((w.batch,) + tuple(w.spatial)), ndim, w.sampling, w.want_idx)
 
     vox_s = total / (ms * 1e-3)
     out = {

@@ -34,6 +34,10 @@ batches:
   9  2-D  8x1x1024x1024,    as 7                                   (EDT, dist)
  10  2-D  8x1x256x256,      as 8                                   (EDT, dist)
  11  3-D  8x1x64^3,         as 3 with r ~ U[2, 15]                 (EDT, dist)
+ 12  3-D  2x1x256^3,        the masks and sampling of 4            (EDT, dist only)
+ 13  3-D  2x1x256^3,        as 3 with r ~ U[8, 60]                 (EDT, dist)
+ 14  2-D  8x1x1024x1024,    one background pixel per image         (EDT, dist)
+ 15  3-D  2x1x256^3,        one background voxel, at the origin    (EDT, dist)
 
 Smaller twins keep the generator and scale ball radii with the smallest
 extent, so parity tests can cover the same structure at sizes the oracle
@@ -59,6 +63,7 @@ class Workload:
     param: dict = field(default_factory=dict)
     sampling: tuple | None = None
     want_idx: bool = False
+    seed_key: int | None = None      # draw the masks of another workload (default: this one)
 
     @property
     def ndim(self) -> int:
@@ -93,6 +98,16 @@ WORKLOADS = {
                  {"count": 20, "r_min": 2.5, "r_max": 30.0}),
     11: Workload(11, "edt3d_8x64x64x64_balls", 8, (64, 64, 64), "balls_fg",
                  {"count": 30, "r_min": 2.0, "r_max": 15.0}),
+    # workload 4's masks and sampling, distances only
+    12: Workload(12, "edt3d_2x256x256x256_aniso_dist", 2, (256, 256, 256), "bernoulli_bg",
+                 {"p_bg": 0.01, "at_least_one": False}, (2.5, 0.8, 0.8), False, seed_key=4),
+    # a 3-D shape off the 128^3 / 64^3 plane path: the headline structure at 256^3
+    13: Workload(13, "edt3d_2x256x256x256_balls", 2, (256, 256, 256), "balls_fg",
+                 {"count": 30, "r_min": 8.0, "r_max": 60.0}),
+    # the longest distances a sample can have: one background element per
+    # sample (uniform position), and one at the origin corner
+    14: Workload(14, "edt2d_8x1024x1024_single", 8, (1024, 1024), "single_bg", {}),
+    15: Workload(15, "edt3d_2x256x256x256_corner", 2, (256, 256, 256), "corner_bg", {}),
 }
 
 
@@ -117,7 +132,7 @@ def _balls(rng, spatial, count, r_min, r_max, scale):
 def sample_mask(w: Workload, b: int, spatial=None) -> np.ndarray:
     """Mask of sample `b` (uint8, nonzero = foreground) at `spatial` (default: full size)."""
     spatial = tuple(w.spatial if spatial is None else spatial)
-    rng = np.random.default_rng([SEED, w.key, b])
+    rng = np.random.default_rng([SEED, w.key if w.seed_key is None else w.seed_key, b])
     scale = min(spatial) / min(w.spatial)
     if w.kind == "bernoulli_fg":
         fg = rng.random(spatial) < w.param["p_fg"]
@@ -131,6 +146,12 @@ def sample_mask(w: Workload, b: int, spatial=None) -> np.ndarray:
         fg = ~_balls(rng, spatial, w.param["count"], w.param["r_min"], w.param["r_max"], scale)
     elif w.kind == "balls_fg":
         fg = _balls(rng, spatial, w.param["count"], w.param["r_min"], w.param["r_max"], scale)
+    elif w.kind == "single_bg":
+        fg = np.ones(spatial, dtype=bool)
+        fg[tuple(int(rng.integers(0, n)) for n in spatial)] = False
+    elif w.kind == "corner_bg":
+        fg = np.ones(spatial, dtype=bool)
+        fg[(0,) * len(spatial)] = False
     else:
         raise ValueError(w.kind)
     return fg.astype(np.uint8)
