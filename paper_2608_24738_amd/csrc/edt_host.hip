@@ -723,9 +723,13 @@ int run(Request &r) {
                      : launch(nm, k_line_search<M, F, W, 1, S>, lgrid, lblock, p.lds, r.stream, la))
             // lines of the exact transform keep to 8 or 4 per workgroup (the
             // planner sends longer ones to the envelope kernels)
-#define TM_LS(M, F, W)                                                                                  \
-    (p.ls_lpw == 8 ? launch(nm, k_line_search<M, F, W, 8>, lgrid, lblock, p.lds, r.stream, la)         \
-                   : launch(nm, k_line_search<M, F, W, 4>, lgrid, lblock, p.lds, r.stream, la))
+            // lines of at least kLsDirectMinRows take the few-site path
+#define TM_LS(M, F, W)                                                                                            \
+    (n >= kLsDirectMinRows                                                                                         \
+         ? (p.ls_lpw == 8 ? launch(nm, k_line_search<M, F, W, 8, false, true>, lgrid, lblock, p.lds, r.stream, la) \
+                          : launch(nm, k_line_search<M, F, W, 4, false, true>, lgrid, lblock, p.lds, r.stream, la)) \
+         : (p.ls_lpw == 8 ? launch(nm, k_line_search<M, F, W, 8>, lgrid, lblock, p.lds, r.stream, la)              \
+                          : launch(nm, k_line_search<M, F, W, 4>, lgrid, lblock, p.lds, r.stream, la)))
             if (r.sgn) {
                 nm = fin ? "line_search_signed_final" : "line_search_signed";
                 rc = fin ? TM_LS4(kL2, true, false, true) : TM_LS4(kL2, false, false, true);

@@ -23,6 +23,14 @@
 // straight to global memory: the staged copy is what every search reads, and
 // no other workgroup reads these lines.  Fewer lines per workgroup give more
 // workgroups when there are few lines.
+//
+// A workgroup whose lines all hold at most kLsDirect sites (rows holding a
+// value) skips the search: each element takes the minimum over its line's
+// site rows directly, at the cost of the site count instead of the distance
+// (which on such lines can reach the line length).  Every other row holds
+// "no site", so the minimum is the same.  The choice is per workgroup, and
+// the path is compiled in only where the host asks for it (DIRECT, long
+// lines): on short dense lines its mere presence slowed the search.
 #pragma once
 
 #include "edt_fh.h"
@@ -32,6 +40,8 @@ namespace tmedt {
 constexpr int kLsWaves = 16;
 constexpr int kLsUnroll = 8;     // search steps between stop votes
 constexpr int kLsGuard = kLsUnroll;   // guard rows of "no site" per side
+constexpr int kLsDirect = 32;    // lines with at most this many sites take the direct minimum
+constexpr uint32_t kLsDirectMinRows = 512;   // ... when they are at least this long
 
 struct LineSearchArgs {
     int32_t *buf;          // int32 field, batch-flat, in place (kInfI = no site)
@@ -67,6 +77,28 @@ __device__ __forceinline__ bool ls_stop(uint32_t best, int d) {
     else return best <= uint32_t(d);
 }
 
+// Minimum over the site rows sr[0 .. nsites) of line j of the tile for row
+// q (0 when the line has no site: the caller writes "none").
+template <int METRIC, bool W16, int LPW, typename T>
+__device__ __attribute__((noinline)) uint32_t ls_direct_min(const T *row0, const uint16_t *sr, uint32_t nsites,
+                                                            int j, int q) {
+    if (nsites == 0u) return 0u;
+    const T *col = row0 + j;
+    uint32_t best = uint32_t(col[q * LPW]);
+    for (uint32_t k0 = 0; k0 < nsites; k0 += 4) {
+        uint32_t m[4];
+        int rr[4];
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) {
+            rr[s2] = sr[min(k0 + uint32_t(s2), nsites - 1u)];
+            m[s2] = uint32_t(col[rr[s2] * LPW]);
+        }
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) best = min(best, ls_cand<METRIC, W16>(m[s2], abs(q - rr[s2])));
+    }
+    return best;
+}
+
 // SIGNED (euclidean, 32-bit tile): the field is the signed transform's, +F
 // on foreground and -F on background (see k_scan_signed).  The tile keeps
 // the class in bit 31 above |F|; for an element of class c, rows of its own
@@ -75,15 +107,17 @@ __device__ __forceinline__ bool ls_stop(uint32_t best, int d) {
 // repeat the end rows of the line (a repeated row read at a larger distance
 // than its own only overestimates), since no single word reads as "no site"
 // for both classes.
-template <int METRIC, bool FINAL, bool W16, int LPW, bool SIGNED = false>
+template <int METRIC, bool FINAL, bool W16, int LPW, bool SIGNED = false, bool DIRECT = false>
 __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs a) {
+    static_assert(!(SIGNED && DIRECT), "the signed field has no few-site lines");
     static_assert(!SIGNED || (METRIC == kL2 && !W16), "signed transform: euclidean, 32-bit tile");
     using T = typename std::conditional<W16, uint16_t, uint32_t>::type;
     constexpr uint32_t NONE = W16 ? 0xffffu : 0xffffffffu;
     constexpr int RPW = kWave / LPW;                 // rows per wave and step
     constexpr int STEP = kLsWaves * RPW;             // row step of one lane
     extern __shared__ __attribute__((aligned(16))) uint8_t ls_lds[];
-    __shared__ uint32_t has_site[LPW];
+    __shared__ uint32_t has_site[LPW];       // sites on the line
+    __shared__ uint16_t site_row[LPW][kLsDirect];
     T *tile = reinterpret_cast<T *>(ls_lds);
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
@@ -136,12 +170,40 @@ __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs
             if (q < n) {
                 if (SIGNED) row0[q * LPW + j] = v[s] < 0 ? (0x80000000u | uint32_t(-v[s])) : uint32_t(v[s]);
                 else row0[q * LPW + j] = v[s] == kInfI ? T(NONE) : T(v[s]);
-                seen |= v[s] != kInfI ? 1u : 0u;
+                if (DIRECT) seen += v[s] != kInfI ? 1u : 0u;
+                else seen |= v[s] != kInfI ? 1u : 0u;
             }
         }
     }
-    if (seen) atomicOr(&has_site[j], 1u);
+    // sites per line: the lanes of a wave holding the same line (l, l + LPW,
+    // ...) add up their counts, one LDS atomic per line and wave
+    if constexpr (DIRECT) {
+#pragma unroll
+        for (int m = LPW; m < kWave; m <<= 1) seen += uint32_t(__shfl_xor(int(seen), m, kWave));
+        if (lane < LPW && seen) atomicAdd(&has_site[j], seen);
+    } else {
+        if (seen) atomicOr(&has_site[j], 1u);
+    }
     __syncthreads();
+    // A workgroup whose lines all have at most kLsDirect sites (uniform test)
+    // takes the direct minimum: wave w lists the site rows of line w, 64 rows
+    // per ballot.
+    bool few = DIRECT;
+#pragma unroll
+    for (int k = 0; k < LPW; ++k) few &= has_site[k] <= uint32_t(kLsDirect);
+    if (few && wv < LPW && has_site[wv] != 0u) {
+        const T *colw = row0 + wv;
+        uint32_t cnt = 0;
+        for (int qb = 0; qb < n; qb += kWave) {
+            const int q = qb + lane;
+            const bool site = q < n && uint32_t(colw[q * LPW]) < NONE;
+            const uint64_t b = __ballot(site);
+            const uint32_t pos = cnt + uint32_t(__builtin_popcountll(b & ((uint64_t(1) << lane) - 1)));
+            if (site && pos < uint32_t(kLsDirect)) site_row[wv][pos] = uint16_t(q);
+            cnt += uint32_t(__builtin_popcountll(b));
+        }
+    }
+    if (few) __syncthreads();
     if (SIGNED) {
         for (int k = t; k < kLsGuard * LPW; k += kWave * kLsWaves) {
             tile[k] = row0[k % LPW];
@@ -151,7 +213,44 @@ __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs
     }
     const bool has = SIGNED || has_site[j] != 0u;
 
+
+    // result of row q of this lane's line from its minimum `best`
+    auto out = [&](int q, uint32_t best, uint32_t cq) {
+        const uint64_t e = base + uint64_t(q) * a.inner;
+        if (SIGNED) {
+            const bool none = best >= uint32_t(kInfI);     // one class in the whole sample
+            if (!FINAL) {
+                const int32_t v = none ? kInfI : int32_t(best);
+                a.buf[e] = cq ? -v : v;
+            } else {
+                const int64_t v = none ? virtual_sq<int64_t>(q, i, a.ndim, a.shape, a.wall) : int64_t(best);
+                const float dv = v < (int64_t(1) << 24) ? sqrt_rn_int(uint32_t(v)) : float(sqrt(double(v)));
+                a.dist[e] = cq ? -dv : dv;
+            }
+        } else if (!FINAL) {
+            a.buf[e] = has ? int32_t(best) : kInfI;
+        } else if (METRIC != kL2) {
+            a.buf[e] = has ? int32_t(best) : -1;       // chamfer: nothing reachable
+        } else {
+            int64_t v;
+            if (has) v = int64_t(best);
+            else v = virtual_sq<int64_t>(q, i, a.ndim, a.shape, a.wall);   // no background
+            const float dv = v < (int64_t(1) << 24) ? sqrt_rn_int(uint32_t(v)) : float(sqrt(double(v)));
+            if (a.dist) a.dist[e] = dv;
+            if (a.sq) a.sq[e] = int32_t(v);
+        }
+    };
     // ---- search and output --------------------------------------------------
+    if (few) {
+        // minimum over the line's site rows, out of line so that the search
+        // loop below is compiled as if this path did not exist
+        for (int qw = wv * RPW; qw < n; qw += STEP) {
+            const int q = qw + sub;
+            if (!(live && q < n)) continue;
+            out(q, ls_direct_min<METRIC, W16, LPW>(row0, site_row[j], has_site[j], j, q), 0u);
+        }
+        return;
+    }
     for (int qw = wv * RPW; qw < n; qw += STEP) {      // wave-uniform
         const int q = qw + sub;
         const bool mine = live && q < n;
@@ -181,44 +280,22 @@ __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs
             for (int s = 0; s < kLsUnroll; ++s)
                 best = min(best, ls_cand<METRIC, W16>(min(offer(u[s]), offer(w[s])), d + s));
         };
+        auto stop_all = [&](int dd) { return __all(ls_stop<METRIC>(best, dd)); };
         uint32_t ua[kLsUnroll], wa[kLsUnroll], ub[kLsUnroll], wb[kLsUnroll];
         int d = 1;
         read(d, ua, wa);
         // every row has been examined once d passes n
-        while (!__all(ls_stop<METRIC>(best, d))) {
+        while (!stop_all(d)) {
             read(d + kLsUnroll, ub, wb);
             fold(d, ua, wa);
             d += kLsUnroll;
-            if (d > n || __all(ls_stop<METRIC>(best, d))) break;
+            if (d > n || stop_all(d)) break;
             read(d + kLsUnroll, ua, wa);
             fold(d, ub, wb);
             d += kLsUnroll;
             if (d > n) break;
         }
-        if (!mine) continue;
-        const uint64_t e = base + uint64_t(q) * a.inner;
-        if (SIGNED) {
-            const bool none = best >= uint32_t(kInfI);     // one class in the whole sample
-            if (!FINAL) {
-                const int32_t v = none ? kInfI : int32_t(best);
-                a.buf[e] = cq ? -v : v;
-            } else {
-                const int64_t v = none ? virtual_sq<int64_t>(q, i, a.ndim, a.shape, a.wall) : int64_t(best);
-                const float dv = v < (int64_t(1) << 24) ? sqrt_rn_int(uint32_t(v)) : float(sqrt(double(v)));
-                a.dist[e] = cq ? -dv : dv;
-            }
-        } else if (!FINAL) {
-            a.buf[e] = has ? int32_t(best) : kInfI;
-        } else if (METRIC != kL2) {
-            a.buf[e] = has ? int32_t(best) : -1;       // chamfer: nothing reachable
-        } else {
-            int64_t v;
-            if (has) v = int64_t(best);
-            else v = virtual_sq<int64_t>(q, i, a.ndim, a.shape, a.wall);   // no background
-            const float dv = v < (int64_t(1) << 24) ? sqrt_rn_int(uint32_t(v)) : float(sqrt(double(v)));
-            if (a.dist) a.dist[e] = dv;
-            if (a.sq) a.sq[e] = int32_t(v);
-        }
+        if (mine) out(q, best, cq);
     }
 }
 

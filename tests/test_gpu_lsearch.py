@@ -1,8 +1,9 @@
-"""GPU parity of the whole-line windowed search (lines longer than the paired
-16-bit tile takes), at grid sizes around the 32-workgroup sets that the
-XCD-aware line-group order permutes: below 32, one full set plus a ragged
-tail, and whole sets.  Squared distances and distances must equal the
-oracle's bit for bit; the kernel names show that the line search ran."""
+"""GPU parity of the whole-line passes (lines longer than the paired 16-bit
+tile takes: the windowed search, with the direct minimum where a line
+has few sites), at grid sizes around the 32-workgroup sets that the XCD-aware
+line-group order permutes: below 32, one full set plus a ragged tail, and
+whole sets.  Squared distances and distances must equal the oracle's bit for
+bit; the kernel names show that a whole-line pass ran."""
 import numpy as np
 import pytest
 
