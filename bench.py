@@ -188,8 +188,10 @@ def time_op(step, args, stream):
     per = {}
     for name, t in binding.prof_read():
         per.setdefault(name, []).append(t)
+    shapes = dict(binding.prof_launches())
     binding.prof_enable(0)
-    kernels = {k: {"avg_ms": sum(v) / len(v), "launches": len(v)} for k, v in per.items()}
+    kernels = {k: {"avg_ms": sum(v) / len(v), "launches": len(v), "launch": shapes.get(k)}
+               for k, v in per.items()}
     return ms, kernels
 
 

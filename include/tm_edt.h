@@ -115,6 +115,11 @@ const char *tm_strerror(int status);
 int tm_prof_enable(int max_kernels);
 int tm_prof_count(void);
 int tm_prof_read(int i, const char **name, float *ms);
+/* Launch shape of timed kernel i: info[0..5] = workgroups, threads per
+ * workgroup, dynamic LDS bytes, static LDS bytes, registers per thread and
+ * private (scratch) bytes per thread as the HIP runtime reports them (-1 if
+ * it cannot).  Returns TM_OK or TM_ERR_SHAPE. */
+int tm_prof_launch(int i, int64_t *info);
 
 /* Metrics of the brute-force transform (paper, Section 2.3.2). */
 typedef enum {

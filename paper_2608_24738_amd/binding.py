@@ -63,6 +63,8 @@ def load() -> ctypes.CDLL:
             lib.tm_prof_read.restype = i32
             lib.tm_prof_read.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p),
                                          ctypes.POINTER(ctypes.c_float)]
+            lib.tm_prof_launch.restype = i32
+            lib.tm_prof_launch.argtypes = [i32, ctypes.POINTER(ctypes.c_int64)]
             lib.tm_selftest_host.restype = i32
             lib.tm_selftest_host.argtypes = []
             lib.tm_mask_nonzero.restype = i32
@@ -402,6 +404,23 @@ def prof_enable(max_kernels: int) -> None:
     rc = load().tm_prof_enable(int(max_kernels))
     if rc != TM_OK:
         raise TMError(rc, "tm_prof_enable")
+
+
+def prof_launches() -> list:
+    """[(kernel name, {workgroups, threads, lds_dynamic, lds_static, regs, scratch})]
+    for every kernel timed since prof_enable."""
+    lib = load()
+    out = []
+    keys = ("workgroups", "threads", "lds_dynamic", "lds_static", "regs", "scratch")
+    for i in range(lib.tm_prof_count()):
+        name = ctypes.c_char_p()
+        rc = lib.tm_prof_read(i, ctypes.byref(name), None)
+        info = (ctypes.c_int64 * 6)()
+        rc = rc or lib.tm_prof_launch(i, info)
+        if rc != TM_OK:
+            raise TMError(rc, "tm_prof_launch")
+        out.append((name.value.decode(), dict(zip(keys, list(info)))))
+    return out
 
 
 def prof_read() -> list:

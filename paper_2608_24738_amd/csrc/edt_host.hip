@@ -16,6 +16,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <array>
 #include <atomic>
 #include <cmath>
 #include <mutex>
@@ -47,6 +48,9 @@ struct Prof {
     std::atomic<int> next{0};
     std::vector<hipEvent_t> start, stop;
     std::vector<const char *> names;
+    // per launch: workgroups, threads per workgroup, dynamic LDS bytes,
+    // static LDS bytes, registers per thread, private (scratch) bytes per thread
+    std::vector<std::array<int64_t, 6>> info;
 };
 Prof &prof() {
     static Prof p;
@@ -81,6 +85,13 @@ int launch(const char *name, K kernel, dim3 grid, dim3 block, size_t lds, hipStr
            const Args &args) {
     if (allow_lds(kernel, lds) != hipSuccess) return TM_ERR_HIP;
     int slot = prof_begin(name, s);
+    if (slot >= 0) {
+        hipFuncAttributes fa{};
+        const bool ok = hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(kernel)) == hipSuccess;
+        prof().info[slot] = {int64_t(grid.x) * grid.y * grid.z, int64_t(block.x) * block.y * block.z,
+                             int64_t(lds), ok ? int64_t(fa.sharedSizeBytes) : -1,
+                             ok ? int64_t(fa.numRegs) : -1, ok ? int64_t(fa.localSizeBytes) : -1};
+    }
     hipLaunchKernelGGL(kernel, grid, block, lds, s, args);
     hipError_t e = hipGetLastError();
     prof_end(slot, s);
@@ -1025,6 +1036,7 @@ extern "C" int tm_prof_enable(int max_kernels) {
     p.start.resize(max_kernels);
     p.stop.resize(max_kernels);
     p.names.assign(max_kernels, nullptr);
+    p.info.assign(max_kernels, {});
     for (int k = 0; k < max_kernels; ++k) {
         if (hipEventCreate(&p.start[k]) != hipSuccess || hipEventCreate(&p.stop[k]) != hipSuccess) {
             p.start.resize(k);
@@ -1047,6 +1059,13 @@ extern "C" int tm_prof_read(int i, const char **name, float *ms) {
     if (i < 0 || i >= tm_prof_count()) return TM_ERR_SHAPE;
     if (name) *name = p.names[i];
     if (ms && hipEventElapsedTime(ms, p.start[i], p.stop[i]) != hipSuccess) return TM_ERR_HIP;
+    return TM_OK;
+}
+
+extern "C" int tm_prof_launch(int i, int64_t *info) {
+    Prof &p = prof();
+    if (i < 0 || i >= tm_prof_count() || !info) return TM_ERR_SHAPE;
+    for (int k = 0; k < 6; ++k) info[k] = p.info[i][k];
     return TM_OK;
 }
 
