@@ -71,6 +71,10 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
         return total * (1 + out_bytes)
     if base == "scan_signed":                # mask in, signed field out
         return total * (1 + 4)
+    if base == "col_scan_signed":            # mask in, class and axis-0 distance as one byte out
+        return total * (1 + 1)
+    if base == "plane_signed_final":         # those bytes in, signed distances out
+        return total * (1 + out_bytes)
     if base in ("fh_field", "tile_pair", "cdt_pair", "cdt_line", "cdt_none",
                 "line_search", "line_search_signed"):
         return total * (fin + fout)

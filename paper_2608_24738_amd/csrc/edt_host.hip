@@ -34,6 +34,7 @@
 #include "edt_small.h"
 #include "edt_mask.h"
 #include "edt_long.h"
+#include "edt_psigned.h"
 
 using namespace tmedt;
 
@@ -301,6 +302,32 @@ int run_plane(Request &r, uint64_t total, uint64_t vox) {
                   lds, r.stream, tg);
 }
 
+// Plane order for the signed transform of rank-3 inputs of 128 x 128 planes
+// (n0 <= 128): the axis-0 scan of both classes (k_col_scan_signed, straight
+// from the mask), then one workgroup per plane for the last two axes
+// (k_plane_signed).  Returns kNotPlane, before any launch, when the input
+// does not qualify.
+int run_plane_signed(Request &r, uint64_t total, uint64_t vox) {
+    if (r.ndim != 3 || r.shape[1] != uint32_t(kPsN) || r.shape[2] != uint32_t(kPsN) || r.shape[0] > 128)
+        return kNotPlane;
+    if (uintptr_t(r.in) % 2 != 0 || uintptr_t(r.dist) % 16 != 0) return kNotPlane;
+    ColArgs c{};
+    c.mask = r.in;
+    c.buf = reinterpret_cast<int32_t *>(r.dist);
+    c.n0 = r.shape[0];
+    c.S = uint32_t(vox / r.shape[0]);
+    c.blocks = uint32_t(c.S / kColBlock);
+    c.div_blocks = Div32::make(c.blocks);
+    const dim3 cgrid(uint32_t(total / (uint64_t(c.n0) * kColBlock))), cblock(kWave * kColWaves);
+    int rc = launch("col_scan_signed", k_col_scan_signed, cgrid, cblock, 0, r.stream, c);
+    if (rc != TM_OK) return rc;
+    PlaneSignedArgs ps{};
+    ps.out = r.dist;
+    ps.n0 = r.shape[0];
+    return launch("plane_signed_final", k_plane_signed, dim3(uint32_t(total / (kPsN * kPsN))), dim3(kPsThreads), kPsLds,
+                  r.stream, ps);
+}
+
 // Plan of every strided pass, axis nd-2 down to 0, before anything is
 // launched.  index_path: the index carrier (flat index of the nearest
 // background element); otherwise the field carrier (unit squared distances).
@@ -462,6 +489,10 @@ int run(Request &r) {
     }
     if (!r.idx && r.unit && !r.big && r.metric == kL2 && !r.sgn) {
         const int rc = run_plane(r, total, vox);
+        if (rc != kNotPlane) return rc;
+    }
+    if (r.sgn) {
+        const int rc = run_plane_signed(r, total, vox);
         if (rc != kNotPlane) return rc;
     }
 

@@ -1,0 +1,333 @@
+// edt_psigned.h -- plane-ordered signed transform EDT(M) - EDT(not M) for
+// rank-3 inputs of 128 x 128 planes (paper, Sections 1 and 2.3.2: the
+// boundary-loss field, one 1-D pass per axis).
+//
+// For a query of class c the separable passes minimise, over the elements r
+// of a line, the value that r offers to class c plus the squared distance
+// along the line: an element of the other class is a site (offers 0), an
+// element of class c offers what the earlier passes found for it.  Both
+// classes are carried side by side as a u16 pair per element,
+//     .x = offer to background queries,  .y = offer to foreground queries,
+// so one packed minimum serves both.
+//
+//   k_col_scan_signed: axis 0 straight from the mask.  Every element gets the
+//     distance along axis 0 to the nearest element of the other class (1 ..
+//     127, 0 when its column has none), stored with its class in one byte
+//     (class << 7 | distance) in the 8-bit plane layout: the 16384 elements of
+//     each 128 x 128 plane as bytes at the start of the plane's own 64 KiB of
+//     the output.
+//   k_plane_signed: one workgroup per plane.  It stages the bytes as u16 pairs
+//     (squares; an element offers 0 to the other class), searches along the
+//     plane's first axis, then along its second, and writes +sqrt to the
+//     foreground and -sqrt to the background, correctly rounded.  A sample
+//     holding one class only measures from the virtual element (-1, 0, 0).
+#pragma once
+
+#include "edt_fh.h"
+#include "edt_col.h"
+
+namespace tmedt {
+
+// ---------------------------------------------------------------------------
+// Axis 0: distance to the other class along each column, with the class.
+// A workgroup owns 128 adjacent columns of one sample and all n0 <= 128 rows;
+// lane l holds columns 2l and 2l+1 (one 2-byte mask load per row, both
+// columns in one register as a u16 pair), wave w rows [16w, 16w + 16).  The
+// waves exchange the first and last row of each class in their chunk through
+// LDS; every row then gets its distance to the nearest background row and to
+// the nearest foreground row above it from two saturating runs (one of them is
+// 0: the row's own class), and the same below.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(kWave * kColWaves) k_col_scan_signed(ColArgs a) {
+    // per wave and lane, u16 pairs (column 2l, column 2l+1): first row of each
+    // class in the chunk (0xffff: none) and last row + 1 (0: none)
+    __shared__ uint32_t first_b[kColWaves][kWave], last_b1[kColWaves][kWave];
+    __shared__ uint32_t first_f[kColWaves][kWave], last_f1[kColWaves][kWave];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const uint32_t sample = a.div_blocks.div(blockIdx.x);
+    const uint32_t blk = blockIdx.x - sample * a.blocks;
+    const uint64_t S = a.S;
+    const int n0 = int(a.n0);
+    const int r0 = wv * kColRows;
+    const int nr = max(0, min(kColRows, n0 - r0));
+    const uint64_t e_wave = uint64_t(sample) * uint64_t(n0) * S + uint64_t(r0) * S + uint64_t(blk) * kColBlock;
+    const uint32_t lcol = 2u * uint32_t(lane);
+    const __amdgpu_buffer_rsrc_t rin =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t *>(a.mask + e_wave), 0, 0x7fffffff, 0x00020000);
+    // f[j]: u16 pair, 0xffff where the column is foreground at row r0 + j;
+    // bit j of each half of m: the same
+    uint32_t f[kColRows];
+    uint32_t m = 0;
+    if (nr > 0) {
+        uint32_t xr[kColRows];
+#pragma unroll
+        for (int j = 0; j < kColRows; ++j)
+            xr[j] = __builtin_amdgcn_raw_buffer_load_b16(rin, lcol, uint32_t(min(j, nr - 1)) * uint32_t(S), 0);
+#pragma unroll
+        for (int j = 0; j < kColRows; ++j) {
+            uint32_t t = __builtin_amdgcn_perm(0u, xr[j], 0x0c010c00u);
+            __asm__("" : "+v"(t));
+            const col_i16x2 neg = __builtin_bit_cast(col_i16x2, col_u16x2{0, 0} - col_pair(t));
+            f[j] = __builtin_bit_cast(uint32_t, neg >> col_i16x2{15, 15});
+            m |= (f[j] & 0x00010001u) << j;
+        }
+    }
+    {
+        const uint32_t vm = (1u << nr) - 1u;       // rows of the chunk, per half
+        const uint32_t f0 = m & vm, f1 = (m >> 16) & vm;
+        const uint32_t b0 = ~m & vm, b1 = (~m >> 16) & vm;
+        auto first_of = [&](uint32_t x) { return x ? uint32_t(r0) + __builtin_ctz(x) : 0xffffu; };
+        auto last1_of = [&](uint32_t x) { return x ? uint32_t(r0) + 32u - __builtin_clz(x) : 0u; };
+        first_b[wv][lane] = first_of(b0) | (first_of(b1) << 16);
+        last_b1[wv][lane] = last1_of(b0) | (last1_of(b1) << 16);
+        first_f[wv][lane] = first_of(f0) | (first_of(f1) << 16);
+        last_f1[wv][lane] = last1_of(f0) | (last1_of(f1) << 16);
+    }
+    __syncthreads();
+    if (nr == 0) return;
+
+    // last row + 1 of each class above the chunk, first row below it
+    col_u16x2 upb = col_u16x2{0, 0}, upf = col_u16x2{0, 0};
+    col_u16x2 dnb = col_u16x2{0xffff, 0xffff}, dnf = col_u16x2{0xffff, 0xffff};
+#pragma unroll
+    for (int w = 0; w < kColWaves; ++w) {
+        if (w < wv) {
+            upb = __builtin_elementwise_max(upb, col_pair(last_b1[w][lane]));
+            upf = __builtin_elementwise_max(upf, col_pair(last_f1[w][lane]));
+        } else if (w > wv) {
+            dnb = __builtin_elementwise_min(dnb, col_pair(first_b[w][lane]));
+            dnf = __builtin_elementwise_min(dnf, col_pair(first_f[w][lane]));
+        }
+    }
+    // Runs: rows since the last row of each class (0 at rows of that class;
+    // from 0x4000 when there is none), so at every row one of the two is 0
+    // and the other is the distance to the other class on that side.
+    const col_u16x2 big = col_u16x2{0x4000, 0x4000};
+    const col_u16x2 one = col_u16x2{1, 1};
+    const col_u16x2 zero = col_u16x2{0, 0};
+    const col_u16x2 none = col_u16x2{0xffff, 0xffff};
+    const col_u16x2 vr0 = col_u16x2{uint16_t(r0), uint16_t(r0)};
+    const col_u16x2 vend = col_u16x2{uint16_t(r0 + nr), uint16_t(r0 + nr)};
+    col_u16x2 bwb = __builtin_elementwise_min(__builtin_elementwise_sub_sat(dnb, vend), dnb == none ? big : none);
+    col_u16x2 bwf = __builtin_elementwise_min(__builtin_elementwise_sub_sat(dnf, vend), dnf == none ? big : none);
+    uint32_t dn[kColRows];
+#pragma unroll
+    for (int j = kColRows - 1; j >= 0; --j) {
+        if (j < nr) {
+            bwb = col_pair(col_word(__builtin_elementwise_add_sat(bwb, one)) & f[j]);
+            bwf = col_pair(col_word(__builtin_elementwise_add_sat(bwf, one)) & ~f[j]);
+        }
+        dn[j] = col_word(bwb) | col_word(bwf);
+    }
+    col_u16x2 fwb = __builtin_elementwise_max(__builtin_elementwise_sub_sat(vr0, upb), upb == zero ? big : zero);
+    col_u16x2 fwf = __builtin_elementwise_max(__builtin_elementwise_sub_sat(vr0, upf), upf == zero ? big : zero);
+    char *const out_wave = reinterpret_cast<char *>(a.buf) + plane8_offset(e_wave);
+    const __amdgpu_buffer_rsrc_t rout = __builtin_amdgcn_make_buffer_rsrc(out_wave, 0, 0x7fffffff, 0x00020000);
+#pragma unroll
+    for (int j = 0; j < kColRows; ++j) {
+        if (j < nr) {
+            fwb = col_pair(col_word(__builtin_elementwise_add_sat(fwb, one)) & f[j]);
+            fwf = col_pair(col_word(__builtin_elementwise_add_sat(fwf, one)) & ~f[j]);
+            const col_u16x2 d = __builtin_elementwise_min(col_pair(col_word(fwb) | col_word(fwf)), col_pair(dn[j]));
+            // a real distance is at most 127 (n0 <= 128); none (0x4000 and up) -> 128 -> 0
+            const uint32_t c = (col_word(__builtin_elementwise_min(d, col_u16x2{128, 128})) & 0x007f007fu) |
+                               (f[j] & 0x00800080u);
+            // rows are 4 S bytes apart in the plane layout (S is a multiple of 128 * 128)
+            __builtin_amdgcn_raw_buffer_store_b16(uint16_t(__builtin_amdgcn_perm(0u, c, 0x0c0c0200u)), rout, lcol,
+                                                  uint32_t(j) * uint32_t(S) * 4u, 0);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// The last two axes, one workgroup of 16 waves per 128 x 128 plane.
+//
+// Each element keeps one 16-bit value: the squared distance to the other
+// class found so far (from the axes already processed; 0xffff: none yet).
+// Along a line, the queries of one run (maximal stretch of one class) need
+// only the rows of that run and the two rows just outside it, which belong to
+// the other class and offer 0; every row beyond those is farther than they
+// are and offers at least 0.  So the tile is kept twice, two columns per
+// 32-bit word: U, read for rows before the query, where the last row of each
+// run offers 0, and W, read for rows after it, where the first row of each run
+// offers 0; every other row offers its own value.  A query of class c then
+// meets its own run's values and the exact boundary sites, while any row it
+// reads of the other class beyond its run offers a candidate at least as large
+// as the boundary site's, so no class test is needed in the search.  The
+// search runs over 16 x 16 patches (a lane: two adjacent lines, two adjacent
+// queries, sharing the reads of each block of four steps) until every value
+// of the wave is at most d^2; G guard rows of "no site" above and below the
+// tile keep a block's reads inside it.
+// ---------------------------------------------------------------------------
+constexpr int kPsWaves = 16;
+constexpr int kPsThreads = kWave * kPsWaves;
+constexpr int kPsN = 128;
+constexpr int kPsG = 4;             // guard rows on either side
+constexpr int kPsRS = 68;           // tile row stride in words: 8 x 8 lane patches read conflict-free
+constexpr int kPsRows = kPsN + 2 * kPsG;
+constexpr size_t kPsLds = size_t(2) * kPsRows * kPsRS * 4;
+
+struct PlaneSignedArgs {
+    float *out;            // batch-flat outputs; plane p's bytes at byte offset 65536 p
+    uint32_t n0;           // axis-0 extent
+};
+
+// u16 pair of the axis-0 bytes b0, b1 (class << 7 | distance, 0: none):
+// squared distances, 0xffff for none.
+__device__ __forceinline__ uint32_t ps_sq_pair(uint32_t b0, uint32_t b1) {
+    const uint32_t d0 = b0 & 127u, d1 = b1 & 127u;
+    return (d0 ? d0 * d0 : 0xffffu) | ((d1 ? d1 * d1 : 0xffffu) << 16);
+}
+
+// Halves of `v` whose bit in `z` (bit 0: low half, bit 1: high half) is set
+// become 0.
+__device__ __forceinline__ uint32_t ps_zero_halves(uint32_t v, uint32_t z) {
+    return v & ((z & 1u) ? 0xffff0000u : 0xffffffffu) & ((z & 2u) ? 0x0000ffffu : 0xffffffffu);
+}
+
+// Both queries (tile rows q and q + 1 of line pair `word`) of one lane: the
+// smallest value plus squared distance over the rows of U before and W after
+// each query.
+__device__ __forceinline__ void ps_search(const uint32_t *tU, const uint32_t *tW, int q, int word, u16x2 &bA,
+                                          u16x2 &bB) {
+    const int o = (q + kPsG) * kPsRS + word;
+    // own value: the larger of the two copies (at most one of them is a boundary
+    // 0, unless the run is one element long, where the neighbours give 1)
+    bA = __builtin_elementwise_max(__builtin_elementwise_max(as_pair(tU[o]), as_pair(tW[o])), splat(1));
+    bB = __builtin_elementwise_max(__builtin_elementwise_max(as_pair(tU[o + kPsRS]), as_pair(tW[o + kPsRS])), splat(1));
+    for (int d = 1; d < kPsN; d += 4) {
+        const u16x2 m = __builtin_elementwise_max(bA, bB);
+        if (__all(as_word(__builtin_elementwise_sub_sat(m, splat(d * d))) == 0)) break;
+        // rows q-d-3 .. q-d+1 of U and q+d .. q+d+4 of W; a block wholly past
+        // an end of the line reads guard rows and the end row, with distances
+        // larger than the true ones (candidates that only overestimate)
+        const int lo = max(q - d - 3, -kPsG) + kPsG;
+        const int hi = min(q + d, kPsN - 1) + kPsG;
+        const uint32_t *pu = tU + lo * kPsRS + word;
+        const uint32_t *pw = tW + hi * kPsRS + word;
+        u16x2 U[5], W[5];
+#pragma unroll
+        for (int k = 0; k < 5; ++k) {
+            U[k] = as_pair(pu[k * kPsRS]);
+            W[k] = as_pair(pw[k * kPsRS]);
+        }
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+            const u16x2 sq = splat((d + st) * (d + st));
+            bA = __builtin_elementwise_min(bA, __builtin_elementwise_add_sat(__builtin_elementwise_min(U[3 - st], W[st]), sq));
+            bB = __builtin_elementwise_min(bB, __builtin_elementwise_add_sat(__builtin_elementwise_min(U[4 - st], W[st + 1]), sq));
+        }
+    }
+}
+
+__global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) {
+    extern __shared__ __attribute__((aligned(16))) uint32_t ps_lds[];
+    uint32_t *const tU = ps_lds;
+    uint32_t *const tW = ps_lds + kPsRows * kPsRS;
+    __shared__ uint16_t cls16[kPsN][8];   // class bits of each row, 16 columns per entry
+    __shared__ uint16_t st16[kPsN][8];    // along the row: class differs from the column before
+    __shared__ uint16_t en16[kPsN][8];    // along the row: class differs from the column after
+    const int t = threadIdx.x;
+    const int lane = t & (kWave - 1);
+    const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
+    const uint32_t p = blockIdx.x;
+    float *const outp = a.out + uint64_t(p) * (kPsN * kPsN);
+
+    // ---- stage: thread t holds columns 16 (t & 7) .. + 15 of row t >> 3 -----------
+    const int sr = t >> 3, sg = t & 7;
+    uint32_t gv[8];
+    uint32_t cls;
+    {
+        const uint4 v = reinterpret_cast<const uint4 *>(outp)[t];
+        const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+        cls = 0;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const uint32_t b0 = (w4[k >> 1] >> (16 * (k & 1))) & 0xffu;
+            const uint32_t b1 = (w4[k >> 1] >> (16 * (k & 1) + 8)) & 0xffu;
+            gv[k] = ps_sq_pair(b0, b1);
+            cls |= ((b0 >> 7) | ((b1 >> 7) << 1)) << (2 * k);
+        }
+        cls16[sr][sg] = uint16_t(cls);
+        for (int i = t; i < 2 * 2 * kPsG * kPsRS; i += kPsThreads) {
+            const int tile = i / (2 * kPsG * kPsRS), k = i % (2 * kPsG * kPsRS);
+            const int row = k / kPsRS, col = k % kPsRS;
+            ps_lds[tile * kPsRows * kPsRS + (row < kPsG ? row : kPsN + row) * kPsRS + col] = 0xffffffffu;
+        }
+    }
+    __syncthreads();
+    {
+        // runs along the plane's first axis (columns): starts and ends
+        const uint32_t up = sr > 0 ? cls16[sr - 1][sg] : cls;
+        const uint32_t dn = sr < kPsN - 1 ? cls16[sr + 1][sg] : cls;
+        const uint32_t s1 = cls ^ up, e1 = cls ^ dn;
+        // runs along the second axis (rows)
+        const uint32_t lb = sg > 0 ? (cls16[sr][sg - 1] >> 15) & 1u : cls & 1u;
+        const uint32_t rb = sg < 7 ? cls16[sr][sg + 1] & 1u : (cls >> 15) & 1u;
+        st16[sr][sg] = uint16_t((cls ^ ((cls << 1) | lb)) & 0xffffu);
+        en16[sr][sg] = uint16_t((cls ^ ((cls >> 1) | (rb << 15))) & 0xffffu);
+        const int o = (sr + kPsG) * kPsRS + 8 * sg;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            tU[o + k] = ps_zero_halves(gv[k], (e1 >> (2 * k)) & 3u);
+            tW[o + k] = ps_zero_halves(gv[k], (s1 >> (2 * k)) & 3u);
+        }
+    }
+    __syncthreads();
+
+    // ---- search along the first axis: patches of 16 rows x 16 columns -------------
+    const int rho = lane >> 3, jw = lane & 7;
+    u16x2 rA[4], rB[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int pi = 4 * wv + i, pr = pi >> 3, pc = pi & 7;
+        ps_search(tU, tW, 16 * pr + 2 * rho, 8 * pc + jw, rA[i], rB[i]);
+    }
+    __syncthreads();
+    // results, transposed: tile row = column, word = pair of rows; boundaries of
+    // the runs along the rows
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int pi = 4 * wv + i, pr = pi >> 3, pc = pi & 7;
+        const int q = 16 * pr + 2 * rho, c0 = 16 * pc + 2 * jw;
+        const uint32_t sh = 2 * jw;
+        const uint32_t eA = (en16[q][pc] >> sh) & 3u, eB = (en16[q + 1][pc] >> sh) & 3u;
+        const uint32_t sA = (st16[q][pc] >> sh) & 3u, sB = (st16[q + 1][pc] >> sh) & 3u;
+        const uint32_t A = as_word(rA[i]), B = as_word(rB[i]);
+        // column c0: (row q, row q+1) = low halves; column c0+1: high halves
+        const uint32_t w0 = (A & 0xffffu) | (B << 16), w1 = (A >> 16) | (B & 0xffff0000u);
+        const int o = (c0 + kPsG) * kPsRS + 8 * pr + rho;
+        tU[o] = ps_zero_halves(w0, (eA & 1u) | ((eB & 1u) << 1));
+        tU[o + kPsRS] = ps_zero_halves(w1, (eA >> 1) | (eB & 2u));
+        tW[o] = ps_zero_halves(w0, (sA & 1u) | ((sB & 1u) << 1));
+        tW[o + kPsRS] = ps_zero_halves(w1, (sA >> 1) | (sB & 2u));
+    }
+    __syncthreads();
+
+    // ---- search along the second axis, then signed distances ----------------------
+    const uint32_t x0 = p % a.n0;        // the plane's position along axis 0
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int pi = 4 * wv + i, pr = pi >> 3, pc = pi & 7;
+        u16x2 fA, fB;
+        const int c = 16 * pr + 2 * rho;       // columns c, c + 1
+        const int r0 = 16 * pc + 2 * jw;       // rows r0, r0 + 1
+        ps_search(tU, tW, c, 8 * pc + jw, fA, fB);
+        auto value = [&](int r, int cc, uint32_t h) {
+            const bool fg = (cls16[r][cc >> 4] >> (cc & 15)) & 1u;
+            uint32_t d2 = h;
+            if (h == 0xffffu)   // one class in the whole sample: the virtual element (-1, 0, 0)
+                d2 = (x0 + 1) * (x0 + 1) + uint32_t(r * r) + uint32_t(cc * cc);
+            const float dv = sqrt_rn_int(d2);
+            return fg ? dv : -dv;
+        };
+        // fA = (row r0, row r0+1) at column c; fB the same at column c + 1
+        *reinterpret_cast<float2 *>(outp + r0 * kPsN + c) =
+            float2{value(r0, c, fA.x), value(r0, c + 1, fB.x)};
+        *reinterpret_cast<float2 *>(outp + (r0 + 1) * kPsN + c) =
+            float2{value(r0 + 1, c, fA.y), value(r0 + 1, c + 1, fB.y)};
+    }
+}
+
+}  // namespace tmedt
