@@ -61,9 +61,15 @@ __global__ void __launch_bounds__(kWave * kColWaves) k_col_scan_signed(ColArgs a
     uint32_t m = 0;
     if (nr > 0) {
         uint32_t xr[kColRows];
+        if (nr == kColRows) {
 #pragma unroll
-        for (int j = 0; j < kColRows; ++j)
-            xr[j] = __builtin_amdgcn_raw_buffer_load_b16(rin, lcol, uint32_t(min(j, nr - 1)) * uint32_t(S), 0);
+            for (int j = 0; j < kColRows; ++j)
+                xr[j] = __builtin_amdgcn_raw_buffer_load_b16(rin, lcol, uint32_t(j) * uint32_t(S), 0);
+        } else {
+#pragma unroll
+            for (int j = 0; j < kColRows; ++j)
+                xr[j] = __builtin_amdgcn_raw_buffer_load_b16(rin, lcol, uint32_t(min(j, nr - 1)) * uint32_t(S), 0);
+        }
 #pragma unroll
         for (int j = 0; j < kColRows; ++j) {
             uint32_t t = __builtin_amdgcn_perm(0u, xr[j], 0x0c010c00u);
@@ -107,37 +113,45 @@ __global__ void __launch_bounds__(kWave * kColWaves) k_col_scan_signed(ColArgs a
     const col_u16x2 one = col_u16x2{1, 1};
     const col_u16x2 zero = col_u16x2{0, 0};
     const col_u16x2 none = col_u16x2{0xffff, 0xffff};
-    const col_u16x2 vr0 = col_u16x2{uint16_t(r0), uint16_t(r0)};
-    const col_u16x2 vend = col_u16x2{uint16_t(r0 + nr), uint16_t(r0 + nr)};
-    col_u16x2 bwb = __builtin_elementwise_min(__builtin_elementwise_sub_sat(dnb, vend), dnb == none ? big : none);
-    col_u16x2 bwf = __builtin_elementwise_min(__builtin_elementwise_sub_sat(dnf, vend), dnf == none ? big : none);
-    uint32_t dn[kColRows];
-#pragma unroll
-    for (int j = kColRows - 1; j >= 0; --j) {
-        if (j < nr) {
-            bwb = col_pair(col_word(__builtin_elementwise_add_sat(bwb, one)) & f[j]);
-            bwf = col_pair(col_word(__builtin_elementwise_add_sat(bwf, one)) & ~f[j]);
-        }
-        dn[j] = col_word(bwb) | col_word(bwf);
-    }
-    col_u16x2 fwb = __builtin_elementwise_max(__builtin_elementwise_sub_sat(vr0, upb), upb == zero ? big : zero);
-    col_u16x2 fwf = __builtin_elementwise_max(__builtin_elementwise_sub_sat(vr0, upf), upf == zero ? big : zero);
     char *const out_wave = reinterpret_cast<char *>(a.buf) + plane8_offset(e_wave);
     const __amdgpu_buffer_rsrc_t rout = __builtin_amdgcn_make_buffer_rsrc(out_wave, 0, 0x7fffffff, 0x00020000);
+    // The row loops are instantiated for a full chunk (no per-row tests) and
+    // for a ragged last chunk.
+    auto runs = [&](auto full_tag) {
+        constexpr bool FULL = decltype(full_tag)::value;
+        const int rows = FULL ? kColRows : nr;
+        const col_u16x2 vr0 = col_u16x2{uint16_t(r0), uint16_t(r0)};
+        const col_u16x2 vend = col_u16x2{uint16_t(r0 + rows), uint16_t(r0 + rows)};
+        col_u16x2 bwb = __builtin_elementwise_min(__builtin_elementwise_sub_sat(dnb, vend), dnb == none ? big : none);
+        col_u16x2 bwf = __builtin_elementwise_min(__builtin_elementwise_sub_sat(dnf, vend), dnf == none ? big : none);
+        uint32_t dn[kColRows];
 #pragma unroll
-    for (int j = 0; j < kColRows; ++j) {
-        if (j < nr) {
-            fwb = col_pair(col_word(__builtin_elementwise_add_sat(fwb, one)) & f[j]);
-            fwf = col_pair(col_word(__builtin_elementwise_add_sat(fwf, one)) & ~f[j]);
-            const col_u16x2 d = __builtin_elementwise_min(col_pair(col_word(fwb) | col_word(fwf)), col_pair(dn[j]));
-            // a real distance is at most 127 (n0 <= 128); none (0x4000 and up) -> 128 -> 0
-            const uint32_t c = (col_word(__builtin_elementwise_min(d, col_u16x2{128, 128})) & 0x007f007fu) |
-                               (f[j] & 0x00800080u);
-            // rows are 4 S bytes apart in the plane layout (S is a multiple of 128 * 128)
-            __builtin_amdgcn_raw_buffer_store_b16(uint16_t(__builtin_amdgcn_perm(0u, c, 0x0c0c0200u)), rout, lcol,
-                                                  uint32_t(j) * uint32_t(S) * 4u, 0);
+        for (int j = kColRows - 1; j >= 0; --j) {
+            if (FULL || j < rows) {
+                bwb = col_pair(col_word(__builtin_elementwise_add_sat(bwb, one)) & f[j]);
+                bwf = col_pair(col_word(__builtin_elementwise_add_sat(bwf, one)) & ~f[j]);
+            }
+            dn[j] = col_word(bwb) | col_word(bwf);
         }
-    }
+        col_u16x2 fwb = __builtin_elementwise_max(__builtin_elementwise_sub_sat(vr0, upb), upb == zero ? big : zero);
+        col_u16x2 fwf = __builtin_elementwise_max(__builtin_elementwise_sub_sat(vr0, upf), upf == zero ? big : zero);
+#pragma unroll
+        for (int j = 0; j < kColRows; ++j) {
+            if (FULL || j < rows) {
+                fwb = col_pair(col_word(__builtin_elementwise_add_sat(fwb, one)) & f[j]);
+                fwf = col_pair(col_word(__builtin_elementwise_add_sat(fwf, one)) & ~f[j]);
+                const col_u16x2 d = __builtin_elementwise_min(col_pair(col_word(fwb) | col_word(fwf)), col_pair(dn[j]));
+                // a real distance is at most 127 (n0 <= 128); none (0x4000 and up) -> 128 -> 0
+                const uint32_t c = (col_word(__builtin_elementwise_min(d, col_u16x2{128, 128})) & 0x007f007fu) |
+                                   (f[j] & 0x00800080u);
+                // rows are 4 S bytes apart in the plane layout (S is a multiple of 128 * 128)
+                __builtin_amdgcn_raw_buffer_store_b16(uint16_t(__builtin_amdgcn_perm(0u, c, 0x0c0c0200u)), rout, lcol,
+                                                      uint32_t(j) * uint32_t(S) * 4u, 0);
+            }
+        }
+    };
+    if (nr == kColRows) runs(std::true_type{});
+    else runs(std::false_type{});
 }
 
 // ---------------------------------------------------------------------------
@@ -196,29 +210,48 @@ __device__ __forceinline__ void ps_search(const uint32_t *tU, const uint32_t *tW
     // 0, unless the run is one element long, where the neighbours give 1)
     bA = __builtin_elementwise_max(__builtin_elementwise_max(as_pair(tU[o]), as_pair(tW[o])), splat(1));
     bB = __builtin_elementwise_max(__builtin_elementwise_max(as_pair(tU[o + kPsRS]), as_pair(tW[o + kPsRS])), splat(1));
-    for (int d = 1; d < kPsN; d += 4) {
+    // Block at distance d reads rows q-d-3 .. q-d+1 of U and q+d .. q+d+4 of W
+    // (word indices lo, hi below).  A block wholly past an end of the line
+    // reads guard rows and the end row, with distances larger than the true
+    // ones (candidates that only overestimate): lo stops at tile row 0, hi at
+    // the tile row of the last line row.
+    // (LDS byte addresses: lo into U, hi into W).
+    constexpr uint32_t kStep = 4 * kPsRS * 4;       // four rows, in bytes
+    const uint32_t bu = lds_byte_addr(tU), bw = lds_byte_addr(tW);
+    const uint32_t lo_min = bu + 4 * word, hi_max = bw + 4 * ((kPsN - 1 + kPsG) * kPsRS + word);
+    int lo = int(bu) + 4 * (o - 4 * kPsRS);         // d = 1 (may pass below U: clamped)
+    uint32_t hi = bw + 4 * (o + kPsRS);
+    int d = 1;
+    do {
         const u16x2 m = __builtin_elementwise_max(bA, bB);
         if (__all(as_word(__builtin_elementwise_sub_sat(m, splat(d * d))) == 0)) break;
-        // rows q-d-3 .. q-d+1 of U and q+d .. q+d+4 of W; a block wholly past
-        // an end of the line reads guard rows and the end row, with distances
-        // larger than the true ones (candidates that only overestimate)
-        const int lo = max(q - d - 3, -kPsG) + kPsG;
-        const int hi = min(q + d, kPsN - 1) + kPsG;
-        const uint32_t *pu = tU + lo * kPsRS + word;
-        const uint32_t *pw = tW + hi * kPsRS + word;
+        const uint32_t lb = uint32_t(max(lo, int(lo_min))), hb = min(hi, hi_max);
         u16x2 U[5], W[5];
 #pragma unroll
         for (int k = 0; k < 5; ++k) {
-            U[k] = as_pair(pu[k * kPsRS]);
-            W[k] = as_pair(pw[k * kPsRS]);
+            U[k] = as_pair(lds_word(lb + 4 * k * kPsRS));
+            W[k] = as_pair(lds_word(hb + 4 * k * kPsRS));
+        }
+        u16x2 cA[4], cB[4];
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+            cA[st] = __builtin_elementwise_min(U[3 - st], W[st]);
+            cB[st] = __builtin_elementwise_min(U[4 - st], W[st + 1]);
         }
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
             const u16x2 sq = splat((d + st) * (d + st));
-            bA = __builtin_elementwise_min(bA, __builtin_elementwise_add_sat(__builtin_elementwise_min(U[3 - st], W[st]), sq));
-            bB = __builtin_elementwise_min(bB, __builtin_elementwise_add_sat(__builtin_elementwise_min(U[4 - st], W[st + 1]), sq));
+            cA[st] = __builtin_elementwise_add_sat(cA[st], sq);
+            cB[st] = __builtin_elementwise_add_sat(cB[st], sq);
         }
-    }
+        bA = __builtin_elementwise_min(
+            bA, __builtin_elementwise_min(__builtin_elementwise_min(cA[0], cA[1]), __builtin_elementwise_min(cA[2], cA[3])));
+        bB = __builtin_elementwise_min(
+            bB, __builtin_elementwise_min(__builtin_elementwise_min(cB[0], cB[1]), __builtin_elementwise_min(cB[2], cB[3])));
+        lo -= int(kStep);
+        hi += kStep;
+        d += 4;
+    } while (d < kPsN);
 }
 
 __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) {
