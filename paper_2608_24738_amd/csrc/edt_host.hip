@@ -34,7 +34,7 @@
 #include "edt_small.h"
 #include "edt_mask.h"
 #include "edt_long.h"
-#include "edt_psigned.h"
+#include "edt_plane.h"
 
 using namespace tmedt;
 
@@ -298,8 +298,16 @@ int run_plane(Request &r, uint64_t total, uint64_t vox) {
     const dim3 pgrid(uint32_t(total / P / kPairLines));
     if (P == 64)
         return launch("plane_final.i16", k_tile_pair<true, false, 8, kL2, 64>, pgrid, tblock, lds, r.stream, tg);
-    return launch(bytes ? "plane_final.i8" : "plane_final.i16", k_tile_pair<true, false, 8, kL2, 128>, pgrid, tblock,
-                  lds, r.stream, tg);
+    if (!bytes)
+        return launch("plane_final.i16", k_tile_pair<true, false, 8, kL2, 128>, pgrid, tblock, lds, r.stream, tg);
+    PlaneEdtArgs pe{};
+    pe.bytes = reinterpret_cast<const uint8_t *>(buf);
+    pe.dist = r.dist;
+    pe.sq = r.sq;
+    pe.n0 = r.shape[0];
+    constexpr int kEdtLut = 1024;
+    return launch("plane_final.i8", k_plane_edt<kEdtLut>, dim3(uint32_t(total / (kPsN * kPsN))), dim3(kPsThreads),
+                  2 * kPsTile + 4 * kEdtLut, r.stream, pe);
 }
 
 // Plane order for the signed transform of rank-3 inputs of 128 x 128 planes

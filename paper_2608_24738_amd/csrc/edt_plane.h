@@ -1,26 +1,26 @@
-// edt_psigned.h -- plane-ordered signed transform EDT(M) - EDT(not M) for
-// rank-3 inputs of 128 x 128 planes (paper, Sections 1 and 2.3.2: the
-// boundary-loss field, one 1-D pass per axis).
+// edt_plane.h -- the last two axes of rank-3 inputs of 128 x 128 planes in
+// one workgroup per plane, after a pass along axis 0 (paper, Section 2.3.2:
+// one 1-D pass per axis; the order of the axes changes no distance).
 //
-// For a query of class c the separable passes minimise, over the elements r
-// of a line, the value that r offers to class c plus the squared distance
-// along the line: an element of the other class is a site (offers 0), an
-// element of class c offers what the earlier passes found for it.  Both
-// classes are carried side by side as a u16 pair per element,
-//     .x = offer to background queries,  .y = offer to foreground queries,
-// so one packed minimum serves both.
+//   k_plane_edt: the exact transform (Section 2.3.2).  It reads the axis-0
+//     distances that k_col_scan leaves as bytes, searches along the plane's
+//     first axis, then along its second, and writes the distance and / or
+//     its square, correctly rounded, with the virtual element (-1, 0, 0) for
+//     samples without background.
+//   k_col_scan_signed + k_plane_signed: the signed transform EDT(M) -
+//     EDT(not M), the field of boundary losses (Section 1).  For a query of
+//     class c a line's minimum runs over what each element offers to class c
+//     plus the squared distance along the line: an element of the other class
+//     is a site (offers 0), an element of class c offers what the earlier
+//     axes found for it.  The axis-0 pass gives every element its distance
+//     along axis 0 to the other class (1 .. 127, 0 when its column has none)
+//     and its class, as one byte; the plane pass carries one value per
+//     element (the squared distance to the other class found so far) and
+//     writes +sqrt to the foreground and -sqrt to the background.
 //
-//   k_col_scan_signed: axis 0 straight from the mask.  Every element gets the
-//     distance along axis 0 to the nearest element of the other class (1 ..
-//     127, 0 when its column has none), stored with its class in one byte
-//     (class << 7 | distance) in the 8-bit plane layout: the 16384 elements of
-//     each 128 x 128 plane as bytes at the start of the plane's own 64 KiB of
-//     the output.
-//   k_plane_signed: one workgroup per plane.  It stages the bytes as u16 pairs
-//     (squares; an element offers 0 to the other class), searches along the
-//     plane's first axis, then along its second, and writes +sqrt to the
-//     foreground and -sqrt to the background, correctly rounded.  A sample
-//     holding one class only measures from the virtual element (-1, 0, 0).
+// Bytes travel in the 8-bit plane layout: the 16384 elements of each
+// 128 x 128 plane as bytes at the start of that plane's own 64 KiB of the
+// float32 output, which the plane pass overwrites after staging them.
 #pragma once
 
 #include "edt_fh.h"
@@ -157,22 +157,27 @@ __global__ void __launch_bounds__(kWave * kColWaves) k_col_scan_signed(ColArgs a
 // ---------------------------------------------------------------------------
 // The last two axes, one workgroup of 16 waves per 128 x 128 plane.
 //
-// Each element keeps one 16-bit value: the squared distance to the other
-// class found so far (from the axes already processed; 0xffff: none yet).
-// Along a line, the queries of one run (maximal stretch of one class) need
-// only the rows of that run and the two rows just outside it, which belong to
-// the other class and offer 0; every row beyond those is farther than they
-// are and offers at least 0.  So the tile is kept twice, two columns per
-// 32-bit word: U, read for rows before the query, where the last row of each
-// run offers 0, and W, read for rows after it, where the first row of each run
-// offers 0; every other row offers its own value.  A query of class c then
-// meets its own run's values and the exact boundary sites, while any row it
-// reads of the other class beyond its run offers a candidate at least as large
-// as the boundary site's, so no class test is needed in the search.  The
-// search runs over 16 x 16 patches (a lane: two adjacent lines, two adjacent
-// queries, sharing the reads of each block of four steps) until every value
-// of the wave is at most d^2; G guard rows of "no site" above and below the
-// tile keep a block's reads inside it.
+// The plane is staged as a tile of 16-bit values (two columns per 32-bit
+// word; 0xffff: no site yet), searched along its first axis, written back
+// transposed (two rows per word), and searched along its second axis.  The
+// search runs over 16 x 16 patches: a lane takes two adjacent lines (one
+// word) and two adjacent queries, whose candidates in each block of four
+// steps share ten reads, until every value of the wave is at most d^2.  G
+// guard rows of "no site" above and below the tile keep a block's reads
+// inside it.
+//
+// Signed transform: each element keeps the squared distance to the other
+// class found so far.  Along a line, the queries of one run (maximal stretch
+// of one class) need only the rows of that run and the two rows just outside
+// it, which belong to the other class and offer 0; every row beyond those is
+// farther than they are and offers at least 0.  So the tile is kept twice: U,
+// read for rows before the query, where the last row of each run offers 0,
+// and W, read for rows after it, where the first row of each run offers 0;
+// every other row offers its own value.  A query then meets its own run's
+// values and the exact boundary sites, while any row of the other class it
+// reads beyond its run offers a candidate at least as large as the boundary
+// site's, so the search needs no class test.  The exact transform uses one
+// tile for both (background offers 0).
 // ---------------------------------------------------------------------------
 constexpr int kPsWaves = 16;
 constexpr int kPsThreads = kWave * kPsWaves;
@@ -180,15 +185,14 @@ constexpr int kPsN = 128;
 constexpr int kPsG = 4;             // guard rows on either side
 constexpr int kPsRS = 68;           // tile row stride in words: 8 x 8 lane patches read conflict-free
 constexpr int kPsRows = kPsN + 2 * kPsG;
-constexpr size_t kPsLds = size_t(2) * kPsRows * kPsRS * 4;
+constexpr size_t kPsTile = size_t(kPsRows) * kPsRS * 4;
+constexpr size_t kPsLds = 2 * kPsTile;     // signed: U and W
 
 struct PlaneSignedArgs {
     float *out;            // batch-flat outputs; plane p's bytes at byte offset 65536 p
     uint32_t n0;           // axis-0 extent
 };
 
-// u16 pair of the axis-0 bytes b0, b1 (class << 7 | distance, 0: none):
-// squared distances, 0xffff for none.
 __device__ __forceinline__ uint32_t ps_sq_pair(uint32_t b0, uint32_t b1) {
     const uint32_t d0 = b0 & 127u, d1 = b1 & 127u;
     return (d0 ? d0 * d0 : 0xffffu) | ((d1 ? d1 * d1 : 0xffffu) << 16);
@@ -203,13 +207,21 @@ __device__ __forceinline__ uint32_t ps_zero_halves(uint32_t v, uint32_t z) {
 // Both queries (tile rows q and q + 1 of line pair `word`) of one lane: the
 // smallest value plus squared distance over the rows of U before and W after
 // each query.
+template <bool SIGNED>
 __device__ __forceinline__ void ps_search(const uint32_t *tU, const uint32_t *tW, int q, int word, u16x2 &bA,
                                           u16x2 &bB) {
     const int o = (q + kPsG) * kPsRS + word;
-    // own value: the larger of the two copies (at most one of them is a boundary
-    // 0, unless the run is one element long, where the neighbours give 1)
-    bA = __builtin_elementwise_max(__builtin_elementwise_max(as_pair(tU[o]), as_pair(tW[o])), splat(1));
-    bB = __builtin_elementwise_max(__builtin_elementwise_max(as_pair(tU[o + kPsRS]), as_pair(tW[o + kPsRS])), splat(1));
+    if constexpr (SIGNED) {
+        // own value: the larger of the two copies (at most one of them is a
+        // boundary 0, unless the run is one element long, where the
+        // neighbours give 1)
+        bA = __builtin_elementwise_max(__builtin_elementwise_max(as_pair(tU[o]), as_pair(tW[o])), splat(1));
+        bB = __builtin_elementwise_max(__builtin_elementwise_max(as_pair(tU[o + kPsRS]), as_pair(tW[o + kPsRS])),
+                                       splat(1));
+    } else {
+        bA = as_pair(tU[o]);
+        bB = as_pair(tU[o + kPsRS]);
+    }
     // Block at distance d reads rows q-d-3 .. q-d+1 of U and q+d .. q+d+4 of W
     // (word indices lo, hi below).  A block wholly past an end of the line
     // reads guard rows and the end row, with distances larger than the true
@@ -315,7 +327,7 @@ __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) 
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int pi = 4 * wv + i, pr = pi >> 3, pc = pi & 7;
-        ps_search(tU, tW, 16 * pr + 2 * rho, 8 * pc + jw, rA[i], rB[i]);
+        ps_search<true>(tU, tW, 16 * pr + 2 * rho, 8 * pc + jw, rA[i], rB[i]);
     }
     __syncthreads();
     // results, transposed: tile row = column, word = pair of rows; boundaries of
@@ -346,7 +358,7 @@ __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) 
         u16x2 fA, fB;
         const int c = 16 * pr + 2 * rho;       // columns c, c + 1
         const int r0 = 16 * pc + 2 * jw;       // rows r0, r0 + 1
-        ps_search(tU, tW, c, 8 * pc + jw, fA, fB);
+        ps_search<true>(tU, tW, c, 8 * pc + jw, fA, fB);
         auto value = [&](int r, int cc, uint32_t h) {
             const bool fg = (cls16[r][cc >> 4] >> (cc & 15)) & 1u;
             uint32_t d2 = h;
@@ -360,6 +372,118 @@ __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) 
             float2{value(r0, c, fA.x), value(r0, c + 1, fB.x)};
         *reinterpret_cast<float2 *>(outp + (r0 + 1) * kPsN + c) =
             float2{value(r0 + 1, c, fA.y), value(r0 + 1, c + 1, fB.y)};
+    }
+}
+
+
+// ---------------------------------------------------------------------------
+// Exact transform of one 128 x 128 plane per workgroup, from the axis-0
+// distances of k_col_scan (bytes: 0 .. 127, 255 for none).
+// ---------------------------------------------------------------------------
+struct PlaneEdtArgs {
+    const uint8_t *bytes;  // plane p's axis-0 bytes at byte offset 65536 p (inside dist or sq)
+    float *dist;           // batch-flat outputs (either may be null)
+    int32_t *sq;
+    uint32_t n0;           // axis-0 extent
+};
+
+// The waves claim the 64 patches of each search from a counter in LDS, so a
+// wave with light patches takes more of them and the waves reach the barrier
+// after each search together.  The first search writes its results straight
+// into a second tile, transposed (tile row = column, word = pair of rows),
+// which the second search reads.  LUT square roots in LDS.
+template <int LUT>
+__global__ void __launch_bounds__(kPsThreads, 8) k_plane_edt(PlaneEdtArgs a) {
+    extern __shared__ __attribute__((aligned(16))) uint32_t ps_lds[];
+    uint32_t *const tA = ps_lds;                       // axis-0 squares
+    uint32_t *const tB = ps_lds + kPsRows * kPsRS;     // after the first search, transposed
+    uint32_t *const lut = ps_lds + 2 * kPsRows * kPsRS;   // correctly rounded sqrt of 0 .. LUT-1
+    __shared__ uint32_t claim[2];                      // next patch of each search
+    const int t = threadIdx.x;
+    const int lane = t & (kWave - 1);
+    const uint32_t p = blockIdx.x;
+    const uint64_t pe = uint64_t(p) * (kPsN * kPsN);   // first element of the plane
+
+    // ---- stage: thread t holds columns 16 (t & 7) .. + 15 of row t >> 3 -----------
+    {
+        const uint4 v = *reinterpret_cast<const uint4 *>(a.bytes + uint64_t(p) * 65536u + 16u * uint32_t(t));
+        const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+        const int o = ((t >> 3) + kPsG) * kPsRS + 8 * (t & 7);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const uint32_t b0 = (w4[k >> 1] >> (16 * (k & 1))) & 0xffu;
+            const uint32_t b1 = (w4[k >> 1] >> (16 * (k & 1) + 8)) & 0xffu;
+            tA[o + k] = (b0 == 255u ? 0xffffu : b0 * b0) | ((b1 == 255u ? 0xffffu : b1 * b1) << 16);
+        }
+        for (int i = t; i < 2 * 2 * kPsG * kPsRS; i += kPsThreads) {
+            const int tile = i / (2 * kPsG * kPsRS), k = i % (2 * kPsG * kPsRS);
+            const int row = k / kPsRS, col = k % kPsRS;
+            ps_lds[tile * kPsRows * kPsRS + (row < kPsG ? row : kPsN + row) * kPsRS + col] = 0xffffffffu;
+        }
+        for (int i = t; i < LUT; i += kPsThreads) lut[i] = __builtin_bit_cast(uint32_t, sqrt_rn_int(uint32_t(i)));
+        if (t < 2) claim[t] = 0;
+    }
+    __syncthreads();
+
+    const int rho = lane >> 3, jw = lane & 7;
+    // next patch of search s for this wave (uniform), 64 when none is left
+    auto next_patch = [&](int s) {
+        uint32_t i = 0;
+        if (lane == 0) i = atomicAdd(&claim[s], 1u);
+        return __builtin_amdgcn_readfirstlane(i);
+    };
+
+    // ---- search along the first axis: patches of 16 rows x 16 columns -------------
+    for (uint32_t pi = next_patch(0); pi < 64; pi = next_patch(0)) {
+        const int pr = int(pi >> 3), pc = int(pi & 7);
+        u16x2 rA, rB;
+        ps_search<false>(tA, tA, 16 * pr + 2 * rho, 8 * pc + jw, rA, rB);
+        const int c0 = 16 * pc + 2 * jw;
+        const uint32_t A = as_word(rA), B = as_word(rB);
+        const int o = (c0 + kPsG) * kPsRS + 8 * pr + rho;
+        tB[o] = __builtin_amdgcn_perm(B, A, 0x05040100u);           // (A.lo, B.lo)
+        tB[o + kPsRS] = __builtin_amdgcn_perm(B, A, 0x07060302u);   // (A.hi, B.hi)
+    }
+    __syncthreads();
+
+    // ---- search along the second axis, then the outputs ---------------------------
+    const uint32_t x0 = p % a.n0;        // the plane's position along axis 0
+    for (uint32_t pi = next_patch(1); pi < 64; pi = next_patch(1)) {
+        const int pr = int(pi >> 3), pc = int(pi & 7);
+        u16x2 fA, fB;
+        const int c = 16 * pr + 2 * rho;       // columns c, c + 1
+        const int r0 = 16 * pc + 2 * jw;       // rows r0, r0 + 1
+        ps_search<false>(tB, tB, c, 8 * pc + jw, fA, fB);
+        // fA = (row r0, row r0+1) at column c; fB the same at column c + 1
+        uint32_t d2[4] = {fA.x, fB.x, fA.y, fB.y};   // (r0, c), (r0, c+1), (r0+1, c), (r0+1, c+1)
+        // no background in the whole sample (every value "none"): distances to
+        // the virtual element (-1, 0, 0)
+        const u16x2 mx = __builtin_elementwise_max(fA, fB);
+        if (__any(mx.x == 0xffffu || mx.y == 0xffffu)) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t r = uint32_t(r0 + (k >> 1)), cc = uint32_t(c + (k & 1));
+                if (d2[k] == 0xffffu) d2[k] = (x0 + 1) * (x0 + 1) + r * r + cc * cc;
+            }
+        }
+        const bool small = mx.x < uint32_t(LUT) && mx.y < uint32_t(LUT);
+        float dv[4];
+        if (__all(small)) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) dv[k] = __builtin_bit_cast(float, lut[d2[k]]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) dv[k] = sqrt_rn_int(d2[k]);
+        }
+        const uint64_t e0 = pe + uint64_t(r0) * kPsN + uint32_t(c), e1 = e0 + kPsN;
+        if (a.dist) {
+            *reinterpret_cast<float2 *>(a.dist + e0) = float2{dv[0], dv[1]};
+            *reinterpret_cast<float2 *>(a.dist + e1) = float2{dv[2], dv[3]};
+        }
+        if (a.sq) {
+            *reinterpret_cast<int2 *>(a.sq + e0) = int2{int32_t(d2[0]), int32_t(d2[1])};
+            *reinterpret_cast<int2 *>(a.sq + e1) = int2{int32_t(d2[2]), int32_t(d2[3])};
+        }
     }
 }
 
