@@ -227,8 +227,8 @@ bool plan_line_search(FhPlan &p, uint32_t n, uint64_t total, bool w16, int min_l
 // Plane order for distance outputs of unit-sampled rank-3 inputs whose last
 // two extents are both 128, or both 64 with an even number of planes per
 // sample: the axis-0 nearest-zero scan first (k_col_scan, straight from the
-// mask), then one workgroup per 128 lines of the last two axes (one
-// 128 x 128 plane or two 64 x 64 planes; k_tile_pair with PLANE).  Axis-0
+// mask), then one workgroup per 128 x 128 plane (k_plane_edt) or per two
+// 64 x 64 planes (k_tile_pair with PLANE) for the last two axes.  Axis-0
 // distances reach 128 x 128 planes as bytes, 64 x 64 planes as 16-bit
 // squares.  (Rank 4 would put the middle axes between the two kernels; on a
 // sparse 4-D input that order measured slower than the last-axis-first one,
@@ -276,30 +276,28 @@ int run_plane(Request &r, uint64_t total, uint64_t vox) {
                    : launch("col_scan.o16", k_col_scan<false>, cgrid, cblock, 0, r.stream, c);
     if (rc != TM_OK) return rc;
 
-    PairArgs tg{};
-    tg.buf = buf;
-    tg.total = uint32_t(total);
-    tg.dist = r.dist;
-    tg.sq = r.sq;
-    tg.ndim = nd;
-    tg.vox = uint32_t(vox);
-    for (int b = 0; b < nd; ++b) {
-        tg.shape[b] = r.shape[b];
-        tg.wall[b] = 1.0;
+    if (P == 64) {
+        PairArgs tg{};
+        tg.buf = buf;
+        tg.total = uint32_t(total);
+        tg.dist = r.dist;
+        tg.sq = r.sq;
+        tg.ndim = nd;
+        tg.vox = uint32_t(vox);
+        for (int b = 0; b < nd; ++b) {
+            tg.shape[b] = r.shape[b];
+            tg.wall[b] = 1.0;
+        }
+        tg.n = P;
+        tg.inner = P;
+        tg.div_inner = Div32::make(P);
+        tg.lines = uint32_t(total / P);
+        tg.out_seg = 0;
+        tg.in_seg = 1;
+        const size_t lds = size_t(P + 2 * kGuard16) * kRowW * 4;
+        return launch("plane_final.i16", k_tile_pair<true, false, 8, kL2, 64>, dim3(uint32_t(total / P / kPairLines)),
+                      dim3(kWave * kPairWaves), lds, r.stream, tg);
     }
-    const dim3 tblock(kWave * kPairWaves);
-    tg.n = P;
-    tg.inner = P;
-    tg.div_inner = Div32::make(P);
-    tg.lines = uint32_t(total / P);
-    tg.out_seg = 0;
-    tg.in_seg = bytes ? 2 : 1;
-    const size_t lds = size_t(P + 2 * kGuard16) * kRowW * 4;
-    const dim3 pgrid(uint32_t(total / P / kPairLines));
-    if (P == 64)
-        return launch("plane_final.i16", k_tile_pair<true, false, 8, kL2, 64>, pgrid, tblock, lds, r.stream, tg);
-    if (!bytes)
-        return launch("plane_final.i16", k_tile_pair<true, false, 8, kL2, 128>, pgrid, tblock, lds, r.stream, tg);
     PlaneEdtArgs pe{};
     pe.bytes = reinterpret_cast<const uint8_t *>(buf);
     pe.dist = r.dist;

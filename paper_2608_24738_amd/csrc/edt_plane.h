@@ -326,7 +326,7 @@ __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) 
     u16x2 rA[4], rB[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int pi = 4 * wv + i, pr = pi >> 3, pc = pi & 7;
+        const int pi = wv + kPsWaves * i, pr = pi >> 3, pc = pi & 7;
         ps_search<true>(tU, tW, 16 * pr + 2 * rho, 8 * pc + jw, rA[i], rB[i]);
     }
     __syncthreads();
@@ -334,7 +334,7 @@ __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) 
     // the runs along the rows
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int pi = 4 * wv + i, pr = pi >> 3, pc = pi & 7;
+        const int pi = wv + kPsWaves * i, pr = pi >> 3, pc = pi & 7;
         const int q = 16 * pr + 2 * rho, c0 = 16 * pc + 2 * jw;
         const uint32_t sh = 2 * jw;
         const uint32_t eA = (en16[q][pc] >> sh) & 3u, eB = (en16[q + 1][pc] >> sh) & 3u;
@@ -354,7 +354,7 @@ __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) 
     const uint32_t x0 = p % a.n0;        // the plane's position along axis 0
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int pi = 4 * wv + i, pr = pi >> 3, pc = pi & 7;
+        const int pi = wv + kPsWaves * i, pr = pi >> 3, pc = pi & 7;
         u16x2 fA, fB;
         const int c = 16 * pr + 2 * rho;       // columns c, c + 1
         const int r0 = 16 * pc + 2 * jw;       // rows r0, r0 + 1
