@@ -158,9 +158,13 @@ int tm_dt_bf(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch
  * virtual element (-1, 0, ..., 0) with that class's sign.  No element is
  * zero.  Unit sampling; float32 results, each the correctly rounded square
  * root of the exact integer squared distance with its sign.  The mask is
- * read once: one field carries +F on foreground and -F on background, and
- * every pass lets an element's own class offer values and the other class
- * offer sites.  in_u8, ndim, shape, batch as for tm_edt; out_dist: device
+ * read once: in every pass an element's own class offers the values found so
+ * far and the other class offers sites.  Rank-3 inputs of 128 x 128 planes
+ * with an axis-0 extent up to 128 run axis 0 first (class and distance to
+ * the other class as one byte per element, kept inside out_dist) and then
+ * one workgroup per plane; other shapes carry one field (+F on foreground,
+ * -F on background) through whole-line passes.  in_u8, ndim, shape, batch as
+ * for tm_edt; out_dist: device
  * float32 [batch][shape...], written completely.  Errors: as tm_edt (no
  * sampling argument), and TM_ERR_UNSUPPORTED for lines longer than about
  * 40 700 elements along an axis other than the last (one whole 32-bit line

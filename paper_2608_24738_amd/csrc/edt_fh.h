@@ -1,9 +1,11 @@
-// edt_fh.h -- lower-envelope passes of the separable EDT along strided axes
-// (paper, Section 2.3.2: each 1-D pass computes the lower envelope of a
-// family of parabolas in one sweep, following Felzenszwalb and Huttenlocher,
-// 2012):
+// edt_fh.h -- the strided-axis passes of the separable EDT (paper, Section
+// 2.3.2; Felzenszwalb and Huttenlocher, 2012).  Each pass is one exact 1-D
+// minimisation per line,
 //
-//     g'(q) = min over sites p of the line of  g(p) + w (q - p)^2.
+//     g'(q) = min over sites p of the line of  g(p) + w (q - p)^2,
+//
+// taken here either by walking the line's lower envelope of parabolas (the
+// kernels of this section) or by the windowed exact searches further down.
 //
 // gfx950 mapping: one lane owns one line, and the 64 lanes of a wavefront own
 // 64 lines that are adjacent in memory, so each step along the line is one
