@@ -224,6 +224,16 @@ bool plan_line_search(FhPlan &p, uint32_t n, uint64_t total, bool w16, int min_l
     return true;
 }
 
+// Multiplier of the plane permutation of the plane kernels (workgroup b
+// takes plane b * m mod planes): the first of a few primes that does not
+// divide the plane count, so m is coprime to it.
+uint32_t plane_stride(uint32_t planes) {
+    static const uint32_t primes[] = {397, 401, 409, 419, 421, 431, 433, 439};
+    for (uint32_t m : primes)
+        if (planes % m != 0) return m % planes == 0 ? 1u : m % planes;
+    return 1;
+}
+
 // Plane order for distance outputs of unit-sampled rank-3 inputs whose last
 // two extents are both 128, or both 64 with an even number of planes per
 // sample: the axis-0 nearest-zero scan first (k_col_scan, straight from the
@@ -303,6 +313,8 @@ int run_plane(Request &r, uint64_t total, uint64_t vox) {
     pe.dist = r.dist;
     pe.sq = r.sq;
     pe.n0 = r.shape[0];
+    pe.planes = uint32_t(total / (kPsN * kPsN));
+    pe.mult = plane_stride(pe.planes);
     constexpr int kEdtLut = 1024;
     return launch("plane_final.i8", k_plane_edt<kEdtLut>, dim3(uint32_t(total / (kPsN * kPsN))), dim3(kPsThreads),
                   2 * kPsTile + 4 * kEdtLut, r.stream, pe);

@@ -126,3 +126,14 @@ def test_planes_64_degenerate_and_odd():
     # an odd number of planes per sample keeps the other path
     parity_plane(rand_mask((2, 5, 64, 64), 0.02, 9), 3, "64 odd planes", expect_plane=False)
 
+
+
+# Workgroup b takes plane b * m mod planes: plane counts divisible by the
+# first multiplier the host tries (397), and ones that are not, including
+# counts below it.  Every plane must be written exactly once with its own
+# result, including samples without background (virtual element).
+@pytest.mark.parametrize("batch,n0", [(397, 1), (3, 97), (1, 1), (5, 79)])
+def test_plane_permutation_counts(batch, n0):
+    mask = rand_mask((batch, n0, 128, 128), 0.01, 4000 + batch + n0)
+    mask[0] = 1
+    parity_plane(mask, 3, "planes=%d" % (batch * n0))
