@@ -35,6 +35,7 @@
 #include "edt_mask.h"
 #include "edt_long.h"
 #include "edt_plane.h"
+#include "edt_lpair.h"
 
 using namespace tmedt;
 
@@ -191,6 +192,11 @@ int validate(const uint8_t *in, int ndim, const int64_t *shape, int64_t batch,
 // per workgroup) is faster.
 constexpr uint64_t kPairMinLines = 256 * kPairLines;
 
+// Workgroups of 16 lines below which the packed line pass leaves compute
+// units idle (two workgroups of 16 waves fill one): fewer lines take the
+// whole-line search with 8 lines per workgroup.
+constexpr uint64_t kLpMinGroups = 512;
+
 // Plan of one strided pass.
 struct FhPlan {
     uint32_t lpw;
@@ -205,6 +211,7 @@ struct FhPlan {
     uint32_t rbits;  // tidx, unit sampling: bits of the row in a key
     bool lng;        // index carrier, envelope in the line's own storage (k_fh_long)
     bool l1long;     // taxicab, two running minima in place (k_cdt_l1_long)
+    bool lp16;       // 16 lines per workgroup, two per packed 16-bit word (k_line_pair16)
 };
 
 // Whole-line windowed search: 8 lines per workgroup (a wave covers 8 rows
@@ -443,6 +450,23 @@ int plan_passes(const Request &r, uint64_t total, bool index_path, FhPlan *fh) {
                     const uint64_t planes = (uint64_t(n2) - g + kPairLines - 1) / n2 + 1;
                     if (planes * (n2 / 32) * 2 <= uint64_t(kWave)) p.from_mask = true;
                 }
+                continue;
+            }
+        }
+        // Unit sampling without indices, lines of up to 512 rows (a multiple
+        // of 16) whose 16 neighbours along the later axes are adjacent in
+        // memory: 16 lines per workgroup, two per packed 16-bit word, while
+        // that leaves at least two workgroups per compute unit and every
+        // exact candidate stays in int32.
+        if (!index_path && r.unit && n <= kLpMaxN && n % 16 == 0) {
+            uint64_t inner = 1;
+            for (int b = a + 1; b < nd; ++b) inner *= r.shape[b];
+            const uint64_t groups = total / n / kLpLines;
+            const void *field = r.dist ? static_cast<const void *>(r.dist) : static_cast<const void *>(r.sq);
+            if (inner % kLpLines == 0 && groups >= kLpMinGroups && groups < (uint64_t(1) << 31) &&
+                fmax + uint64_t(n - 1) * (n - 1) < uint64_t(kInfI) && uintptr_t(field) % 16 == 0) {
+                p.lp16 = true;
+                p.lds = lpair_lds(n);
                 continue;
             }
         }
@@ -759,6 +783,23 @@ int run(Request &r) {
                     rc = fin ? launch(nm, k_tile_pair<true, false, 16>, tgrid, tblock, p.lds, r.stream, tg)
                              : launch(nm, k_tile_pair<false, false, 16>, tgrid, tblock, p.lds, r.stream, tg);
             }
+        } else if (p.lp16) {
+            LinePairArgs lp{};
+            lp.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
+            lp.dist = r.dist;
+            lp.sq = r.sq;
+            lp.lines = uint32_t(lines);
+            lp.n = n;
+            lp.inner = uint32_t(inner);
+            lp.div_inner = Div32::make(lp.inner);
+            lp.ndim = nd;
+            for (int b = 0; b < nd; ++b) {
+                lp.shape[b] = r.shape[b];
+                lp.wall[b] = r.w[b];
+            }
+            const dim3 lgrid(uint32_t(lines / kLpLines)), lblock(kPsThreads);
+            rc = fin ? launch("line_pair_final", k_line_pair16<true>, lgrid, lblock, p.lds, r.stream, lp)
+                     : launch("line_pair", k_line_pair16<false>, lgrid, lblock, p.lds, r.stream, lp);
         } else if (p.ls_lpw) {
             LineSearchArgs la{};
             la.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
