@@ -792,6 +792,7 @@ int run(Request &r) {
             lp.n = n;
             lp.inner = uint32_t(inner);
             lp.div_inner = Div32::make(lp.inner);
+            lp.mult = plane_stride(uint32_t((lines / kLpLines) & ~uint64_t(31)) / 4u);
             lp.ndim = nd;
             for (int b = 0; b < nd; ++b) {
                 lp.shape[b] = r.shape[b];

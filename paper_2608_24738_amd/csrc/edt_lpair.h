@@ -44,6 +44,7 @@ struct LinePairArgs {
     uint32_t n;            // line length, a multiple of 16, at most kLpMaxN
     uint32_t inner;        // element stride of the line, a multiple of 16
     Div32 div_inner;
+    uint32_t mult;         // order of the sets of 4 line groups (coprime to their count)
     int32_t ndim;
     uint32_t shape[kMaxDim];
     double wall[kMaxDim];  // ones (virtual element of a final pass)
@@ -120,6 +121,11 @@ __global__ void __launch_bounds__(kPsThreads, 8) k_line_pair16(LinePairArgs a) {
     if (g < (gridDim.x & ~31u)) {
         const uint32_t x = g & 7u, i = g >> 3;
         g = (i >> 2) * 32u + x * 4u + (i & 3u);
+        // ... and the sets of 4 line groups are taken in the order
+        // s * mult mod sets, so that neighbouring (similar) lines do not all
+        // come last
+        const uint32_t sets = (gridDim.x & ~31u) / 4u;
+        g = uint32_t((uint64_t(g >> 2) * a.mult) % sets) * 4u + (g & 3u);
     }
     const uint32_t L0 = g * uint32_t(kLpLines);
     const uint32_t o = a.div_inner.div(L0);
@@ -224,13 +230,30 @@ __global__ void __launch_bounds__(kPsThreads, 8) k_line_pair16(LinePairArgs a) {
         const int q = 16 * int(pi) + 2 * rho;      // rows q, q + 1; lines 2 jw, 2 jw + 1
         u16x2 bA, bB;
         lp_search(code, n, q, jw, bA, bB);
-        const uint32_t h[4] = {bA.x, bA.y, bB.x, bB.y};   // (q, 2jw), (q, 2jw+1), (q+1, 2jw), (q+1, 2jw+1)
+        uint32_t h[4] = {bA.x, bA.y, bB.x, bB.y};   // (q, 2jw), (q, 2jw+1), (q+1, 2jw), (q+1, 2jw+1)
+        if (__builtin_expect(__any(h[0] >= 0xfffeu || h[1] >= 0xfffeu || h[2] >= 0xfffeu || h[3] >= 0xfffeu), 0)) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int qq = q + (k >> 1), l = 2 * jw + (k & 1);
-            uint32_t v = h[k];
-            if (v >= 0xfffeu) v = exact_search(qq, l);      // distance of 256 or more, or none
-            emit(qq, l, v, v == uint32_t(kInfI));
+            for (int k = 0; k < 4; ++k) {
+                const int qq = q + (k >> 1), l = 2 * jw + (k & 1);
+                if (h[k] >= 0xfffeu) h[k] = exact_search(qq, l);   // distance of 256 or more, or none
+                emit(qq, l, h[k], h[k] == uint32_t(kInfI));
+            }
+            continue;
+        }
+        // every result exact in 16 bits: the two lines of each row in one store
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const uint64_t e = base + uint64_t(q + k) * a.inner + uint32_t(2 * jw);
+            const uint32_t v0 = h[2 * k], v1 = h[2 * k + 1];
+            if (!FINAL) {
+                *reinterpret_cast<int2 *>(a.buf + e) = int2{int32_t(v0), int32_t(v1)};
+                continue;
+            }
+            const bool small = v0 < uint32_t(kLpLut) && v1 < uint32_t(kLpLut);
+            const float d0 = small ? __builtin_bit_cast(float, lut[v0]) : sqrt_rn_int(v0);
+            const float d1 = small ? __builtin_bit_cast(float, lut[v1]) : sqrt_rn_int(v1);
+            if (a.dist) *reinterpret_cast<float2 *>(a.dist + e) = float2{d0, d1};
+            if (a.sq) *reinterpret_cast<int2 *>(a.sq + e) = int2{int32_t(v0), int32_t(v1)};
         }
     }
 }
