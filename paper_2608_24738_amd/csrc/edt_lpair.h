@@ -13,8 +13,9 @@
 // kernels on the codes (a lane: one word, two adjacent rows, whose candidates
 // in each block of four steps share ten reads).  A candidate built on a
 // clamped code is at least 0xfffe, and so is every true candidate through
-// that row, so a result below 0xfffe is exact; a result of 0xfffe or more
-// (a distance of at least 256) is searched again in 32-bit on the exact copy.
+// that row, so a result below 0xfffe is exact; a wave with any result of
+// 0xfffe or more (a distance of at least 256, or no site) searches its patch
+// again in 32-bit on the exact copy.
 // Workgroups whose lines hold at most kLpDirect rows with any site take, for
 // every element, the minimum over those rows directly from the exact copy:
 // on such lines the distances can reach the line length.
@@ -101,6 +102,42 @@ __device__ __forceinline__ void lp_search(const uint32_t *code, int n, int q, in
     } while (d < n);
 }
 
+// The same search on the exact int32 copy ([row][16 lines]), for a patch
+// where some result needs more than 16 bits: rows q and q + 1 of lines l and
+// l + 1 (one 8-byte read per row), no site = kInfI (values plus squared
+// distances stay below 2^31 on this path, host eligibility, so kInfI plus
+// any squared distance stays above every real candidate in uint32).  Reads
+// clamp to the line's first and last rows.
+__device__ __forceinline__ void lp_search32(const int32_t *exact, int n, int q, int l, uint32_t (&best)[4]) {
+    auto row2 = [&](int r) {
+        const int rr = min(max(r, 0), n - 1);
+        const int2 v = *reinterpret_cast<const int2 *>(exact + rr * kLpLines + l);
+        return uint2{uint32_t(v.x), uint32_t(v.y)};
+    };
+    const uint2 a0 = row2(q), a1 = row2(q + 1);
+    best[0] = a0.x; best[1] = a0.y; best[2] = a1.x; best[3] = a1.y;
+    for (int d = 1; d < n; d += 4) {
+        const uint32_t dd = uint32_t(d) * uint32_t(d);
+        const uint32_t m = max(max(best[0], best[1]), max(best[2], best[3]));
+        if (__all(m <= dd)) break;
+        uint2 U[5], W[5];
+#pragma unroll
+        for (int k = 0; k < 5; ++k) {
+            U[k] = row2(q - d - 3 + k);        // rows q-d-3 .. q-d+1
+            W[k] = row2(q + d + k);            // rows q+d .. q+d+4
+        }
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+            const uint32_t s2 = uint32_t(d + st) * uint32_t(d + st);
+            // row q: U[3-st], W[st]; row q+1: U[4-st], W[st+1]
+            best[0] = min(best[0], min(U[3 - st].x, W[st].x) + s2);
+            best[1] = min(best[1], min(U[3 - st].y, W[st].y) + s2);
+            best[2] = min(best[2], min(U[4 - st].x, W[st + 1].x) + s2);
+            best[3] = min(best[3], min(U[4 - st].y, W[st + 1].y) + s2);
+        }
+    }
+}
+
 template <bool FINAL>
 __global__ void __launch_bounds__(kPsThreads, 8) k_line_pair16(LinePairArgs a) {
     extern __shared__ __attribute__((aligned(16))) uint32_t lp_lds[];
@@ -185,24 +222,6 @@ __global__ void __launch_bounds__(kPsThreads, 8) k_line_pair16(LinePairArgs a) {
         if (a.dist) a.dist[e] = dv;
         if (a.sq) a.sq[e] = int32_t(d2);
     };
-    // exact minimum for element (q, l) over the rows at growing distance
-    auto exact_search = [&](int q, int l) -> uint32_t {
-        uint32_t best = uint32_t(exact[q * kLpLines + l]);    // kInfI: no site yet
-        for (int d = 1; d < n; ++d) {
-            if (best <= uint32_t(d) * uint32_t(d)) break;
-            const uint32_t dd = uint32_t(d) * uint32_t(d);
-            if (q - d >= 0) {
-                const uint32_t u = uint32_t(exact[(q - d) * kLpLines + l]);
-                if (u != uint32_t(kInfI)) best = min(best, u + dd);
-            }
-            if (q + d < n) {
-                const uint32_t w = uint32_t(exact[(q + d) * kLpLines + l]);
-                if (w != uint32_t(kInfI)) best = min(best, w + dd);
-            }
-        }
-        return best;
-    };
-
     if (nsites <= uint32_t(kLpDirect)) {
         // few site rows: the minimum over them, for every element
         for (int k = t; k < n * kLpLines; k += kPsThreads) {
@@ -226,17 +245,32 @@ __global__ void __launch_bounds__(kPsThreads, 8) k_line_pair16(LinePairArgs a) {
         return __builtin_amdgcn_readfirstlane(k);
     };
     const uint32_t npatch = uint32_t(n / 16);
+    // Results past 16 bits come in regions (far from any site), so a wave
+    // that needed the exact search on a patch starts its next patch there,
+    // until a patch's results all fit 16 bits again.
+    bool wide = false;
     for (uint32_t pi = next_patch(); pi < npatch; pi = next_patch()) {
         const int q = 16 * int(pi) + 2 * rho;      // rows q, q + 1; lines 2 jw, 2 jw + 1
-        u16x2 bA, bB;
-        lp_search(code, n, q, jw, bA, bB);
-        uint32_t h[4] = {bA.x, bA.y, bB.x, bB.y};   // (q, 2jw), (q, 2jw+1), (q+1, 2jw), (q+1, 2jw+1)
-        if (__builtin_expect(__any(h[0] >= 0xfffeu || h[1] >= 0xfffeu || h[2] >= 0xfffeu || h[3] >= 0xfffeu), 0)) {
+        uint32_t h[4];                              // (q, 2jw), (q, 2jw+1), (q+1, 2jw), (q+1, 2jw+1)
+        bool redo = wide;
+        if (!wide) {
+            u16x2 bA, bB;
+            lp_search(code, n, q, jw, bA, bB);
+            h[0] = bA.x;
+            h[1] = bA.y;
+            h[2] = bB.x;
+            h[3] = bB.y;
+            redo = __any(h[0] >= 0xfffeu || h[1] >= 0xfffeu || h[2] >= 0xfffeu || h[3] >= 0xfffeu);
+        }
+        if (__builtin_expect(redo, 0)) {
+            // a distance of 256 or more, or no site: the patch on the exact copy
+            lp_search32(exact, n, q, 2 * jw, h);
+            wide = __any(h[0] >= 0xfffeu || h[1] >= 0xfffeu || h[2] >= 0xfffeu || h[3] >= 0xfffeu);
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const int qq = q + (k >> 1), l = 2 * jw + (k & 1);
-                if (h[k] >= 0xfffeu) h[k] = exact_search(qq, l);   // distance of 256 or more, or none
-                emit(qq, l, h[k], h[k] == uint32_t(kInfI));
+                const bool none = h[k] >= uint32_t(kInfI);
+                emit(qq, l, none ? 0u : h[k], none);
             }
             continue;
         }

@@ -80,3 +80,14 @@ def test_3d_intermediate_and_final():
 def test_full_workload_2():
     mask = workloads.make_mask(2)[:, 0]
     check(mask, 2, "32x512^2 discs")
+
+
+def test_corner_blob():
+    # background only in a 40 x 40 corner block: 40 site rows in every
+    # workgroup (the search runs) and distances up to ~670 (most patches are
+    # redone on the exact copy)
+    mask = np.ones((16, 512, 512), np.uint8)
+    mask[:, :40, :40] = 0
+    mask[5, :40, :40] = 1
+    mask[5, 300:340, 470:510] = 0
+    check(mask, 2, "corner blob")
