@@ -1092,29 +1092,40 @@ __global__ void __launch_bounds__(kWave * kPairWaves, MAXRB <= 8 ? 8 : 1) k_tile
         else if (nb == 3) search_pair2<0, 3, METRIC>(row0 + (q1 - 12) * kRowW + cw, best1, best2, d);
         else if (nb == 2) search_pair2<0, 2, METRIC>(row0 + (q1 - 8) * kRowW + cw, best1, best2, d);
         else if (nb == 1) search_pair2<0, 1, METRIC>(row0 + (q1 - 4) * kRowW + cw, best1, best2, d);
-        // Longer searches and rows near the ends: reads clamp into the
-        // guard rows.  The clamp works on LDS byte addresses, so each read
-        // costs one add and one min / max, against uniform bounds: the first
-        // data word of the first guard row and the last one of the last
-        // guard row.  (A row stride exceeds the data words of a row, so a
-        // read past the guard rows is clamped to one of those two words,
-        // which hold "no site" like the whole guard row.)
-        const uint32_t a1 = lds_byte_addr(row0 + q1 * kRowW + cw), a2 = lds_byte_addr(row0 + q2 * kRowW + cw);
-        const uint32_t a_lo = lds_byte_addr(tw);
-        const uint32_t a_hi = lds_byte_addr(row0 + (n + kGuard16 - 1) * kRowW + (kWave - 1));
+        // Longer searches and rows near the ends: each block of four steps
+        // reads rows q-d-3 .. q-d and q+d .. q+d+3 of each chain from two LDS
+        // byte addresses (immediate offsets from them), stepped by four rows
+        // per block and clamped at the guard rows: the low base at the first
+        // guard row, the high base at the fourth-last one.  A base is clamped
+        // only when every row of its block lies past that end of the line
+        // (kGuard16 = 4 guard rows), and then the block reads guard rows only,
+        // which hold "no site".
+        static_assert(kGuard16 == 4, "a clamped block of four rows reads guard rows only");
+        constexpr uint32_t kRowB = 4u * kRowW;                      // row stride in bytes
+        const uint32_t a_lo = lds_byte_addr(tw + cw);               // guard row 0, this lane's word
+        const uint32_t a_hi = lds_byte_addr(row0 + (n + kGuard16 - 4) * kRowW + cw);
+        int lo1 = int(lds_byte_addr(row0 + q1 * kRowW + cw)) - int((d + 3) * kRowB);
+        int lo2 = int(lds_byte_addr(row0 + q2 * kRowW + cw)) - int((d + 3) * kRowB);
+        uint32_t hi1 = lds_byte_addr(row0 + q1 * kRowW + cw) + uint32_t(d) * kRowB;
+        uint32_t hi2 = lds_byte_addr(row0 + q2 * kRowW + cw) + uint32_t(d) * kRowB;
         while (!__all(stop_at<METRIC>(__builtin_elementwise_max(best1, best2), d))) {
+            const uint32_t l1 = uint32_t(max(lo1, int(a_lo))), l2 = uint32_t(max(lo2, int(a_lo)));
+            const uint32_t h1 = min(hi1, a_hi), h2 = min(hi2, a_hi);
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
                 const int dd = d + s;
-                const uint32_t step = 4u * uint32_t(dd * kRowW);   // uniform
-                // a1 - step may wrap below 0 when dd is large: compare as signed
-                const u16x2 u = as_pair(lds_word(uint32_t(max(int(a1 - step), int(a_lo)))));
-                const u16x2 w = as_pair(lds_word(min(a1 + step, a_hi)));
-                const u16x2 x = as_pair(lds_word(uint32_t(max(int(a2 - step), int(a_lo)))));
-                const u16x2 y = as_pair(lds_word(min(a2 + step, a_hi)));
+                // row q - dd is row 3 - s of the low block, q + dd row s of the high one
+                const u16x2 u = as_pair(lds_word(l1 + (3 - s) * kRowB));
+                const u16x2 w = as_pair(lds_word(h1 + s * kRowB));
+                const u16x2 x = as_pair(lds_word(l2 + (3 - s) * kRowB));
+                const u16x2 y = as_pair(lds_word(h2 + s * kRowB));
                 best1 = __builtin_elementwise_min(best1, cand<METRIC>(__builtin_elementwise_min(u, w), dd));
                 best2 = __builtin_elementwise_min(best2, cand<METRIC>(__builtin_elementwise_min(x, y), dd));
             }
+            lo1 -= int(4 * kRowB);
+            lo2 -= int(4 * kRowB);
+            hi1 += 4 * kRowB;
+            hi2 += 4 * kRowB;
             d += 4;
             if (d > n + 4) break;   // every row has been examined
         }
