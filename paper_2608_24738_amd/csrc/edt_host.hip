@@ -476,13 +476,13 @@ int plan_passes(const Request &r, uint64_t total, bool index_path, FhPlan *fh) {
         // Index carrier, lines up to 256 rows: tiled windowed search.  Unit
         // sampling packs (value, row) into one key below 2^31.
         if (index_path && n <= 256) {
-            const size_t tb = size_t(2) * idx_tile_words(n) * 4;
+            const size_t tb = idx_tile_lds(n, !r.unit);
             int rb = bits_for(n - 1);
             if (rb < 1) rb = 1;
             const uint64_t kv = fmax + uint64_t(n - 1) * (n - 1);
             const bool keys_fit = !r.unit || (rb < 31 && kv < (uint64_t(1) << 31) &&
                                               ((kv << rb) | uint64_t(n - 1)) < (uint64_t(1) << 31));
-            if (tb + 1024 <= kLdsBytes && keys_fit && total / n + kWave < (uint64_t(1) << 32)) {
+            if (tb + 2048 <= kLdsBytes && keys_fit && total / n + kIdxLines < (uint64_t(1) << 32)) {
                 p.tidx = true;
                 p.rbits = uint32_t(rb);
                 p.lds = tb;
@@ -890,13 +890,37 @@ int run(Request &r) {
             }
             x.dist = fin ? r.dist : nullptr;
             x.sq = fin ? r.sq : nullptr;
-            const dim3 igrid(uint32_t((lines + kWave - 1) / kWave)), iblock(kWave * kIdxWaves);
-            if (r.unit)
-                rc = fin ? launch("tile_idx_final", k_tile_idx<false, true>, igrid, iblock, p.lds, r.stream, x)
-                         : launch("tile_idx", k_tile_idx<false, false>, igrid, iblock, p.lds, r.stream, x);
-            else
-                rc = fin ? launch("tile_idx_final", k_tile_idx<true, true>, igrid, iblock, p.lds, r.stream, x)
-                         : launch("tile_idx", k_tile_idx<true, false>, igrid, iblock, p.lds, r.stream, x);
+            const dim3 igrid(uint32_t((lines + kIdxLines - 1) / kIdxLines)), iblock(kWave * kIdxWaves);
+            // Ranks 2 and 3 take kernels with the rank and axis built in;
+            // FAST ones when every extent after axis 0 is a power of two, the
+            // line length a multiple of 32 and every buffer below 2 GiB.
+            bool fast = (nd == 2 || nd == 3) && n % 32 == 0;
+            {
+                uint32_t shb = 0;
+                for (int b = nd - 1; b >= 0; --b) {
+                    const uint32_t e = r.shape[b];
+                    if (b > 0 && (e & (e - 1)) != 0) fast = false;
+                    x.sh[b] = shb;
+                    x.msk[b] = b > 0 ? e - 1 : 0xffffffffu;
+                    if (b > 0) shb += uint32_t(__builtin_ctz(e));
+                }
+                const uint64_t cb = r.batch * cstride * 4, db = r.batch * vox * 4;
+                if (cb >= (uint64_t(1) << 31) || db >= (uint64_t(1) << 31)) fast = false;
+                x.cbytes = uint32_t(cb);
+                x.dbytes = uint32_t(db);
+            }
+            const char *nm = fin ? "tile_idx_final" : "tile_idx";
+#define TM_TIDX_ND(S, F)                                                                          \
+    (nd == 2   ? launch(nm, k_tile_idx<S, true, 2, 0, F>, igrid, iblock, p.lds, r.stream, x)      \
+     : a == 1  ? launch(nm, k_tile_idx<S, false, 3, 1, F>, igrid, iblock, p.lds, r.stream, x)     \
+               : launch(nm, k_tile_idx<S, true, 3, 0, F>, igrid, iblock, p.lds, r.stream, x))
+#define TM_TIDX(S)                                                                                \
+    (nd == 2 || nd == 3 ? (fast ? TM_TIDX_ND(S, true) : TM_TIDX_ND(S, false))                      \
+     : fin              ? launch(nm, k_tile_idx<S, true>, igrid, iblock, p.lds, r.stream, x)      \
+                        : launch(nm, k_tile_idx<S, false>, igrid, iblock, p.lds, r.stream, x))
+            rc = r.unit ? TM_TIDX(false) : TM_TIDX(true);
+#undef TM_TIDX
+#undef TM_TIDX_ND
         } else {
             IndexArgs x{};
             x.idx = cidx;

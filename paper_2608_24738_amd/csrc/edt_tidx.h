@@ -1,21 +1,26 @@
 // Tiled pass on the index carrier: nearest background elements (and, on the
 // last pass, distances and coordinates) for unit or anisotropic sampling.
 //
-// A workgroup owns 64 adjacent lines of one pass.  It stages, per line and
-// row, the carried site (the in-sample flat index of the nearest background
-// element found by the earlier passes, -1 for none) and the site's squared
-// distance over the axes already processed, recomputed from the site's
-// coordinates.  Each element then runs the windowed exact search over the
-// rows of its line: examine rows at growing distance d and stop once
-// w d^2 exceeds the best value found.  The winner's site comes from the
-// staged copy, so the pass can overwrite its lines in place.
+// A workgroup owns 32 adjacent lines of one pass (two workgroups fit a
+// compute unit at 256 rows, so one stages while the other searches).  It
+// stages, per line and row, the carried site (the in-sample flat index of the
+// nearest background element found by the earlier passes, -1 for none) and
+// the site's squared distance over the axes already processed, recomputed
+// from the site's coordinates.  Each element then runs the windowed exact
+// search over the rows of its line: examine rows at growing distance d and
+// stop once w d^2 exceeds the best value found.  The winner's site comes from
+// the staged copy, so the pass can overwrite its lines in place.
 //
 // Unit sampling: values are exact integers and a candidate is the key
 // (value << RB) | row, so one integer minimum picks the smallest value and,
 // among equal values, the smallest row: the canonical choice of the
 // separable method (smallest flat index among nearest elements).
-// Sampled: values are float, w = s_a^2; ties keep the first candidate met
-// (any nearest element is correct there).
+// Sampled: values are float, w = s_a^2.  Each step keeps only the smaller
+// of its two rows' candidates (min(f(q-e), f(q+e)) + w e^2, which rounds to
+// the smaller of the two sums), and each block of four steps only its
+// minimum, the first block that reached the best value and that block's four
+// candidates; the row is found once at the end (any nearest element is
+// correct there).
 #pragma once
 
 #include "edt_fh.h"
@@ -23,9 +28,10 @@
 namespace tmedt {
 
 constexpr int kIdxWaves = 16;
+constexpr int kIdxLines = 32;     // lines per workgroup
 constexpr int kIdxGuard = 4;       // guard rows of "no site" per side
-constexpr int kIdxRowW = kWave + 8;  // padded row stride (words)
-constexpr int kIdxPatch = 8;       // patch: 8 rows x 8 lines
+constexpr int kIdxRowW = kIdxLines + 4;  // padded row stride (words)
+constexpr int kIdxPatch = 8;       // patch: 8 rows x 8 lines (PR x 64 / PR in general)
 
 struct IdxTileArgs {
     int32_t *idx;            // the carrier of the sites: slice 0 of [batch][ndim][vox], or a
@@ -47,57 +53,55 @@ struct IdxTileArgs {
     Div32 div_shape[kMaxDim];
     double wall[kMaxDim];    // squared sampling per axis
     uint32_t shape[kMaxDim];
+    // FAST kernels only: every extent after axis 0 is a power of two and
+    // every buffer below 2 GiB.  Coordinate b of an in-sample flat index y
+    // is (y >> sh[b]) & msk[b]; rc / rd / rs span the carrier buffer (from
+    // idx), dist and sq.
+    uint32_t sh[kMaxDim];
+    uint32_t msk[kMaxDim];
+    uint32_t cbytes, dbytes;
 };
 
-// LDS words of the two tile arrays for lines of n rows.
+// LDS words of the two tile arrays for lines of n rows, and of the table of
+// w k^2 for k = 0 .. n + 7 (sampled searches; three leading words align the
+// blocks' reads).
 __host__ __device__ constexpr uint32_t idx_tile_words(uint32_t n) { return (n + 2 * kIdxGuard) * kIdxRowW; }
-
-// Sampled search blocks BLK .. NBLK-1 (four steps each, unrolled at compile
-// time): candidates f(q -+ d) + w d^2 at immediate LDS offsets from `pb`,
-// the word of row q - 4 NBLK (every read stays in the tile).  Keeps the
-// first strictly smaller candidate and its row offset; ends early once every
-// lane of the wave has w d^2 above its best value.
-template <int BLK, int NBLK>
-__device__ __forceinline__ void search_samp(const uint32_t *pb, float w, float &fbest, int &roff, int &dnext) {
-    if constexpr (BLK < NBLK) {
-        constexpr int d = 1 + 4 * BLK;
-        constexpr int R = 4 * NBLK;
-        if (__all(w * float(d * d) > fbest)) return;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            const int dd = d + s;
-            const float add = w * float(dd * dd);
-            const float cu = __builtin_bit_cast(float, pb[(R - dd) * kIdxRowW]) + add;
-            const float cv = __builtin_bit_cast(float, pb[(R + dd) * kIdxRowW]) + add;
-            if (cu < fbest) {
-                fbest = cu;
-                roff = -dd;
-            }
-            if (cv < fbest) {
-                fbest = cv;
-                roff = dd;
-            }
-        }
-        dnext = d + 4;
-        search_samp<BLK + 1, NBLK>(pb, w, fbest, roff, dnext);
-    }
+__host__ __device__ constexpr uint32_t idx_step_words(uint32_t n) { return (n + 12 + 3) & ~3u; }
+__host__ __device__ constexpr size_t idx_tile_lds(uint32_t n, bool samp) {
+    return size_t(2 * idx_tile_words(n) + (samp ? idx_step_words(n) : 0u)) * 4u;
 }
 
-template <bool SAMP, bool FINAL>
+// ND, AX: rank and axis of the pass fixed at compile time (ND = 0: taken
+// from the arguments), so the coordinate loops unroll without tests.
+// FAST (ND > 0 only): coordinates by shifts and masks, and every global
+// access through a buffer resource with a 32-bit byte offset, the row and
+// slice parts of which are wave-uniform scalar offsets.
+// Rows of a search patch (its lines: 64 / rows).  FAST passes take 2 rows of
+// 32 lines, so each store instruction writes two whole 128-byte segments
+// (2 x 256^3 sampled with indices: final pass 171 -> 145 us, middle pass
+// 117 -> 109 us against 8 x 8 patches); the others keep 8 x 8.
+__host__ __device__ constexpr int idx_patch_rows(bool fast) { return fast ? 2 : 8; }
+
+template <bool SAMP, bool FINAL, int ND = 0, int AX = 0, bool FAST = false>
 __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
     extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
-    __shared__ __attribute__((aligned(16))) uint8_t any_site[kWave][kIdxWaves];   // [line][wave]
-    __shared__ uint4 line_info[kWave];     // per line: sample, base of row 0, position i, live
+    constexpr int kGroups = kWave * kIdxWaves / kIdxLines;   // staging row groups
+    static_assert(kIdxLines == 32, "staging: lanes l and l + 32 of a wave take line l");
+    __shared__ __attribute__((aligned(16))) uint32_t wave_has[kIdxWaves];   // per wave: bit l set when line l has a site in its rows
+    // per line: sample and base of row 0 in slice 0 (FAST: byte offsets of
+    // row 0 in the carrier and in the outputs), position i, live
+    __shared__ uint4 line_info[kIdxLines];
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
     const int n = int(a.n);
-    const int nd = a.ndim;
-    const int ax = a.axis;
+    const int nd = ND ? ND : a.ndim;
+    const int ax = ND ? AX : a.axis;
     const uint32_t tw = idx_tile_words(uint32_t(n));
     uint32_t *val0 = lds + kIdxGuard * kIdxRowW;             // row 0 of the values / keys
     int32_t *site0 = reinterpret_cast<int32_t *>(lds + tw) + kIdxGuard * kIdxRowW;   // row 0 of the sites
-    const uint32_t L0 = blockIdx.x * uint32_t(kWave);
+    float *const step = reinterpret_cast<float *>(lds + 2 * tw) + 3;   // sampled: step[k] = w k^2
+    const uint32_t L0 = blockIdx.x * uint32_t(kIdxLines);
 
     // Line j of the workgroup: sample, base of the line in slice 0, position
     // along the later axes.
@@ -133,23 +137,28 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         }
     };
     // squared distance over the axes after `ax` between this lane's line and
-    // site y (in-sample flat), or "none" (sampled: float sum of the exact
-    // integer squares times the squared sampling)
+    // site y (in-sample flat; its coordinates along those axes are its
+    // remainders by the later extents), or "none" (sampled: float sum of the
+    // exact integer squares times the squared sampling)
     auto carried = [&](int32_t y, uint32_t &key_or_bits, int q) {
         if (y < 0) {
             key_or_bits = SAMP ? __builtin_bit_cast(uint32_t, __builtin_inff()) : uint32_t(kInfI);
             return;
         }
-        uint32_t yi = a.div_inner.div(uint32_t(y));
-        yi = uint32_t(y) - yi * a.inner;               // site position along the later axes
+        uint32_t yi = uint32_t(y);
         float accf = 0.0f;
         uint32_t acci = 0;
 #pragma unroll
         for (int b = kMaxDim - 1; b >= 0; --b) {
             if (b > ax && b < nd) {
-                const uint32_t qy = a.div_shape[b].div(yi);
-                const int dy = int(yi - qy * a.div_shape[b].d) - xc[b];
-                yi = qy;
+                int dy;
+                if constexpr (FAST) {
+                    dy = int((uint32_t(y) >> a.sh[b]) & a.msk[b]) - xc[b];
+                } else {
+                    const uint32_t qy = a.div_shape[b].div(yi);
+                    dy = int(yi - qy * a.div_shape[b].d) - xc[b];
+                    yi = qy;
+                }
                 if (SAMP) accf += wf[b] * float(dy * dy);
                 else acci += uint32_t(dy * dy);
             }
@@ -157,120 +166,209 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         key_or_bits = SAMP ? __builtin_bit_cast(uint32_t, accf) : ((acci << a.rbits) | uint32_t(q));
     };
 
-    // ---- guard rows and staging ---------------------------------------------
+    // ---- guard rows, step table and staging ---------------------------------
     for (int k = t; k < kIdxGuard * kIdxRowW; k += kWave * kIdxWaves) {
         const uint32_t none = SAMP ? __builtin_bit_cast(uint32_t, __builtin_inff()) : uint32_t(kInfI);
         lds[k] = none;
         val0[n * kIdxRowW + k] = none;
     }
-    const Line me = line_of(lane);
-    if (wv == 0) line_info[lane] = uint4{me.s, me.base, me.i, me.live ? 1u : 0u};
+    if constexpr (SAMP) {
+        const float w = float(a.wall[ax]);
+        for (int k = t; k <= n + 7; k += kWave * kIdxWaves) step[k] = w * float(k * k);
+    }
+    // thread t stages line t % kIdxLines, rows t / kIdxLines + kGroups j
+    const int sl = t & (kIdxLines - 1), sg = t / kIdxLines;
+    const Line me = line_of(sl);
+    const uint32_t cvo = (me.s * uint32_t(a.cstride) + me.base) * 4u;   // FAST: carrier byte offset of row 0
+    if (t < kIdxLines)
+        line_info[sl] = FAST ? uint4{cvo, (me.s * a.vox + me.base) * 4u, me.i, me.live ? 1u : 0u}
+                             : uint4{me.s, me.base, me.i, me.live ? 1u : 0u};
     line_coords(me.i);
     const int32_t *src = a.idx + uint64_t(me.s) * a.cstride + me.base;
+    // FAST only (a null resource elsewhere)
+    const __amdgpu_buffer_rsrc_t rc = make_rsrc(a.idx, FAST ? a.cbytes : 0u);
+    const __amdgpu_buffer_rsrc_t rd = make_rsrc(a.dist, FAST && a.dist ? a.dbytes : 0u);
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.sq, FAST && a.sq ? a.dbytes : 0u);
     uint32_t seen = 0;
     constexpr int SB = 8;
-    for (int q0 = wv; q0 < n; q0 += kIdxWaves * SB) {
+    const uint32_t svo = cvo + uint32_t(sg) * a.inner * 4u;
+    for (int it = 0; it * kGroups * SB < n; ++it) {
+        const int q0 = sg + it * kGroups * SB;
         int32_t y[SB];
 #pragma unroll
-        for (int j = 0; j < SB; ++j) y[j] = src[uint64_t(min(q0 + j * kIdxWaves, n - 1)) * a.inner];
+        for (int j = 0; j < SB; ++j) {
+            // FAST: n is a multiple of 32 = kGroups, so the rows of a load
+            // are all in the line or all past it (a uniform test)
+            if constexpr (FAST) {
+                const int u = it * kGroups * SB + j * kGroups;
+                y[j] = u < n ? int32_t(__builtin_amdgcn_raw_buffer_load_b32(rc, svo, uint32_t(u) * a.inner * 4u, 0))
+                             : -1;
+            } else
+                y[j] = src[uint64_t(min(q0 + j * kGroups, n - 1)) * a.inner];
+        }
 #pragma unroll
         for (int j = 0; j < SB; ++j) {
-            const int q = q0 + j * kIdxWaves;
+            const int q = q0 + j * kGroups;
             if (q < n) {
                 const int32_t yy = me.live ? y[j] : -1;
                 uint32_t v;
                 carried(yy, v, q);
                 seen |= yy >= 0 ? 1u : 0u;
-                val0[q * kIdxRowW + lane] = v;
-                site0[q * kIdxRowW + lane] = yy;
+                val0[q * kIdxRowW + sl] = v;
+                site0[q * kIdxRowW + sl] = yy;
             }
         }
     }
-    any_site[lane][wv] = uint8_t(seen);
+    {
+        // lanes l and l + 32 of a wave stage line l
+        const uint64_t bal = __ballot(seen != 0u);
+        if (lane == 0) wave_has[wv] = uint32_t(bal) | uint32_t(bal >> 32);
+    }
     __syncthreads();
+    uint32_t has_mask = 0;
+#pragma unroll
+    for (int k = 0; k < kIdxWaves; k += 4) {
+        const uint4 h = *reinterpret_cast<const uint4 *>(&wave_has[k]);
+        has_mask |= h.x | h.y | h.z | h.w;
+    }
 
     // ---- search and output, patch by patch ----------------------------------
-    // Patch p = (row block p / 8, line block (p + p / 8) % 8); lane l takes
-    // row 8 rb + l / 8 of line 8 cb + l % 8.
-    const int pr = lane >> 3;
-    const float w = float(a.wall[ax]);
+    // Patch p = (row block rb = p / L, line block (p + rb) % L) with L =
+    // kIdxLines / 8; lane l takes row 8 rb + l / 8 of line 8 cb + l % 8.
+    //
+    // The search runs in blocks of four steps d .. d+3.  A block reads rows
+    // q-d-3 .. q-d and q+d .. q+d+3 at fixed offsets from two LDS byte
+    // addresses that step by four rows per block and are clamped to the
+    // first guard row above and the first one below the line: a clamped
+    // block lies wholly past that end of the line, where every candidate is
+    // "none" and the guard rows it then reads are "none" too.  The candidate
+    // of step e is the smaller of the two rows at distance e plus the weight
+    // of e (for unit keys the minimum of the two keys, whose low bits keep
+    // the row).
+    constexpr int kRB = kIdxRowW * 4;              // row stride in bytes
+    constexpr int PR = idx_patch_rows(FAST);   // rows of a patch
+    constexpr int PL = kWave / PR;                 // lines of a patch
+    const int pr = lane / PL;
     const uint32_t rmask = (1u << a.rbits) - 1u;
-    const int npatch = 8 * ((n + kIdxPatch - 1) / kIdxPatch);
+    constexpr int kLB = kIdxLines / PL;            // line blocks
+    const int npatch = kLB * ((n + PR - 1) / PR);
     int32_t *slice0 = nullptr;
     for (int p = wv; p < npatch; p += kIdxWaves) {
-        const int rbk = p >> 3;
-        const int ln = kIdxPatch * ((p + rbk) & 7) + (lane & 7);
-        const uint4 hv = *reinterpret_cast<const uint4 *>(&any_site[ln][0]);
-        const bool has = (hv.x | hv.y | hv.z | hv.w) != 0u;
-        const int qr = kIdxPatch * rbk + pr;
+        const int rbk = p / kLB;
+        const int ln = PL * ((p + rbk) % kLB) + (lane % PL);
+        const bool has = (has_mask >> ln) & 1u;
+        const int qr = PR * rbk + pr;
         const int q = min(qr, n - 1);
-        const uint32_t *col = val0 + ln;
-        int r_best = q;
-        uint32_t kbest = col[q * kIdxRowW];
-        float fbest = __builtin_bit_cast(float, kbest);
-        if (!has) {                                   // nothing to find: stop at once
-            kbest = 0;
-            fbest = 0.0f;
-        }
-        int d0 = 1;
-        if constexpr (SAMP) {
-            // Unrolled blocks while every read of the patch stays in the tile
-            // (guard rows included); the loop below takes over from d0.
-            const int q_lo = kIdxPatch * rbk, q_hi = min(q_lo + kIdxPatch - 1, n - 1);
-            const int room = min(q_lo + kIdxGuard, n - 1 + kIdxGuard - q_hi);
-            int roff = 0;
-            if (room >= 16) search_samp<0, 4>(col + (q - 16) * kIdxRowW, w, fbest, roff, d0);
-            else if (room >= 12) search_samp<0, 3>(col + (q - 12) * kIdxRowW, w, fbest, roff, d0);
-            else if (room >= 8) search_samp<0, 2>(col + (q - 8) * kIdxRowW, w, fbest, roff, d0);
-            else if (room >= 4) search_samp<0, 1>(col + (q - 4) * kIdxRowW, w, fbest, roff, d0);
-            r_best = q + roff;
-        }
-        for (int d = d0;; d += 4) {
+        const int cb = int(lds_byte_addr(val0 + ln));          // row 0 of this lane's line
+        const int lo_min = cb - kIdxGuard * kRB;               // first guard row above the line
+        const uint32_t hi_max = uint32_t(cb + n * kRB);        // first guard row below it
+        // best value (sampled: float bits, ordered as unsigned integers for
+        // values >= 0) or key; nothing to find: 0, which stops at once
+        uint32_t best = has ? lds_word(uint32_t(cb + q * kRB)) : 0u;
+        int bd = 0;                                            // sampled: block of the best (0: own row)
+        uint32_t cbk[4] = {0u, 0u, 0u, 0u};                    // sampled: that block's four candidates
+        int lo = cb + (q - 4) * kRB;                           // row q - d - 3 at d = 1
+        uint32_t hi = uint32_t(cb + (q + 1) * kRB);            // row q + d at d = 1
+        // sampled: the weights of the block ahead, read one block early
+        float4 ad = SAMP ? *reinterpret_cast<const float4 *>(step + 1) : float4{};
+        for (int d = 1; d <= n; d += 4) {
             bool done;
-            if (SAMP) done = w * float(d) * float(d) > fbest;
-            else done = (uint64_t(uint32_t(d) * uint32_t(d)) << a.rbits) > uint64_t(kbest);
-            if (__all(done) || d > n) break;
+            if (SAMP) done = ad.x > __builtin_bit_cast(float, best);
+            else done = (uint64_t(uint32_t(d) * uint32_t(d)) << a.rbits) > uint64_t(best);
+            if (__all(done)) break;
+            const uint32_t lb = uint32_t(max(lo, lo_min)), hb = min(hi, hi_max);
+            uint32_t c[4];
+            if constexpr (SAMP) {
+                const float adk[4] = {ad.x, ad.y, ad.z, ad.w};
+                ad = *reinterpret_cast<const float4 *>(step + d + 4);
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const int dd = d + s;
-                const int lo = max(q - dd, -kIdxGuard), hi = min(q + dd, n + kIdxGuard - 1);
-                const uint32_t u = col[lo * kIdxRowW], v = col[hi * kIdxRowW];
-                if (SAMP) {
-                    const float add = w * float(dd) * float(dd);
-                    const float cu = __builtin_bit_cast(float, u) + add;
-                    const float cv = __builtin_bit_cast(float, v) + add;
-                    if (cu < fbest) {
-                        fbest = cu;
-                        r_best = q - dd;
-                    }
-                    if (cv < fbest) {
-                        fbest = cv;
-                        r_best = q + dd;
-                    }
-                } else {
-                    // keys of "no site" stay above every real key
-                    const uint32_t add = uint32_t(dd * dd) << a.rbits;
-                    const uint32_t cu = u == uint32_t(kInfI) ? u : u + add;
-                    const uint32_t cv = v == uint32_t(kInfI) ? v : v + add;
-                    kbest = min(kbest, min(cu, cv));
-                }
+                for (int k = 0; k < 4; ++k)
+                    c[k] = __builtin_bit_cast(uint32_t,
+                                              __builtin_bit_cast(float, min(lds_word(lb + (3 - k) * kRB),
+                                                                            lds_word(hb + k * kRB))) + adk[k]);
+                const uint32_t m = min(min(c[0], c[1]), min(c[2], c[3]));
+                const bool imp = m < best;
+                bd = imp ? d : bd;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) cbk[k] = imp ? c[k] : cbk[k];
+                best = min(best, m);
+            } else {
+                // "none" keys (0x7fffffff) plus a weight stay above every real
+                // key, which is below 2^31 with its weight (no wrap: the
+                // weights are below 2^31)
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    c[k] = min(lds_word(lb + (3 - k) * kRB), lds_word(hb + k * kRB)) +
+                           (uint32_t((d + k) * (d + k)) << a.rbits);
+                best = min(best, min(min(c[0], c[1]), min(c[2], c[3])));
             }
+            lo -= 4 * kRB;
+            hi += 4 * kRB;
+        }
+        // sampled: the row of the best value.  Its step e = bd + k is the
+        // first of the block's candidates equal to it; the row is q - e when
+        // that row's own candidate equals it (same operands, same sum), else
+        // q + e.  A row q - e above the first guard row reads that guard row
+        // ("none").
+        int r_best = q;
+        if (SAMP && bd > 0) {
+            int k = 3;
+#pragma unroll
+            for (int j = 2; j >= 0; --j) k = cbk[j] == best ? j : k;
+            const int e = bd + k;
+            const float ce = __builtin_bit_cast(float, lds_word(uint32_t(max(cb + (q - e) * kRB, lo_min)))) + step[e];
+            r_best = __builtin_bit_cast(uint32_t, ce) == best ? q - e : q + e;
         }
         if (qr >= n) continue;
         // ---- output of element (row qr, line ln) ----------------------------
         const uint4 li = line_info[ln];
         if (!li.w) continue;
+        int32_t site = -1;
+        if (has) {
+            const int rw = SAMP ? r_best : int(best & rmask);
+            site = site0[rw * kIdxRowW + ln];
+        }
+        if constexpr (FAST) {
+            const uint32_t ro = uint32_t(qr) * a.inner * 4u;   // byte offset of row qr
+            const uint32_t co = li.x + ro;                     // the element in slice 0 of the carrier
+            if (!FINAL) {
+                __builtin_amdgcn_raw_buffer_store_b32(uint32_t(site), rc, co, 0, 0);
+                continue;
+            }
+            const float fbest = __builtin_bit_cast(float, best);
+            double d2;
+            if (site >= 0) {
+                d2 = SAMP ? double(fbest) : double(best >> a.rbits);
+                if (a.coords) {
+#pragma unroll
+                    for (int b = 0; b < ND; ++b)
+                        __builtin_amdgcn_raw_buffer_store_b32((uint32_t(site) >> a.sh[b]) & a.msk[b], rc, co,
+                                                              uint32_t(b) * a.vox * 4u, 0);
+                }
+            } else {
+                // no background in the sample: the virtual element (-1, 0, ..., 0)
+                d2 = SAMP ? virtual_sq<double>(qr, li.z, nd, a.shape, a.wall)
+                          : double(virtual_sq<int64_t>(qr, li.z, nd, a.shape, a.wall));
+                if (a.coords) {
+#pragma unroll
+                    for (int b = 0; b < ND; ++b)
+                        __builtin_amdgcn_raw_buffer_store_b32(b == 0 ? 0xffffffffu : 0u, rc, co,
+                                                              uint32_t(b) * a.vox * 4u, 0);
+                }
+            }
+            const float dist = (SAMP && site >= 0)                ? sqrtf(fbest)
+                               : (!SAMP && d2 < 16777216.0) ? sqrt_rn_int(uint32_t(d2))
+                                                            : float(sqrt(d2));
+            if (a.dist) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, dist), rd, li.y + ro, 0, 0);
+            if (a.sq) __builtin_amdgcn_raw_buffer_store_b32(uint32_t(int32_t(d2)), rs, li.y + ro, 0, 0);
+            continue;
+        }
         Line l;
         l.s = li.x;
         l.base = li.y;
         l.i = li.z;
         slice0 = a.idx + uint64_t(l.s) * a.cstride;
         const uint64_t e = uint64_t(l.base) + uint64_t(qr) * a.inner;   // in-sample flat
-        int32_t site = -1;
-        if (has) {
-            const int rw = SAMP ? r_best : int(kbest & rmask);
-            site = site0[rw * kIdxRowW + ln];
-        }
         if (!FINAL) {
             slice0[e] = site;
             continue;
@@ -278,10 +376,11 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         // final pass: coordinates, distance, squared distance (with the
         // carrier in a distance output, the distance replaces the carried
         // site in place: this workgroup staged every row of its lines)
+        const float fbest = __builtin_bit_cast(float, best);
         double d2;
         if (site >= 0) {
             if (SAMP) d2 = double(fbest);
-            else d2 = double(kbest >> a.rbits);
+            else d2 = double(best >> a.rbits);
             if (a.coords) {
                 uint32_t t2 = uint32_t(site);
 #pragma unroll
