@@ -91,6 +91,7 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
     // per line: sample and base of row 0 in slice 0 (FAST: byte offsets of
     // row 0 in the carrier and in the outputs), position i, live
     __shared__ uint4 line_info[kIdxLines];
+    __shared__ uint32_t line_pos0[kIdxLines];  // per line: position o along the earlier axes
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
@@ -107,7 +108,7 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
     // along the later axes.
     struct Line {
         bool live;
-        uint32_t s, base, i;
+        uint32_t s, base, i, o;
     };
     auto line_of = [&](int j) {
         Line l;
@@ -118,23 +119,36 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         const uint32_t r = LL - l.s * a.lps;
         const uint32_t o = a.div_inner.div(r);
         l.i = r - o * a.inner;
+        l.o = o;                                // position along the earlier axes
         l.base = o * a.n * a.inner + l.i;       // in-sample flat of row 0
         return l;
     };
-    // Coordinates along the axes after `ax` of the position i of this lane's
-    // line (staging), computed once.
+    // Axes whose distances the carried sites already hold.  In the generic
+    // kernel the passes run from the last axis to axis 0, so those are the
+    // axes after `ax`.  With the rank built in, a pass along axis AX follows
+    // the last-axis scan, and the final pass every other axis: for rank 3 a
+    // non-final pass along either strided axis has the last axis behind it.
+    auto proc = [&](int b) -> bool {
+        if constexpr (ND > 0) return b != AX && (b == ND - 1 || FINAL);
+        else return b > ax && b < nd;
+    };
+    // Coordinates of this lane's line along the processed axes (staging),
+    // computed once: those after `ax` from its position i along them, those
+    // before from its position o along them (rank 3: o is the coordinate
+    // along axis 0).
     int xc[kMaxDim] = {};
     float wf[kMaxDim] = {};
-    auto line_coords = [&](uint32_t xi) {
+    auto line_coords = [&](uint32_t xi, uint32_t xo) {
 #pragma unroll
         for (int b = kMaxDim - 1; b >= 0; --b) {
             if (b > ax && b < nd) {
                 const uint32_t qx = a.div_shape[b].div(xi);
                 xc[b] = int(xi - qx * a.div_shape[b].d);
-                wf[b] = float(a.wall[b]);
                 xi = qx;
             }
+            if (b < nd && proc(b)) wf[b] = float(a.wall[b]);
         }
+        if constexpr (ND == 3 && AX == 1) xc[0] = int(xo);
     };
     // squared distance over the axes after `ax` between this lane's line and
     // site y (in-sample flat; its coordinates along those axes are its
@@ -150,20 +164,35 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         uint32_t acci = 0;
 #pragma unroll
         for (int b = kMaxDim - 1; b >= 0; --b) {
-            if (b > ax && b < nd) {
-                int dy;
-                if constexpr (FAST) {
-                    dy = int((uint32_t(y) >> a.sh[b]) & a.msk[b]) - xc[b];
-                } else {
-                    const uint32_t qy = a.div_shape[b].div(yi);
-                    dy = int(yi - qy * a.div_shape[b].d) - xc[b];
-                    yi = qy;
+            // (rank 3, final pass along axis 1: axis 0 is the quotient left)
+            const bool need = b < nd && (ND == 3 && AX == 1 && FINAL ? true : b > ax);
+            if (need) {
+                const uint32_t qy = b > 0 ? a.div_shape[b].div(yi) : 0u;
+                const int dy = int(yi - qy * a.div_shape[b].d) - xc[b];
+                yi = qy;
+                if (proc(b)) {
+                    if (SAMP) accf += wf[b] * float(dy * dy);
+                    else acci += uint32_t(dy * dy);
                 }
-                if (SAMP) accf += wf[b] * float(dy * dy);
-                else acci += uint32_t(dy * dy);
             }
         }
         key_or_bits = SAMP ? __builtin_bit_cast(uint32_t, accf) : ((acci << a.rbits) | uint32_t(q));
+    };
+
+    // Squared distance from element (row q of a line at positions i, o) to
+    // the virtual background element (-1, 0, ..., 0), for samples without
+    // background (double when sampled, exact integers otherwise).
+    auto virtual_d2 = [&](int q, uint32_t i, uint32_t o) -> double {
+        if constexpr (ND == 3 && AX == 1) {
+            // x0 = o, x1 = q, x2 = i
+            if (SAMP)
+                return a.wall[0] * double(o + 1) * double(o + 1) + a.wall[1] * double(q) * double(q) +
+                       a.wall[2] * double(i) * double(i);
+            return double(int64_t(o + 1) * (o + 1) + int64_t(q) * q + int64_t(i) * i);
+        } else {
+            return SAMP ? virtual_sq<double>(q, i, nd, a.shape, a.wall)
+                        : double(virtual_sq<int64_t>(q, i, nd, a.shape, a.wall));
+        }
     };
 
     // ---- guard rows, step table and staging ---------------------------------
@@ -183,7 +212,8 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
     if (t < kIdxLines)
         line_info[sl] = FAST ? uint4{cvo, (me.s * a.vox + me.base) * 4u, me.i, me.live ? 1u : 0u}
                              : uint4{me.s, me.base, me.i, me.live ? 1u : 0u};
-    line_coords(me.i);
+    line_coords(me.i, me.o);
+    if (t < kIdxLines) line_pos0[sl] = me.o;
     const int32_t *src = a.idx + uint64_t(me.s) * a.cstride + me.base;
     // FAST only (a null resource elsewhere)
     const __amdgpu_buffer_rsrc_t rc = make_rsrc(a.idx, FAST ? a.cbytes : 0u);
@@ -192,30 +222,62 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
     uint32_t seen = 0;
     constexpr int SB = 8;
     const uint32_t svo = cvo + uint32_t(sg) * a.inner * 4u;
-    for (int it = 0; it * kGroups * SB < n; ++it) {
-        const int q0 = sg + it * kGroups * SB;
-        int32_t y[SB];
+    if constexpr (FAST) {
+        // n is a multiple of 32 = kGroups, so every row test is uniform, and
+        // the values are computed without branches ("none" selected at the end)
+        const int32_t dead = me.live ? 0 : -1;
+        int32_t ymax = -1;
+        uint32_t *const vrow = val0 + sg * kIdxRowW + sl;
+        int32_t *const srow = site0 + sg * kIdxRowW + sl;
+        for (int it = 0; it * kGroups * SB < n; ++it) {
+            int32_t y[SB];
 #pragma unroll
-        for (int j = 0; j < SB; ++j) {
-            // FAST: n is a multiple of 32 = kGroups, so the rows of a load
-            // are all in the line or all past it (a uniform test)
-            if constexpr (FAST) {
+            for (int j = 0; j < SB; ++j) {
                 const int u = it * kGroups * SB + j * kGroups;
                 y[j] = u < n ? int32_t(__builtin_amdgcn_raw_buffer_load_b32(rc, svo, uint32_t(u) * a.inner * 4u, 0))
                              : -1;
-            } else
-                y[j] = src[uint64_t(min(q0 + j * kGroups, n - 1)) * a.inner];
-        }
+            }
 #pragma unroll
-        for (int j = 0; j < SB; ++j) {
-            const int q = q0 + j * kGroups;
-            if (q < n) {
-                const int32_t yy = me.live ? y[j] : -1;
-                uint32_t v;
-                carried(yy, v, q);
-                seen |= yy >= 0 ? 1u : 0u;
-                val0[q * kIdxRowW + sl] = v;
-                site0[q * kIdxRowW + sl] = yy;
+            for (int j = 0; j < SB; ++j) {
+                const int u = it * kGroups * SB + j * kGroups;
+                if (u < n) {
+                    const int32_t yy = y[j] | dead;
+                    float accf = 0.0f;
+                    uint32_t acci = 0;
+#pragma unroll
+                    for (int b = ND - 1; b >= 0; --b) {
+                        if (proc(b)) {
+                            const int dy = int((uint32_t(yy) >> a.sh[b]) & a.msk[b]) - xc[b];
+                            if (SAMP) accf += wf[b] * float(dy * dy);
+                            else acci += uint32_t(dy * dy);
+                        }
+                    }
+                    const uint32_t v = SAMP ? __builtin_bit_cast(uint32_t, accf) : ((acci << a.rbits) | uint32_t(sg + u));
+                    const uint32_t none = SAMP ? __builtin_bit_cast(uint32_t, __builtin_inff()) : uint32_t(kInfI);
+                    ymax = max(ymax, yy);
+                    vrow[u * kIdxRowW] = yy < 0 ? none : v;
+                    srow[u * kIdxRowW] = yy;
+                }
+            }
+        }
+        seen = ymax >= 0 ? 1u : 0u;
+    } else {
+        for (int it = 0; it * kGroups * SB < n; ++it) {
+            const int q0 = sg + it * kGroups * SB;
+            int32_t y[SB];
+#pragma unroll
+            for (int j = 0; j < SB; ++j) y[j] = src[uint64_t(min(q0 + j * kGroups, n - 1)) * a.inner];
+#pragma unroll
+            for (int j = 0; j < SB; ++j) {
+                const int q = q0 + j * kGroups;
+                if (q < n) {
+                    const int32_t yy = me.live ? y[j] : -1;
+                    uint32_t v;
+                    carried(yy, v, q);
+                    seen |= yy >= 0 ? 1u : 0u;
+                    val0[q * kIdxRowW + sl] = v;
+                    site0[q * kIdxRowW + sl] = yy;
+                }
             }
         }
     }
@@ -270,17 +332,19 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         int lo = cb + (q - 4) * kRB;                           // row q - d - 3 at d = 1
         uint32_t hi = uint32_t(cb + (q + 1) * kRB);            // row q + d at d = 1
         // sampled: the weights of the block ahead, read one block early
-        float4 ad = SAMP ? *reinterpret_cast<const float4 *>(step + 1) : float4{};
-        for (int d = 1; d <= n; d += 4) {
+        // One block of four steps d .. d+3; true when the search is over.
+        // Sampled: `cur` holds the block's weights, and `nxt` receives the
+        // next block's (read one block early; the two registers alternate).
+        auto block = [&](int d, const float4 &cur, float4 &nxt) -> bool {
             bool done;
-            if (SAMP) done = ad.x > __builtin_bit_cast(float, best);
+            if (SAMP) done = cur.x > __builtin_bit_cast(float, best);
             else done = (uint64_t(uint32_t(d) * uint32_t(d)) << a.rbits) > uint64_t(best);
-            if (__all(done)) break;
+            if (d > n || __all(done)) return true;
             const uint32_t lb = uint32_t(max(lo, lo_min)), hb = min(hi, hi_max);
             uint32_t c[4];
             if constexpr (SAMP) {
-                const float adk[4] = {ad.x, ad.y, ad.z, ad.w};
-                ad = *reinterpret_cast<const float4 *>(step + d + 4);
+                const float adk[4] = {cur.x, cur.y, cur.z, cur.w};
+                nxt = *reinterpret_cast<const float4 *>(step + d + 4);
 #pragma unroll
                 for (int k = 0; k < 4; ++k)
                     c[k] = __builtin_bit_cast(uint32_t,
@@ -304,6 +368,12 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
             }
             lo -= 4 * kRB;
             hi += 4 * kRB;
+            return false;
+        };
+        float4 adA = SAMP ? *reinterpret_cast<const float4 *>(step + 1) : float4{}, adB{};
+        for (int d = 1;; d += 8) {
+            if (block(d, adA, adB)) break;
+            if (block(d + 4, adB, adA)) break;
         }
         // sampled: the row of the best value.  Its step e = bd + k is the
         // first of the block's candidates equal to it; the row is q - e when
@@ -347,8 +417,7 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
                 }
             } else {
                 // no background in the sample: the virtual element (-1, 0, ..., 0)
-                d2 = SAMP ? virtual_sq<double>(qr, li.z, nd, a.shape, a.wall)
-                          : double(virtual_sq<int64_t>(qr, li.z, nd, a.shape, a.wall));
+                d2 = virtual_d2(qr, li.z, line_pos0[ln]);
                 if (a.coords) {
 #pragma unroll
                     for (int b = 0; b < ND; ++b)
@@ -398,8 +467,7 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
             }
         } else {
             // no background in the sample: the virtual element (-1, 0, ..., 0)
-            d2 = virtual_sq<double>(qr, l.i, nd, a.shape, a.wall);
-            if (!SAMP) d2 = double(virtual_sq<int64_t>(qr, l.i, nd, a.shape, a.wall));
+            d2 = virtual_d2(qr, l.i, line_pos0[ln]);
             if (a.coords) {
                 slice0[e] = -1;
                 for (int b = 1; b < nd; ++b) slice0[uint64_t(b) * a.vox + e] = 0;

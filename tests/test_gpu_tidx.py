@@ -1,8 +1,9 @@
 """GPU parity of the tiled passes on the index carrier (k_tile_idx) in each of
-their forms: rank 2 and 3 with the rank built in, with shift-and-mask
-coordinates and 32-bit buffer offsets when every extent after axis 0 is a
-power of two and the line length a multiple of 32, or with divisions
-otherwise; and the generic form for other ranks.  Every case checks that the
+their forms: rank 2 and 3 with the rank built in (sampled rank 3 in either
+pass order), with shift-and-mask coordinates and 32-bit buffer offsets when
+every extent after axis 0 is a power of two and the line length a multiple of
+32, or with divisions otherwise; and the generic form for other ranks.  Every
+case checks that the
 tiled passes ran, and compares with the oracle element by element: unit
 sampling bit-exact with the canonical indices, sampled within 1e-5 / 1e-6
 with every index a nearest background element.
@@ -15,7 +16,8 @@ from oracle import edt_oracle
 
 pytestmark = pytest.mark.gpu
 
-ANISO3 = (2.5, 0.8, 0.8)
+ANISO3 = (2.5, 0.8, 0.8)      # rank 3, axis 0 weighs most: axis 0 runs first, axis 1 last
+ANISO3B = (0.8, 2.5, 1.0)     # axis 1 weighs most: the default order (axis 1, then axis 0)
 
 
 def rand_mask(shape, p_bg, seed):
@@ -57,6 +59,8 @@ def test_fast_tiles(shape, p_bg, ndim):
     parity_tidx(mask, ndim, samp, tag="sampled")
     # distances only: the flat-index carrier runs inside the distance output
     parity_tidx(mask, ndim, samp, dist=True, idx=False, sq=False, tag="sampled, distances only")
+    if ndim == 3:
+        parity_tidx(mask, ndim, ANISO3B, tag="sampled, default order")
 
 
 # divisions for the coordinates (extents that are not powers of two, or line
@@ -76,6 +80,8 @@ def test_general_tiles(shape, p_bg, ndim):
     parity_tidx(mask, ndim, None, tag="unit")
     parity_tidx(mask, ndim, samp, tag="sampled")
     parity_tidx(mask, ndim, samp, dist=True, idx=False, sq=False, tag="sampled, distances only")
+    if ndim == 3:
+        parity_tidx(mask, ndim, ANISO3B, tag="sampled, default order")
 
 
 def test_longest_searches_and_empty_samples():
@@ -87,6 +93,8 @@ def test_longest_searches_and_empty_samples():
     mask[2] = 0
     parity_tidx(mask, 3, None, tag="corner / none / all")
     parity_tidx(mask, 3, ANISO3, tag="corner / none / all, sampled")
+    parity_tidx(mask, 3, ANISO3B, tag="corner / none / all, sampled, default order")
     m2 = np.ones((2, 33, 40, 50), np.uint8)            # the same with divisions
     m2[0, 0, 39, 0] = 0
     parity_tidx(m2, 3, ANISO3, tag="corner / none, divisions, sampled")
+    parity_tidx(m2, 3, ANISO3B, tag="corner / none, divisions, sampled, default order")
