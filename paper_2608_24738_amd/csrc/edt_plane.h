@@ -390,6 +390,8 @@ __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) 
 // ---------------------------------------------------------------------------
 // Exact transform of one 128 x 128 plane per workgroup, from the axis-0
 // distances of k_col_scan (bytes: 0 .. 127, 255 for none).
+// Values of 65025 (255^2) and above are "none": no site found yet.
+constexpr uint32_t kPsNone = 255u * 255u;
 // ---------------------------------------------------------------------------
 struct PlaneEdtArgs {
     const uint8_t *bytes;  // plane p's axis-0 bytes at byte offset 65536 p (inside dist or sq)
@@ -422,16 +424,21 @@ __global__ void __launch_bounds__(kPsThreads, 8) k_plane_edt(PlaneEdtArgs a) {
         const uint4 v = *reinterpret_cast<const uint4 *>(a.bytes + uint64_t(p) * 65536u + 16u * uint32_t(t));
         const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
         const int o = ((t >> 3) + kPsG) * kPsRS + 8 * (t & 7);
+        // two adjacent bytes spread into the halves of a word and squared in
+        // one packed multiply; "none" (255) becomes 65025, above every real
+        // squared distance of the plane (at most 3 x 127^2 = 48387)
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
-            const uint32_t b0 = (w4[k >> 1] >> (16 * (k & 1))) & 0xffu;
-            const uint32_t b1 = (w4[k >> 1] >> (16 * (k & 1) + 8)) & 0xffu;
-            tA[o + k] = (b0 == 255u ? 0xffffu : b0 * b0) | ((b1 == 255u ? 0xffffu : b1 * b1) << 16);
+            const u16x2 b = as_pair(__builtin_amdgcn_perm(0u, w4[k >> 1], (k & 1) ? 0x0c030c02u : 0x0c010c00u));
+            tA[o + k] = as_word(b * b);
         }
-        for (int i = t; i < 2 * 2 * kPsG * kPsRS; i += kPsThreads) {
-            const int tile = i / (2 * kPsG * kPsRS), k = i % (2 * kPsG * kPsRS);
-            const int row = k / kPsRS, col = k % kPsRS;
-            ps_lds[tile * kPsRows * kPsRS + (row < kPsG ? row : kPsN + row) * kPsRS + col] = 0xffffffffu;
+        // guard rows: four above and four below each tile
+        if (t < kPsG * kPsRS) {
+            constexpr int kBottom = (kPsN + kPsG) * kPsRS;
+            tA[t] = 0xffffffffu;
+            tA[kBottom + t] = 0xffffffffu;
+            tB[t] = 0xffffffffu;
+            tB[kBottom + t] = 0xffffffffu;
         }
         for (int i = t; i < LUT; i += kPsThreads) lut[i] = __builtin_bit_cast(uint32_t, sqrt_rn_int(uint32_t(i)));
         if (t < 2) claim[t] = 0;
@@ -469,14 +476,14 @@ __global__ void __launch_bounds__(kPsThreads, 8) k_plane_edt(PlaneEdtArgs a) {
         ps_search<false>(tB, tB, c, 8 * pc + jw, fA, fB);
         // fA = (row r0, row r0+1) at column c; fB the same at column c + 1
         uint32_t d2[4] = {fA.x, fB.x, fA.y, fB.y};   // (r0, c), (r0, c+1), (r0+1, c), (r0+1, c+1)
-        // no background in the whole sample (every value "none"): distances to
-        // the virtual element (-1, 0, 0)
+        // no background in the whole sample (every value "none", at least
+        // 65025): distances to the virtual element (-1, 0, 0)
         const u16x2 mx = __builtin_elementwise_max(fA, fB);
-        if (__any(mx.x == 0xffffu || mx.y == 0xffffu)) {
+        if (__any(mx.x >= kPsNone || mx.y >= kPsNone)) {
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const uint32_t r = uint32_t(r0 + (k >> 1)), cc = uint32_t(c + (k & 1));
-                if (d2[k] == 0xffffu) d2[k] = (x0 + 1) * (x0 + 1) + r * r + cc * cc;
+                if (d2[k] >= kPsNone) d2[k] = (x0 + 1) * (x0 + 1) + r * r + cc * cc;
             }
         }
         const bool small = mx.x < uint32_t(LUT) && mx.y < uint32_t(LUT);
