@@ -29,9 +29,8 @@ namespace tmedt {
 
 constexpr int kIdxWaves = 16;
 constexpr int kIdxLines = 32;     // lines per workgroup
-constexpr int kIdxGuard = 4;       // guard rows of "no site" per side
+constexpr int kIdxGuard = 5;       // guard rows of "no site" per side (a block reads 5 rows per side)
 constexpr int kIdxRowW = kIdxLines + 4;  // padded row stride (words)
-constexpr int kIdxPatch = 8;       // patch: 8 rows x 8 lines (PR x 64 / PR in general)
 
 struct IdxTileArgs {
     int32_t *idx;            // the carrier of the sites: slice 0 of [batch][ndim][vox], or a
@@ -76,11 +75,12 @@ __host__ __device__ constexpr size_t idx_tile_lds(uint32_t n, bool samp) {
 // FAST (ND > 0 only): coordinates by shifts and masks, and every global
 // access through a buffer resource with a 32-bit byte offset, the row and
 // slice parts of which are wave-uniform scalar offsets.
-// Rows of a search patch (its lines: 64 / rows).  FAST passes take 2 rows of
-// 32 lines, so each store instruction writes two whole 128-byte segments
-// (2 x 256^3 sampled with indices: final pass 171 -> 145 us, middle pass
-// 117 -> 109 us against 8 x 8 patches); the others keep 8 x 8.
-__host__ __device__ constexpr int idx_patch_rows(bool fast) { return fast ? 2 : 8; }
+// Lines of a search patch (a lane takes two adjacent rows of one line, so a
+// patch has 128 / lines rows).  FAST passes take 32 lines, so each store
+// instruction writes two whole 128-byte segments (2 x 256^3 sampled with
+// indices, one row per lane: final pass 171 -> 145 us, middle pass 117 ->
+// 109 us against 8 x 8 patches); the others take 8.
+__host__ __device__ constexpr int idx_patch_lines(bool fast) { return fast ? 32 : 8; }
 
 template <bool SAMP, bool FINAL, int ND = 0, int AX = 0, bool FAST = false>
 __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
@@ -294,105 +294,12 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         has_mask |= h.x | h.y | h.z | h.w;
     }
 
-    // ---- search and output, patch by patch ----------------------------------
-    // Patch p = (row block rb = p / L, line block (p + rb) % L) with L =
-    // kIdxLines / 8; lane l takes row 8 rb + l / 8 of line 8 cb + l % 8.
-    //
-    // The search runs in blocks of four steps d .. d+3.  A block reads rows
-    // q-d-3 .. q-d and q+d .. q+d+3 at fixed offsets from two LDS byte
-    // addresses that step by four rows per block and are clamped to the
-    // first guard row above and the first one below the line: a clamped
-    // block lies wholly past that end of the line, where every candidate is
-    // "none" and the guard rows it then reads are "none" too.  The candidate
-    // of step e is the smaller of the two rows at distance e plus the weight
-    // of e (for unit keys the minimum of the two keys, whose low bits keep
-    // the row).
-    constexpr int kRB = kIdxRowW * 4;              // row stride in bytes
-    constexpr int PR = idx_patch_rows(FAST);   // rows of a patch
-    constexpr int PL = kWave / PR;                 // lines of a patch
-    const int pr = lane / PL;
+    // ---- output of element (row qr, line ln) --------------------------------
     const uint32_t rmask = (1u << a.rbits) - 1u;
-    constexpr int kLB = kIdxLines / PL;            // line blocks
-    const int npatch = kLB * ((n + PR - 1) / PR);
     int32_t *slice0 = nullptr;
-    for (int p = wv; p < npatch; p += kIdxWaves) {
-        const int rbk = p / kLB;
-        const int ln = PL * ((p + rbk) % kLB) + (lane % PL);
-        const bool has = (has_mask >> ln) & 1u;
-        const int qr = PR * rbk + pr;
-        const int q = min(qr, n - 1);
-        const int cb = int(lds_byte_addr(val0 + ln));          // row 0 of this lane's line
-        const int lo_min = cb - kIdxGuard * kRB;               // first guard row above the line
-        const uint32_t hi_max = uint32_t(cb + n * kRB);        // first guard row below it
-        // best value (sampled: float bits, ordered as unsigned integers for
-        // values >= 0) or key; nothing to find: 0, which stops at once
-        uint32_t best = has ? lds_word(uint32_t(cb + q * kRB)) : 0u;
-        int bd = 0;                                            // sampled: block of the best (0: own row)
-        uint32_t cbk[4] = {0u, 0u, 0u, 0u};                    // sampled: that block's four candidates
-        int lo = cb + (q - 4) * kRB;                           // row q - d - 3 at d = 1
-        uint32_t hi = uint32_t(cb + (q + 1) * kRB);            // row q + d at d = 1
-        // sampled: the weights of the block ahead, read one block early
-        // One block of four steps d .. d+3; true when the search is over.
-        // Sampled: `cur` holds the block's weights, and `nxt` receives the
-        // next block's (read one block early; the two registers alternate).
-        auto block = [&](int d, const float4 &cur, float4 &nxt) -> bool {
-            bool done;
-            if (SAMP) done = cur.x > __builtin_bit_cast(float, best);
-            else done = (uint64_t(uint32_t(d) * uint32_t(d)) << a.rbits) > uint64_t(best);
-            if (d > n || __all(done)) return true;
-            const uint32_t lb = uint32_t(max(lo, lo_min)), hb = min(hi, hi_max);
-            uint32_t c[4];
-            if constexpr (SAMP) {
-                const float adk[4] = {cur.x, cur.y, cur.z, cur.w};
-                nxt = *reinterpret_cast<const float4 *>(step + d + 4);
-#pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    c[k] = __builtin_bit_cast(uint32_t,
-                                              __builtin_bit_cast(float, min(lds_word(lb + (3 - k) * kRB),
-                                                                            lds_word(hb + k * kRB))) + adk[k]);
-                const uint32_t m = min(min(c[0], c[1]), min(c[2], c[3]));
-                const bool imp = m < best;
-                bd = imp ? d : bd;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) cbk[k] = imp ? c[k] : cbk[k];
-                best = min(best, m);
-            } else {
-                // "none" keys (0x7fffffff) plus a weight stay above every real
-                // key, which is below 2^31 with its weight (no wrap: the
-                // weights are below 2^31)
-#pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    c[k] = min(lds_word(lb + (3 - k) * kRB), lds_word(hb + k * kRB)) +
-                           (uint32_t((d + k) * (d + k)) << a.rbits);
-                best = min(best, min(min(c[0], c[1]), min(c[2], c[3])));
-            }
-            lo -= 4 * kRB;
-            hi += 4 * kRB;
-            return false;
-        };
-        float4 adA = SAMP ? *reinterpret_cast<const float4 *>(step + 1) : float4{}, adB{};
-        for (int d = 1;; d += 8) {
-            if (block(d, adA, adB)) break;
-            if (block(d + 4, adB, adA)) break;
-        }
-        // sampled: the row of the best value.  Its step e = bd + k is the
-        // first of the block's candidates equal to it; the row is q - e when
-        // that row's own candidate equals it (same operands, same sum), else
-        // q + e.  A row q - e above the first guard row reads that guard row
-        // ("none").
-        int r_best = q;
-        if (SAMP && bd > 0) {
-            int k = 3;
-#pragma unroll
-            for (int j = 2; j >= 0; --j) k = cbk[j] == best ? j : k;
-            const int e = bd + k;
-            const float ce = __builtin_bit_cast(float, lds_word(uint32_t(max(cb + (q - e) * kRB, lo_min)))) + step[e];
-            r_best = __builtin_bit_cast(uint32_t, ce) == best ? q - e : q + e;
-        }
-        if (qr >= n) continue;
-        // ---- output of element (row qr, line ln) ----------------------------
+    auto output = [&](int qr, int ln, bool has, uint32_t best, int r_best) {
         const uint4 li = line_info[ln];
-        if (!li.w) continue;
+        if (!li.w) return;
         int32_t site = -1;
         if (has) {
             const int rw = SAMP ? r_best : int(best & rmask);
@@ -403,7 +310,7 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
             const uint32_t co = li.x + ro;                     // the element in slice 0 of the carrier
             if (!FINAL) {
                 __builtin_amdgcn_raw_buffer_store_b32(uint32_t(site), rc, co, 0, 0);
-                continue;
+                return;
             }
             const float fbest = __builtin_bit_cast(float, best);
             double d2;
@@ -430,7 +337,7 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
                                                             : float(sqrt(d2));
             if (a.dist) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, dist), rd, li.y + ro, 0, 0);
             if (a.sq) __builtin_amdgcn_raw_buffer_store_b32(uint32_t(int32_t(d2)), rs, li.y + ro, 0, 0);
-            continue;
+            return;
         }
         Line l;
         l.s = li.x;
@@ -440,7 +347,7 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         const uint64_t e = uint64_t(l.base) + uint64_t(qr) * a.inner;   // in-sample flat
         if (!FINAL) {
             slice0[e] = site;
-            continue;
+            return;
         }
         // final pass: coordinates, distance, squared distance (with the
         // carrier in a distance output, the distance replaces the carried
@@ -481,6 +388,122 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
                                                         : float(sqrt(d2));
         if (a.dist) a.dist[uint64_t(l.s) * a.vox + e] = dist;
         if (a.sq) a.sq[uint64_t(l.s) * a.vox + e] = int32_t(d2);
+    };
+
+    // ---- search and output, patch by patch ----------------------------------
+    // Patch p = (row block rb = p / L, line block (p + rb) % L), with PL
+    // lines (L = kIdxLines / PL line blocks) and PR = 128 / PL rows: lane l
+    // takes rows PR rb + 2 (l / PL) and the next one of line PL cb + l % PL.
+    //
+    // The search runs in blocks of four steps d .. d+3.  For the lane's two
+    // rows q and q + 1 a block reads rows q-d-3 .. q-d+1 and q+d .. q+d+4 at
+    // fixed offsets from two LDS byte addresses that step by four rows per
+    // block and are clamped to the first guard row above and the first one
+    // below the line: a clamped block lies wholly past that end of the line,
+    // where every candidate is "none" and the guard rows it then reads are
+    // "none" too.  The candidate of step e is the smaller of the two rows at
+    // distance e plus the weight of e (for unit keys the minimum of the two
+    // keys, whose low bits keep the row).
+    constexpr int kRB = kIdxRowW * 4;              // row stride in bytes
+    constexpr int PL = idx_patch_lines(FAST);      // lines of a patch
+    constexpr int PR = 2 * kWave / PL;             // rows of a patch
+    const int pr = 2 * (lane / PL);
+    constexpr int kLB = kIdxLines / PL;            // line blocks
+    const int npatch = kLB * ((n + PR - 1) / PR);
+    for (int p = wv; p < npatch; p += kIdxWaves) {
+        const int rbk = p / kLB;
+        const int ln = PL * ((p + rbk) % kLB) + (lane % PL);
+        const bool has = (has_mask >> ln) & 1u;
+        const int qr = PR * rbk + pr;                          // the lane's rows qr, qr + 1
+        const int q = min(qr, n - 1);
+        const int cb = int(lds_byte_addr(val0 + ln));          // row 0 of this lane's line
+        const int lo_min = cb - kIdxGuard * kRB;               // first guard row above the line
+        const uint32_t hi_max = uint32_t(cb + n * kRB);        // first guard row below it
+        // best values (sampled: float bits, ordered as unsigned integers for
+        // values >= 0) or keys of rows q and q + 1; nothing to find, or a row
+        // past the line: 0, which stops at once
+        uint32_t best[2];
+        best[0] = has && qr < n ? lds_word(uint32_t(cb + q * kRB)) : 0u;
+        best[1] = has && qr + 1 < n ? lds_word(uint32_t(cb + (q + 1) * kRB)) : 0u;
+        int bd[2] = {0, 0};                                    // sampled: block of the best (0: own row)
+        uint32_t cbk[2][4] = {};                               // sampled: that block's four candidates
+        int lo = cb + (q - 4) * kRB;                           // row q - d - 3 at d = 1
+        uint32_t hi = uint32_t(cb + (q + 1) * kRB);            // row q + d at d = 1
+        // One block of four steps d .. d+3; true when the search is over.
+        // Sampled: `cur` holds the block's weights, and `nxt` receives the
+        // next block's (read one block early; the two registers alternate).
+        auto block = [&](int d, const float4 &cur, float4 &nxt) -> bool {
+            bool done;
+            const uint32_t bmax = max(best[0], best[1]);
+            if (SAMP) done = cur.x > __builtin_bit_cast(float, bmax);
+            else done = (uint64_t(uint32_t(d) * uint32_t(d)) << a.rbits) > uint64_t(bmax);
+            if (d > n || __all(done)) return true;
+            const uint32_t lb = uint32_t(max(lo, lo_min)), hb = min(hi, hi_max);
+            uint32_t U[5], W[5];
+#pragma unroll
+            for (int k = 0; k < 5; ++k) {
+                U[k] = lds_word(lb + k * kRB);                 // row q - d - 3 + k
+                W[k] = lds_word(hb + k * kRB);                 // row q + d + k
+            }
+            if constexpr (SAMP) {
+                const float adk[4] = {cur.x, cur.y, cur.z, cur.w};
+                nxt = *reinterpret_cast<const float4 *>(step + d + 4);
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    uint32_t c[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        c[k] = __builtin_bit_cast(uint32_t,
+                                                  __builtin_bit_cast(float, min(U[3 + h - k], W[k + h])) + adk[k]);
+                    const uint32_t m = min(min(c[0], c[1]), min(c[2], c[3]));
+                    const bool imp = m < best[h];
+                    bd[h] = imp ? d : bd[h];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) cbk[h][k] = imp ? c[k] : cbk[h][k];
+                    best[h] = min(best[h], m);
+                }
+            } else {
+                // "none" keys (0x7fffffff) plus a weight stay above every real
+                // key, which is below 2^31 with its weight (no wrap: the
+                // weights are below 2^31)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    uint32_t c[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        c[k] = min(U[3 + h - k], W[k + h]) + (uint32_t((d + k) * (d + k)) << a.rbits);
+                    best[h] = min(best[h], min(min(c[0], c[1]), min(c[2], c[3])));
+                }
+            }
+            lo -= 4 * kRB;
+            hi += 4 * kRB;
+            return false;
+        };
+        float4 adA = SAMP ? *reinterpret_cast<const float4 *>(step + 1) : float4{}, adB{};
+        for (int d = 1;; d += 8) {
+            if (block(d, adA, adB)) break;
+            if (block(d + 4, adB, adA)) break;
+        }
+        for (int h = 0; h < 2; ++h) {
+            const int qh = q + h;
+            // sampled: the row of the best value.  Its step e = bd + k is the
+            // first of the block's candidates equal to it; the row is qh - e
+            // when that row's own candidate equals it (same operands, same
+            // sum), else qh + e.  A row qh - e above the first guard row reads
+            // that guard row ("none").
+            int r_best = qh;
+            if (SAMP && bd[h] > 0) {
+                int k = 3;
+#pragma unroll
+                for (int j = 2; j >= 0; --j) k = cbk[h][j] == best[h] ? j : k;
+                const int e = bd[h] + k;
+                const float ce =
+                    __builtin_bit_cast(float, lds_word(uint32_t(max(cb + (qh - e) * kRB, lo_min)))) + step[e];
+                r_best = __builtin_bit_cast(uint32_t, ce) == best[h] ? qh - e : qh + e;
+            }
+            if (qr + h >= n) continue;
+            output(qr + h, ln, has, best[h], r_best);
+        }
     }
 }
 
