@@ -4,10 +4,13 @@
 //
 // Pass order (paper, Section 2.3.2: one 1-D pass per axis): the contiguous
 // last axis first, as a nearest-zero scan of the mask; then every strided
-// axis down to axis 0 as an in-place lower-envelope pass; the axis-0 pass
-// also writes the final outputs (square root, virtual background element,
-// coordinates).  Running axis 0 last makes the reported index the nearest
-// background element with the smallest row-major flat index.
+// axis down to axis 0 as an in-place exact pass; the last pass also writes
+// the final outputs (square root, virtual background element, coordinates).
+// Running axis 0 last makes the reported index the nearest background
+// element with the smallest row-major flat index.  Sampled rank-3 requests
+// on the index carrier may take their two strided axes in the other order
+// (any nearest element is correct there), and distance-only rank-3 requests
+// on 128 x 128 planes run axis 0 first (plane order).
 //
 // Two carriers: without indices the squared distance itself is carried in
 // the distance (or squared-distance) output; with indices the flat index of

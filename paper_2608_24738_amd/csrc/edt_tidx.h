@@ -8,8 +8,12 @@
 // the site's squared distance over the axes already processed, recomputed
 // from the site's coordinates.  Each element then runs the windowed exact
 // search over the rows of its line: examine rows at growing distance d and
-// stop once w d^2 exceeds the best value found.  The winner's site comes from
-// the staged copy, so the pass can overwrite its lines in place.
+// stop once w d^2 exceeds the best value found; a lane searches two adjacent
+// rows of one line, which share every row read.  The winner's site comes from
+// the staged copy, so the pass can overwrite its lines in place.  The axes
+// already processed are those after the pass axis (passes from the last axis
+// down), or, with the rank built in, the last axis and, in the final pass,
+// every other axis (rank 3 may take its two strided axes in either order).
 //
 // Unit sampling: values are exact integers and a candidate is the key
 // (value << RB) | row, so one integer minimum picks the smallest value and,
