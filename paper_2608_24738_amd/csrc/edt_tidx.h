@@ -154,10 +154,10 @@ __global__ void __launch_bounds__(kWave * kIdxWaves) k_tile_idx(IdxTileArgs a) {
         }
         if constexpr (ND == 3 && AX == 1) xc[0] = int(xo);
     };
-    // squared distance over the axes after `ax` between this lane's line and
-    // site y (in-sample flat; its coordinates along those axes are its
-    // remainders by the later extents), or "none" (sampled: float sum of the
-    // exact integer squares times the squared sampling)
+    // squared distance over the processed axes between this lane's line and
+    // site y (in-sample flat; its coordinate along axis b is its remainder by
+    // extent b after dividing by the later extents), or "none" (sampled:
+    // float sum of the exact integer squares times the squared sampling)
     auto carried = [&](int32_t y, uint32_t &key_or_bits, int q) {
         if (y < 0) {
             key_or_bits = SAMP ? __builtin_bit_cast(uint32_t, __builtin_inff()) : uint32_t(kInfI);
