@@ -79,7 +79,10 @@ typedef enum {
  * inside the line's own output storage, so nothing is allocated).
  *   out_dist  NULL, or [batch][shape...] float32 distances.
  *   out_idx   NULL, or [batch][ndim][shape...] int32 coordinates of the
- *             nearest background element.
+ *             nearest background element: with unit sampling the one with
+ *             the smallest row-major flat index among equally near ones,
+ *             otherwise one of the nearest (paper, Section 2.4: a genuine
+ *             nearest element); (-1, 0, ..., 0) for a sample without any.
  * At least one of out_dist and out_idx must be non-NULL.
  */
 int tm_edt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
