@@ -3,8 +3,9 @@
 
 Default workload: 3-D EDT of 8 x 1 x 128^3 uint8 masks whose foreground is the
 union of 30 random solid balls (radius 4-30 voxels) per volume, unit
-sampling, float32 distances.  One step = one tm_edt call over the whole batch
-with the mask already resident in HBM and the output preallocated.  On this
+sampling, float32 distances.  One step = one tm_edt_ws call over the whole
+batch with the mask already resident in HBM and the output (and the
+workspace, used by 2-D column passes only) preallocated.  On this
 shape the call runs two kernels: the axis-0 nearest-background scan straight
 from the mask, writing one byte per voxel ("col_scan.o8"), and one workgroup
 per 128 x 128 plane doing both remaining axes and the square root
@@ -88,6 +89,8 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
     if base in ("fh_index_final", "tile_idx_final", "fh_long_final"):
         # carrier in; coordinates (with indices) and distances out
         return total * (4 + (4 * ndim if want_idx else 0) + out_bytes)
+    if base == "order":                      # 8 bytes per group of 16 lines: not counted
+        return 0
     if base in ("cdt_l1_long", "cdt_l1_long_final"):
         return total * (4 + 4) * 2                       # two sweeps, each reads and writes
     raise KeyError(name)
@@ -404,9 +407,13 @@ def main():
     if w.want_idx:
         idx = torch.empty((w.batch, 1, ndim) + tuple(w.spatial), dtype=torch.int32, device=dev)
     samp = list(w.sampling) if w.sampling else None
+    # the workspace in which tm_edt_ws keeps a dispatch order (2-D column
+    # passes; none for the other workloads), allocated before timing
+    ws_bytes = binding.tm_edt_workspace_size(ndim, w.spatial, w.batch, samp, w.want_idx)
+    ws = torch.zeros(max(1, ws_bytes // 4), dtype=torch.int32, device=dev) if ws_bytes else None
 
     def step():
-        binding.tm_edt(x, ndim, samp, dist, idx, stream=stream)
+        binding.tm_edt_ws(x, ndim, samp, dist, idx, ws, stream=stream)
 
     # per-kernel durations: HIP events recorded by the library around each of
     # its launches, on the launch stream, over the same number of steps
@@ -435,6 +442,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "batch": w.batch, "channels": 1,
                    "spatial": list(w.spatial), "sampling": samp or "unit",
+                   "workspace_bytes": ws_bytes,
                    "outputs": "float32 distances" + (" + int32 indices" if w.want_idx else ""),
                    "mask_sha256": workloads.mask_digest(mask_np)[:16]},
         "roofline": roofline,

@@ -22,7 +22,8 @@
  *   - Memory: in_u8, out_* are DEVICE pointers owned by the caller; shape
  *     and sampling are HOST pointers read during the call only.  The library
  *     allocates no device memory; intermediate results live in the output
- *     buffers, which are overwritten in full.
+ *     buffers, which are overwritten in full (tm_edt_ws also uses the
+ *     caller's workspace).
  *   - Streams: all work is enqueued on `stream` (0 = the null stream) of the
  *     current device and the call returns without waiting for it.  Results
  *     are valid once that stream has been synchronised.  Calls are reentrant;
@@ -62,7 +63,9 @@ typedef enum {
     TM_ERR_UNSUPPORTED = -9, /* a line is longer than the signed or chessboard kernels hold */
     TM_ERR_HIP = -10,        /* the HIP runtime reported an error while enqueuing */
     TM_ERR_METRIC = -11,     /* metric is not one of tm_metric */
-    TM_ERR_DTYPE = -12       /* dtype is not one of tm_dtype */
+    TM_ERR_DTYPE = -12,      /* dtype is not one of tm_dtype */
+    TM_ERR_WORKSPACE = -13   /* workspace not 4-byte aligned, or (tm_edt_noalloc) the request's
+                                dispatch order needs more than the static workspace holds */
 } tm_status;
 
 /*
@@ -88,6 +91,48 @@ typedef enum {
 int tm_edt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
            const double *sampling, float *out_dist, int32_t *out_idx,
            hipStream_t stream);
+
+/*
+ * tm_edt_ws -- tm_edt with a caller-owned device workspace in which the
+ * library may keep a dispatch order for one of its passes.
+ *
+ * The strided passes search each line as far as each element's final
+ * distance (paper, Section 2.3.2), so on masks with large foreground
+ * regions some groups of lines carry several times the mean work; run last,
+ * they set the end of the pass.  With a workspace, a 2-D distance request
+ * (unit sampling, no indices) whose column pass takes 16 columns per
+ * workgroup has its row pass estimate each group's work, a one-workgroup kernel
+ * order the groups heaviest first, and the column pass dispatch them in that
+ * order.  Results are identical to tm_edt's, bit for bit: the order
+ * decides only when each group runs.
+ *
+ *   workspace        NULL, or a DEVICE pointer, 4-byte aligned, owned by the
+ *                    caller and not overlapping the input or outputs.
+ *   workspace_bytes  its size.  tm_edt_workspace_size() gives the bytes a
+ *                    request uses (8 per group of 16 columns, 0 when it has
+ *                    no ordered pass); with fewer, or a NULL workspace, the
+ *                    call runs exactly as tm_edt.
+ * The workspace is read and written on `stream`.  A call that uses it leaves
+ * its first half (per-group counters) at zero for the next call; whatever
+ * the workspace holds before a call can change only the order, never a
+ * result, so it needs no initialisation (zero-filled memory gives the best
+ * first order).  Calls that can run at the same time must not share a workspace.
+ * Other arguments and errors as tm_edt, plus TM_ERR_WORKSPACE for a
+ * misaligned workspace and TM_ERR_ALIAS for one that overlaps a buffer.
+ */
+int tm_edt_ws(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
+              const double *sampling, float *out_dist, int32_t *out_idx, void *workspace,
+              size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * tm_edt_workspace_size -- bytes of workspace tm_edt_ws uses for a request
+ * with these shapes and sampling, with (with_indices != 0) or without index
+ * output: 8 per group of 16 columns for the requests it orders (at most
+ * 16384 groups), else 0 (also for arguments tm_edt would reject).  Host-only; no HIP call.  The actual
+ * call also needs the input and output pointers 16-byte aligned to use it.
+ */
+size_t tm_edt_workspace_size(int ndim, const int64_t *shape, int64_t batch, const double *sampling,
+                             int with_indices);
 
 /*
  * tm_edt_sq -- exact integer squared distances (unit sampling).

@@ -5,7 +5,8 @@ turns torch tensors into device pointers, shapes and the current HIP stream,
 and turns status codes into exceptions.  There is no fallback: if the library
 is missing, every call raises.
 
-Entry points with the C names (``tm_edt``, ``tm_edt_sq``, ``tm_edt_signed``,
+Entry points with the C names (``tm_edt``, ``tm_edt_ws``, ``tm_edt_workspace_size``,
+``tm_edt_sq``, ``tm_edt_signed``,
 ``tm_dt_bf``, ``tm_cdt``, ``tm_mask_nonzero``, ``tm_strerror``) plus ``scipy.ndimage``-style
 wrappers (``distance_transform_edt``, ``distance_transform_bf``,
 ``distance_transform_cdt``, ``signed_distance_transform``) over
@@ -46,6 +47,10 @@ def load() -> ctypes.CDLL:
             vp, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
             lib.tm_edt.restype = i32
             lib.tm_edt.argtypes = [vp, i32, vp, i64, vp, vp, vp, vp]
+            lib.tm_edt_ws.restype = i32
+            lib.tm_edt_ws.argtypes = [vp, i32, vp, i64, vp, vp, vp, vp, ctypes.c_size_t, vp]
+            lib.tm_edt_workspace_size.restype = ctypes.c_size_t
+            lib.tm_edt_workspace_size.argtypes = [i32, vp, i64, vp, i32]
             lib.tm_edt_sq.restype = i32
             lib.tm_edt_sq.argtypes = [vp, i32, vp, i64, vp, vp, vp]
             lib.tm_dt_bf.restype = i32
@@ -133,6 +138,59 @@ def tm_edt(in_u8: torch.Tensor, ndim: int, sampling=None, out_dist=None, out_idx
                            ctypes.c_void_p(st))
     if rc != TM_OK:
         raise TMError(rc, "tm_edt")
+
+
+def tm_edt_workspace_size(ndim: int, spatial, batch: int, sampling=None, with_indices=False) -> int:
+    """Calls tm_edt_workspace_size: bytes of workspace tm_edt_ws uses (0: none)."""
+    shape = (ctypes.c_int64 * ndim)(*[int(v) for v in spatial])
+    samp = None
+    if sampling is not None:
+        samp = (ctypes.c_double * ndim)(*[float(v) for v in sampling])
+    return int(load().tm_edt_workspace_size(ndim, shape, int(batch), samp, 1 if with_indices else 0))
+
+
+def tm_edt_ws(in_u8: torch.Tensor, ndim: int, sampling=None, out_dist=None, out_idx=None,
+              workspace=None, stream=None) -> None:
+    """Calls tm_edt_ws: tm_edt with ``workspace`` (a device tensor, any dtype,
+    or None) for the dispatch order of its column pass."""
+    _check_mask(in_u8)
+    spatial, batch = _shape_args(in_u8, ndim)
+    vox = in_u8.numel() // max(batch, 1)
+    _check_out(out_dist, torch.float32, batch * vox, "out_dist", in_u8.device)
+    _check_out(out_idx, torch.int32, batch * vox * ndim, "out_idx", in_u8.device)
+    nbytes = 0
+    if workspace is not None:
+        if workspace.device != in_u8.device or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous tensor on %s" % in_u8.device)
+        nbytes = workspace.numel() * workspace.element_size()
+    shape = (ctypes.c_int64 * ndim)(*spatial)
+    samp = None
+    if sampling is not None:
+        samp = (ctypes.c_double * ndim)(*[float(v) for v in sampling])
+    with torch.cuda.device(in_u8.device):
+        st = _stream_handle(stream)
+        rc = load().tm_edt_ws(_ptr(in_u8), ndim, shape, batch, samp, _ptr(out_dist), _ptr(out_idx),
+                              _ptr(workspace), nbytes, ctypes.c_void_p(st))
+    if rc != TM_OK:
+        raise TMError(rc, "tm_edt_ws")
+
+
+# Workspaces of the scipy-style wrapper, one per (device, stream): calls on one
+# stream run in order, so they can share it.
+_workspaces = {}
+
+
+def _workspace(dev, nbytes: int, stream=None):
+    if nbytes <= 0:
+        return None
+    with torch.cuda.device(dev):
+        key = (dev.index, _stream_handle(stream))
+    with _lock:
+        ws = _workspaces.get(key)
+        if ws is None or ws.numel() * 4 < nbytes:
+            ws = torch.zeros((nbytes + 3) // 4, dtype=torch.int32, device=dev)
+            _workspaces[key] = ws
+    return ws
 
 
 def tm_edt_sq(in_u8: torch.Tensor, ndim: int, out_sq=None, out_idx=None, stream=None) -> None:
@@ -309,7 +367,9 @@ def distance_transform_edt(input: torch.Tensor, sampling=None, return_distances:
         dist_out, dist_back = _out_buffer(distances, mask.shape, torch.float32, dev, "distances")
     if return_indices:
         idx_out, idx_back = _out_buffer(indices, lead + (ndim,) + spatial, torch.int32, dev, "indices")
-    tm_edt(mask, ndim, samp, dist_out, idx_out)
+    batch = int(lead[0]) * int(lead[1])
+    ws = _workspace(dev, tm_edt_workspace_size(ndim, spatial, batch, samp, return_indices))
+    tm_edt_ws(mask, ndim, samp, dist_out, idx_out, ws)
     if dist_back is not None:
         dist_back.copy_(dist_out)
     if idx_back is not None:

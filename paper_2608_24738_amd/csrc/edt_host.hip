@@ -39,6 +39,7 @@
 #include "edt_long.h"
 #include "edt_plane.h"
 #include "edt_lpair.h"
+#include "edt_order.h"
 
 using namespace tmedt;
 
@@ -154,6 +155,8 @@ struct Request {
     int metric;      // kL2 (exact transform) or kL1 / kLinf (chamfer; output in sq)
     bool sgn;        // signed transform EDT(M) - EDT(not M) (kL2, unit, output in dist)
     bool big;        // unit sampling with squared distances that may pass int32
+    uint32_t *ws;    // caller workspace for dispatch orders (may be null), 4-byte aligned
+    uint64_t ws_bytes;
 };
 
 int validate(const uint8_t *in, int ndim, const int64_t *shape, int64_t batch,
@@ -506,6 +509,38 @@ int plan_passes(const Request &r, uint64_t total, bool index_path, FhPlan *fh) {
     return TM_OK;
 }
 
+// Words of the last-axis word scan: 32 positions when 64-position words
+// would leave fewer than kWord32Waves wavefronts (twice the wavefronts, and so
+// twice the loads and stores, in flight), else 64.
+struct WordShape {
+    bool w32;
+    uint32_t nw;     // words per line
+    uint32_t lpw;    // whole lines per wavefront
+};
+
+WordShape word_shape(uint32_t nlast, uint64_t lines) {
+    const uint64_t lpw64 = kWave / (nlast / kWave);
+    const bool w32 = nlast <= uint32_t(32 * kWave) && (lines + lpw64 - 1) / lpw64 < kWord32Waves;
+    const uint32_t nw = nlast / (w32 ? 32 : 64);
+    return {w32, nw, uint32_t(kWave) / nw};
+}
+
+// Groups of 16 columns whose dispatch order the workspace carries, or 0: a
+// 2-D distance request whose row pass is the word scan with the unit field
+// and whose column pass is the packed line pass (k_line_pair16), with words
+// per line dividing 64, whole workgroups of the scan inside one sample, and
+// at most kOrderMax groups.  (On 3-D inputs the packed passes measured no
+// faster in cost order.)
+uint64_t order_groups(const Request &r, const FhPlan *fh, uint64_t total) {
+    if (r.ndim != 2 || !r.unit || r.big || r.idx || r.metric != kL2 || r.sgn || !fh[0].lp16) return 0;
+    const uint32_t n0 = r.shape[0], nlast = r.shape[1];
+    if (nlast % kWave != 0 || nlast > uint32_t(kWave * kWave)) return 0;
+    const WordShape wsh = word_shape(nlast, total / nlast);
+    if (kWave % wsh.nw != 0 || n0 % (4 * wsh.lpw) != 0) return 0;
+    const uint64_t groups = total / n0 / kLpLines;
+    return groups <= kOrderMax ? groups : 0;
+}
+
 int run(Request &r) {
     const int nd = r.ndim;
     uint64_t vox = 1;
@@ -517,6 +552,9 @@ int run(Request &r) {
     if (overlaps(r.in, nin, r.dist, nf) || overlaps(r.in, nin, r.sq, nf) ||
         overlaps(r.in, nin, r.idx, ni) || overlaps(r.dist, nf, r.sq, nf) ||
         overlaps(r.dist, nf, r.idx, ni) || overlaps(r.sq, nf, r.idx, ni))
+        return TM_ERR_ALIAS;
+    if (r.ws && (overlaps(r.ws, r.ws_bytes, r.in, nin) || overlaps(r.ws, r.ws_bytes, r.dist, nf) ||
+                 overlaps(r.ws, r.ws_bytes, r.sq, nf) || overlaps(r.ws, r.ws_bytes, r.idx, ni)))
         return TM_ERR_ALIAS;
 
     // Small 2-D samples (both extents at most 64): one workgroup per sample
@@ -577,6 +615,10 @@ int run(Request &r) {
     }
     const uint32_t nlast = r.shape[nd - 1];
 
+    // Dispatch order of the column pass, kept in the workspace (edt_order.h).
+    uint64_t order_n = r.ws ? order_groups(r, fh, total) : 0;
+    if (order_n && r.ws_bytes < order_workspace_bytes(order_n)) order_n = 0;
+
     int rc;
     // ---- pass over the last axis: nearest zero in each contiguous line ----
     // (computed by the next pass itself when that one reads the mask)
@@ -635,18 +677,16 @@ int run(Request &r) {
         }
         const bool word_ok = nlast % kWave == 0 && nlast <= uint32_t(kWave * kWave) &&
                              uintptr_t(r.in) % 16 == 0 && uintptr_t(out) % 16 == 0;
+        if (!word_ok || mode != kScanFieldInt) order_n = 0;
         if (word_ok) {
             WordScanArgs ws{};
             ws.in = r.in;
             ws.n = nlast;
-            // 32-position words when 64-position words would leave fewer than
-            // kWord32Waves wavefronts: twice the wavefronts, and so twice the
-            // loads and stores, in flight.
             ws.lines = total / nlast;
-            const uint64_t lpw64 = kWave / (nlast / kWave);
-            const bool w32 = nlast <= uint32_t(32 * kWave) && (ws.lines + lpw64 - 1) / lpw64 < kWord32Waves;
-            ws.nw = nlast / (w32 ? 32 : 64);
-            ws.lpw = kWave / ws.nw;
+            const WordShape wsh = word_shape(nlast, ws.lines);
+            const bool w32 = wsh.w32;
+            ws.nw = wsh.nw;
+            ws.lpw = wsh.lpw;
             ws.lps = uint32_t(vox / nlast);
             ws.vox = uint32_t(vox);
             ws.ndim = nd;
@@ -657,19 +697,30 @@ int run(Request &r) {
             ws.cstride = s.cstride;
             ws.dist = s.dist;
             ws.sq = s.sq;
+            ws.cost = r.ws;
+            ws.rows = r.shape[0];
             const uint64_t waves = (ws.lines + ws.lpw - 1) / ws.lpw;
             const dim3 grid(uint32_t((waves + 3) / 4)), block(256);
 #define TM_WORD(M)                                                                            \
     (w32 ? launch("scan_word", k_scan_word<M, 32>, grid, block, 0, r.stream, ws)                  \
          : launch("scan_word", k_scan_word<M, 64>, grid, block, 0, r.stream, ws))
             switch (mode) {
-                case kScanFieldInt: rc = TM_WORD(kScanFieldInt); break;
+                case kScanFieldInt:
+                    if (order_n)
+                        rc = w32 ? launch("scan_word.cost", k_scan_word<kScanFieldInt, 32, true>, grid, block, 0, r.stream, ws)
+                                 : launch("scan_word.cost", k_scan_word<kScanFieldInt, 64, true>, grid, block, 0, r.stream, ws);
+                    else
+                        rc = TM_WORD(kScanFieldInt);
+                    break;
                 case kScanFieldL1: rc = TM_WORD(kScanFieldL1); break;
                 case kScanFieldFlt: rc = TM_WORD(kScanFieldFlt); break;
                 case kScanIndex: rc = TM_WORD(kScanIndex); break;
                 default: rc = TM_WORD(kScanFinal); break;
             }
 #undef TM_WORD
+            if (rc == TM_OK && order_n)
+                rc = launch("order", k_order, dim3(1), dim3(kOrderThreads), 0, r.stream,
+                            OrderArgs{r.ws, uint32_t(order_n)});
         } else if (nlast <= uint32_t(kSpan)) {
             s.span_lines = uint32_t(kSpan) / nlast;
             const uint64_t waves = (uint64_t(s.lines) + s.span_lines - 1) / s.span_lines;
@@ -818,6 +869,7 @@ int run(Request &r) {
                 lp.wall[b] = r.w[b];
             }
             const dim3 lgrid(uint32_t(lines / kLpLines)), lblock(kPsThreads);
+            if (order_n && a == 0 && lgrid.x == order_n) lp.order = r.ws + order_n;
             rc = fin ? launch("line_pair_final", k_line_pair16<true>, lgrid, lblock, p.lds, r.stream, lp)
                      : launch("line_pair", k_line_pair16<false>, lgrid, lblock, p.lds, r.stream, lp);
         } else if (p.ls_lpw) {
@@ -1008,6 +1060,44 @@ extern "C" int tm_edt(const uint8_t *in_u8, int ndim, const int64_t *shape, int6
     return run(r);
 }
 
+extern "C" int tm_edt_ws(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
+                         const double *sampling, float *out_dist, int32_t *out_idx, void *workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+    Request r{};
+    int rc = validate(in_u8, ndim, shape, batch, sampling, out_dist, out_idx, nullptr, r, false);
+    if (rc != TM_OK) return rc;
+    if (workspace && uintptr_t(workspace) % 4 != 0) return TM_ERR_WORKSPACE;
+    r.dist = out_dist;
+    r.sq = nullptr;
+    r.idx = out_idx;
+    r.ws = workspace_bytes ? static_cast<uint32_t *>(workspace) : nullptr;
+    r.ws_bytes = workspace ? workspace_bytes : 0;
+    r.stream = stream;
+    return run(r);
+}
+
+extern "C" size_t tm_edt_workspace_size(int ndim, const int64_t *shape, int64_t batch, const double *sampling,
+                                        int with_indices) {
+    Request r{};
+    // any non-null device addresses: only the shapes matter here
+    const void *dummy = reinterpret_cast<const void *>(uintptr_t(4096));
+    if (validate(static_cast<const uint8_t *>(dummy), ndim, shape, batch, sampling, dummy,
+                 with_indices ? dummy : nullptr, nullptr, r, false) != TM_OK)
+        return 0;
+    r.dist = reinterpret_cast<float *>(uintptr_t(4096));
+    r.idx = with_indices ? reinterpret_cast<int32_t *>(uintptr_t(4096)) : nullptr;
+    if (r.idx || !r.unit || r.big || r.ndim != 2) return 0;
+    uint64_t vox = 1;
+    for (int a = 0; a < r.ndim; ++a) vox *= r.shape[a];
+    const uint64_t total = r.batch * vox;
+    // the fused small 2-D kernel takes both extents up to kSmallMax
+    if (r.shape[0] <= uint32_t(kSmallMax) && r.shape[1] <= uint32_t(kSmallMax)) return 0;
+    FhPlan fh[kMaxDim];
+    if (plan_passes(r, total, false, fh) != TM_OK) return 0;
+    const uint64_t g = order_groups(r, fh, total);
+    return g ? size_t(order_workspace_bytes(g)) : 0;
+}
+
 extern "C" int tm_edt_sq(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
                          int32_t *out_sq, int32_t *out_idx, hipStream_t stream) {
     Request r{};
@@ -1153,6 +1243,7 @@ extern "C" const char *tm_strerror(int status) {
         case TM_ERR_HIP: return "HIP runtime error while enqueuing kernels";
         case TM_ERR_METRIC: return "metric must be euclidean, taxicab or chessboard";
         case TM_ERR_DTYPE: return "element type is not one of tm_dtype";
+        case TM_ERR_WORKSPACE: return "workspace is not 4-byte aligned, or the request needs more than the static workspace";
         default: return "unknown status";
     }
 }

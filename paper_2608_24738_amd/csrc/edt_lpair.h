@@ -46,6 +46,7 @@ struct LinePairArgs {
     uint32_t inner;        // element stride of the line, a multiple of 16
     Div32 div_inner;
     uint32_t mult;         // order of the sets of 4 line groups (coprime to their count)
+    const uint32_t *order; // null, or the line group of each workgroup (a permutation, k_order)
     int32_t ndim;
     uint32_t shape[kMaxDim];
     double wall[kMaxDim];  // ones (virtual element of a final pass)
@@ -151,11 +152,15 @@ __global__ void __launch_bounds__(kPsThreads, 8) k_line_pair16(LinePairArgs a) {
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
 
-    // Workgroups that share 128-byte rows run on one XCD (one L2): within
-    // each full set of 32 workgroups, the 4 that the dispatcher sends to one
-    // XCD take 4 consecutive line groups.
+    // With a schedule (k_order), workgroup b takes line group order[b]:
+    // groups estimated heaviest are dispatched first.  Otherwise workgroups
+    // that share 128-byte rows run on one XCD (one L2): within each full set
+    // of 32 workgroups, the 4 that the dispatcher sends to one XCD take 4
+    // consecutive line groups.
     uint32_t g = blockIdx.x;
-    if (g < (gridDim.x & ~31u)) {
+    if (a.order) {
+        g = a.order[g];
+    } else if (g < (gridDim.x & ~31u)) {
         const uint32_t x = g & 7u, i = g >> 3;
         g = (i >> 2) * 32u + x * 4u + (i & 3u);
         // ... and the sets of 4 line groups are taken in the order

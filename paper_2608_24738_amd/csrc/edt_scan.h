@@ -327,6 +327,18 @@ namespace tmedt {
 // its line from two segmented wave scans, then walks its WB positions left
 // to right (distance to the last zero) and right to left (distance to the
 // next zero), keeping the left zero on ties.
+//
+// COST (field output, when the next pass is the packed line pass over the
+// columns of a 2-D input, k_line_pair16): the scan also estimates that pass's
+// work per group of 16 adjacent columns, as the sum over every fourth element
+// of the group of min(d, 128), d the distance just found along the row.  The
+// column search from an element runs as far as its final distance, which d
+// bounds from above, so groups crossing large foreground regions sum high.
+// Words per line divide 64 and the four waves of a workgroup hold rows of one
+// sample (the host checks both),
+// reduce their sums in LDS after their stores, and add them to the group's
+// counter with one relaxed device-scope atomic per group (k_order, next,
+// turns the counters into the column pass's order).
 // ---------------------------------------------------------------------------
 struct WordScanArgs {
     const uint8_t *in;
@@ -344,10 +356,13 @@ struct WordScanArgs {
     uint64_t cstride;      // kScanIndex: carrier elements per sample
     float *dist;           // kScanFinal outputs (each may be null)
     int32_t *sq;
+    uint32_t *cost;        // COST: one counter per group of 16 columns, [sample][n / 16]
+    uint32_t rows;         // COST: rows per sample, a multiple of 4 lpw
 };
 
-template <int MODE, int WB>
+template <int MODE, int WB, bool COST = false>
 __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
+    static_assert(!COST || MODE == kScanFieldInt, "the cost estimate comes with the unit field");
     static_assert(WB == 32 || WB == 64, "a word holds 32 or 64 positions");
     const int lane = threadIdx.x & (kWave - 1);
     const uint64_t wave = uint64_t(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
@@ -416,6 +431,7 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
         dl[p] = last;             // last zero at or before base + p
     }
     int32_t out[WB];
+    uint32_t csum[WB / 16] = {};      // COST: this lane's share of its groups' sums
 #pragma unroll
     for (int p = WB - 1; p >= 0; --p) {
         if ((mask >> p) & 1ull) next = base + p;
@@ -423,6 +439,7 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
         const int l = x - dl[p], r = next - x;   // l, r >= 0
         const bool left = l <= r;
         const int dd = left ? l : r;
+        if (COST && p % 4 == 0) csum[p / 16] += uint32_t(min(dd, 128));
         const int y = left ? dl[p] : next;        // line-relative zero, valid if dd < kFar / 2
         const bool none = dd >= kFar / 2;
         if (MODE == kScanFieldInt || MODE == kScanFieldL1) {
@@ -481,6 +498,24 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
             __builtin_amdgcn_wave_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        }
+        if (COST) {
+            // sums over the wave's lines (lanes w, w + nw, ...), then over the
+            // workgroup's waves, all of one sample: one atomic per group
+            __shared__ uint32_t cs[256 / kWave][kWave * 4];
+#pragma unroll
+            for (int k = 0; k < WB / 16; ++k) {
+                uint32_t v = live ? csum[k] : 0u;
+                for (int d = nw; d < kWave; d <<= 1) v += __shfl_xor(v, d, kWave);
+                if (lw == 0) cs[threadIdx.x / kWave][w * (WB / 16) + k] = v;
+            }
+            __syncthreads();
+            const uint32_t ng = a.n / 16u, t = threadIdx.x;
+            if (t < ng) {
+                const uint32_t smp_c = uint32_t(uint64_t(blockIdx.x) * (256 / kWave) * a.lpw / a.rows);
+                __hip_atomic_fetch_add(a.cost + uint64_t(smp_c) * ng + t, cs[0][t] + cs[1][t] + cs[2][t] + cs[3][t],
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
         }
     } else {
         if (!live) return;

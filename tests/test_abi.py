@@ -15,6 +15,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 TM_OK, TM_ERR_NDIM, TM_ERR_SHAPE, TM_ERR_BATCH, TM_ERR_NULL = 0, -1, -2, -3, -4
 TM_ERR_NO_OUTPUT, TM_ERR_SAMPLING, TM_ERR_TOO_LARGE, TM_ERR_ALIAS = -5, -6, -7, -8
 TM_ERR_UNSUPPORTED, TM_ERR_HIP, TM_ERR_METRIC, TM_ERR_DTYPE = -9, -10, -11, -12
+TM_ERR_WORKSPACE = -13
 
 FAKE_IN = 0x100000           # never dereferenced: every call below fails validation
 FAKE_OUT = 0x40000000
@@ -49,7 +50,7 @@ def test_host_division_constants(lib):
 
 
 def test_strerror_covers_every_status(lib):
-    for s in range(0, -13, -1):
+    for s in range(0, -14, -1):
         msg = binding.tm_strerror(s)
         assert msg and msg != "unknown status", s
     assert binding.tm_strerror(-99) == "unknown status"
@@ -102,6 +103,48 @@ def test_overlapping_buffers(lib):
     assert call_edt(lib, [16, 16], dist=FAKE_IN + 100) == TM_ERR_ALIAS
     assert call_edt(lib, [16, 16], dist=FAKE_OUT, idx=FAKE_OUT + 4) == TM_ERR_ALIAS
     assert call_sq(lib, [16, 16], sq=FAKE_OUT, idx=FAKE_OUT + 512) == TM_ERR_ALIAS
+
+
+FAKE_WS = 0x20000000
+
+
+def call_edt_ws(lib, shape, batch=1, sampling=None, inp=FAKE_IN, dist=FAKE_OUT, idx=None, ws=FAKE_WS,
+                ws_bytes=1 << 16):
+    sh = (ctypes.c_int64 * len(shape))(*shape)
+    samp = (ctypes.c_double * len(shape))(*sampling) if sampling else None
+    return lib.tm_edt_ws(ctypes.c_void_p(inp), len(shape), sh, batch, samp, dist and ctypes.c_void_p(dist),
+                         idx and ctypes.c_void_p(idx), ws and ctypes.c_void_p(ws), ws_bytes, None)
+
+
+def test_workspace_entry_checks(lib):
+    # tm_edt's checks first, then the workspace's own: 4-byte alignment, and
+    # no overlap with the input or outputs (all refused before any HIP call)
+    assert call_edt_ws(lib, [512, 512], batch=0) == TM_ERR_BATCH
+    assert call_edt_ws(lib, [512, 512], dist=None) == TM_ERR_NO_OUTPUT
+    assert call_edt_ws(lib, [512, 512], sampling=[1.0, -1.0]) == TM_ERR_SAMPLING
+    assert call_edt_ws(lib, [512, 512], ws=FAKE_WS + 2) == TM_ERR_WORKSPACE
+    assert call_edt_ws(lib, [512, 512], ws=FAKE_IN + 4096) == TM_ERR_ALIAS
+    assert call_edt_ws(lib, [512, 512], ws=FAKE_OUT + 64, ws_bytes=8) == TM_ERR_ALIAS
+    assert call_edt_ws(lib, [512, 512], ws=FAKE_OUT - 8, ws_bytes=16) == TM_ERR_ALIAS
+
+
+def test_workspace_size(lib):
+    # 8 bytes per group of 16 columns for 2-D distance requests whose column
+    # pass runs 16 columns per workgroup; nothing for other requests
+    size = binding.tm_edt_workspace_size
+    assert size(2, (512, 512), 32) == 8 * 32 * 512 // 16
+    assert size(2, (512, 512), 32, (1.0, 1.0)) == 8 * 1024          # unit sampling spelled out
+    assert size(2, (256, 512), 16) == 8 * 16 * 512 // 16            # 32-position row words
+    assert size(2, (512, 512), 512) == 8 * 16384                     # the most groups one order holds
+    assert size(2, (512, 512), 32, None, True) == 0                  # indices: other passes
+    assert size(2, (512, 512), 32, (1.0, 2.0)) == 0                  # sampled
+    assert size(3, (128, 128, 128), 8) == 0                          # 3-D
+    assert size(2, (64, 64), 100) == 0                               # one workgroup per sample
+    assert size(2, (1024, 1024), 8) == 0                             # lines past 512 rows
+    assert size(2, (256, 256), 8) == 0                               # too few groups to order
+    assert size(2, (512, 512), 513) == 0                             # more groups than one order holds
+    assert size(2, (512, 512), 0) == 0                               # rejected arguments
+    assert size(9, (1,) * 9, 1) == 0
 
 
 def test_remaining_line_length_limits(lib):
