@@ -135,6 +135,24 @@ size_t tm_edt_workspace_size(int ndim, const int64_t *shape, int64_t batch, cons
                              int with_indices);
 
 /*
+ * tm_edt_noalloc -- tm_edt_ws for callers that cannot allocate device
+ * memory or pass a workspace: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  It allocates nothing: its
+ * workspace is a 64 KiB array in the library's own device memory, one per
+ * device (each device the library runs on holds it until the process ends),
+ * whose address is looked up on the first call on each device.  Requests
+ * whose dispatch order needs more (tm_edt_workspace_size() above 65536
+ * bytes: more than 8192 groups of 16 columns) are refused with
+ * TM_ERR_WORKSPACE before anything is enqueued; requests that need none run
+ * as tm_edt.  Every call on a device shares that device's array and leaves
+ * its counters at zero: calls on one device that overlap in time (on
+ * different streams or threads) race for it.  Results equal tm_edt_ws's.
+ * Arguments and other errors as tm_edt.
+ */
+int tm_edt_noalloc(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
+                   const double *sampling, float *out_dist, int32_t *out_idx, hipStream_t stream);
+
+/*
  * tm_edt_sq -- exact integer squared distances (unit sampling).
  *
  *   out_sq    NULL, or [batch][shape...] int32 squared distances.

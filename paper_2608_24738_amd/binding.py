@@ -5,7 +5,8 @@ turns torch tensors into device pointers, shapes and the current HIP stream,
 and turns status codes into exceptions.  There is no fallback: if the library
 is missing, every call raises.
 
-Entry points with the C names (``tm_edt``, ``tm_edt_ws``, ``tm_edt_workspace_size``,
+Entry points with the C names (``tm_edt``, ``tm_edt_ws``, ``tm_edt_noalloc``,
+``tm_edt_workspace_size``,
 ``tm_edt_sq``, ``tm_edt_signed``,
 ``tm_dt_bf``, ``tm_cdt``, ``tm_mask_nonzero``, ``tm_strerror``) plus ``scipy.ndimage``-style
 wrappers (``distance_transform_edt``, ``distance_transform_bf``,
@@ -49,6 +50,8 @@ def load() -> ctypes.CDLL:
             lib.tm_edt.argtypes = [vp, i32, vp, i64, vp, vp, vp, vp]
             lib.tm_edt_ws.restype = i32
             lib.tm_edt_ws.argtypes = [vp, i32, vp, i64, vp, vp, vp, vp, ctypes.c_size_t, vp]
+            lib.tm_edt_noalloc.restype = i32
+            lib.tm_edt_noalloc.argtypes = [vp, i32, vp, i64, vp, vp, vp, vp]
             lib.tm_edt_workspace_size.restype = ctypes.c_size_t
             lib.tm_edt_workspace_size.argtypes = [i32, vp, i64, vp, i32]
             lib.tm_edt_sq.restype = i32
@@ -173,6 +176,26 @@ def tm_edt_ws(in_u8: torch.Tensor, ndim: int, sampling=None, out_dist=None, out_
                               _ptr(workspace), nbytes, ctypes.c_void_p(st))
     if rc != TM_OK:
         raise TMError(rc, "tm_edt_ws")
+
+
+def tm_edt_noalloc(in_u8: torch.Tensor, ndim: int, sampling=None, out_dist=None, out_idx=None,
+                   stream=None) -> None:
+    """Calls tm_edt_noalloc: tm_edt_ws with the library's static workspace."""
+    _check_mask(in_u8)
+    spatial, batch = _shape_args(in_u8, ndim)
+    vox = in_u8.numel() // max(batch, 1)
+    _check_out(out_dist, torch.float32, batch * vox, "out_dist", in_u8.device)
+    _check_out(out_idx, torch.int32, batch * vox * ndim, "out_idx", in_u8.device)
+    shape = (ctypes.c_int64 * ndim)(*spatial)
+    samp = None
+    if sampling is not None:
+        samp = (ctypes.c_double * ndim)(*[float(v) for v in sampling])
+    with torch.cuda.device(in_u8.device):
+        st = _stream_handle(stream)
+        rc = load().tm_edt_noalloc(_ptr(in_u8), ndim, shape, batch, samp, _ptr(out_dist), _ptr(out_idx),
+                                   ctypes.c_void_p(st))
+    if rc != TM_OK:
+        raise TMError(rc, "tm_edt_noalloc")
 
 
 # Workspaces of the scipy-style wrapper, one per (device, stream): calls on one

@@ -1098,6 +1098,58 @@ extern "C" size_t tm_edt_workspace_size(int ndim, const int64_t *shape, int64_t 
     return g ? size_t(order_workspace_bytes(g)) : 0;
 }
 
+namespace {
+
+// ---------------------------------------------------------------------------
+// Allocation-free workspace of tm_edt_noalloc: one static array per device
+// (each device that loads the library holds its own copy, zero at load, until
+// the process ends).  In host code `scratch` names a host-side stand-in, not
+// the device array: its device address comes from hipGetSymbolAddress, once
+// per device with that device current, and only that address is passed on.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = 64 * 1024;     // the dispatch order of up to 8192 groups
+static __device__ __align__(256) uint32_t scratch[kScratchBytes / 4];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint32_t *g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_address(uint32_t **out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TM_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return TM_ERR_HIP;
+        g_scratch_ptr[dev] = static_cast<uint32_t *>(p);
+    }
+    *out = g_scratch_ptr[dev];
+    return TM_OK;
+}
+
+}  // namespace
+
+extern "C" int tm_edt_noalloc(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
+                              const double *sampling, float *out_dist, int32_t *out_idx, hipStream_t stream) {
+    Request r{};
+    int rc = validate(in_u8, ndim, shape, batch, sampling, out_dist, out_idx, nullptr, r, false);
+    if (rc != TM_OK) return rc;
+    const size_t need = tm_edt_workspace_size(ndim, shape, batch, sampling, out_idx != nullptr);
+    if (need > kScratchBytes) return TM_ERR_WORKSPACE;
+    uint32_t *ws = nullptr;
+    if (need) {
+        rc = scratch_address(&ws);
+        if (rc != TM_OK) return rc;
+    }
+    r.dist = out_dist;
+    r.sq = nullptr;
+    r.idx = out_idx;
+    r.ws = ws;
+    r.ws_bytes = ws ? kScratchBytes : 0;
+    r.stream = stream;
+    return run(r);
+}
+
 extern "C" int tm_edt_sq(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
                          int32_t *out_sq, int32_t *out_idx, hipStream_t stream) {
     Request r{};

@@ -147,6 +147,20 @@ def test_workspace_size(lib):
     assert size(9, (1,) * 9, 1) == 0
 
 
+def test_static_workspace_limit(lib):
+    # tm_edt_noalloc refuses, on the host, requests whose dispatch order needs
+    # more than its 64 KiB static workspace (8192 groups of 16 columns)
+    def call(shape, batch):
+        sh = (ctypes.c_int64 * len(shape))(*shape)
+        return lib.tm_edt_noalloc(ctypes.c_void_p(FAKE_IN), len(shape), sh, batch, None,
+                                  ctypes.c_void_p(FAKE_OUT), None, None)
+    assert binding.tm_edt_workspace_size(2, (512, 512), 257) == 8 * 8224 > 65536
+    assert call([512, 512], 257) == TM_ERR_WORKSPACE
+    assert call([512, 512], 0) == TM_ERR_BATCH
+    sh = (ctypes.c_int64 * 2)(512, 512)
+    assert lib.tm_edt_noalloc(ctypes.c_void_p(FAKE_IN), 2, sh, 1, None, None, None, None) == TM_ERR_NO_OUTPUT
+
+
 def test_remaining_line_length_limits(lib):
     # The exact transform takes strided lines of any length (the envelope of a
     # line too long for LDS lives in the line's own storage); the limits left
