@@ -186,7 +186,8 @@ constexpr int kPsG = 4;             // guard rows on either side
 constexpr int kPsRS = 68;           // tile row stride in words: 8 x 8 lane patches read conflict-free
 constexpr int kPsRows = kPsN + 2 * kPsG;
 constexpr size_t kPsTile = size_t(kPsRows) * kPsRS * 4;
-constexpr size_t kPsLds = 2 * kPsTile;     // signed: U and W
+constexpr int kPsSignedLut = 1024;         // signed: square roots of 0 .. 1023 in LDS
+constexpr size_t kPsLds = 2 * kPsTile + 4 * kPsSignedLut;     // signed: U, W and the table
 
 struct PlaneSignedArgs {
     float *out;            // batch-flat outputs; plane p's bytes at byte offset 65536 p
@@ -277,13 +278,16 @@ __device__ __forceinline__ void ps_search(const uint32_t *tU, const uint32_t *tW
     } while (d < kPsN);
 }
 
+// Square roots of values below kPsSignedLut come from a table in LDS; the
+// bits marking where runs start and end along the rows are recomputed from
+// the class bits when the first search's results are written back, which
+// leaves room for the table beside the two tiles (two workgroups per CU).
 __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) {
     extern __shared__ __attribute__((aligned(16))) uint32_t ps_lds[];
     uint32_t *const tU = ps_lds;
     uint32_t *const tW = ps_lds + kPsRows * kPsRS;
+    uint32_t *const lut = ps_lds + 2 * kPsRows * kPsRS;   // correctly rounded sqrt of 0 .. kPsSignedLut-1
     __shared__ uint16_t cls16[kPsN][8];   // class bits of each row, 16 columns per entry
-    __shared__ uint16_t st16[kPsN][8];    // along the row: class differs from the column before
-    __shared__ uint16_t en16[kPsN][8];    // along the row: class differs from the column after
     const int t = threadIdx.x;
     const int lane = t & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
@@ -306,6 +310,7 @@ __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) 
             cls |= ((b0 >> 7) | ((b1 >> 7) << 1)) << (2 * k);
         }
         cls16[sr][sg] = uint16_t(cls);
+        for (int i = t; i < kPsSignedLut; i += kPsThreads) lut[i] = __builtin_bit_cast(uint32_t, sqrt_rn_int(uint32_t(i)));
         for (int i = t; i < 2 * 2 * kPsG * kPsRS; i += kPsThreads) {
             const int tile = i / (2 * kPsG * kPsRS), k = i % (2 * kPsG * kPsRS);
             const int row = k / kPsRS, col = k % kPsRS;
@@ -318,11 +323,6 @@ __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) 
         const uint32_t up = sr > 0 ? cls16[sr - 1][sg] : cls;
         const uint32_t dn = sr < kPsN - 1 ? cls16[sr + 1][sg] : cls;
         const uint32_t s1 = cls ^ up, e1 = cls ^ dn;
-        // runs along the second axis (rows)
-        const uint32_t lb = sg > 0 ? (cls16[sr][sg - 1] >> 15) & 1u : cls & 1u;
-        const uint32_t rb = sg < 7 ? cls16[sr][sg + 1] & 1u : (cls >> 15) & 1u;
-        st16[sr][sg] = uint16_t((cls ^ ((cls << 1) | lb)) & 0xffffu);
-        en16[sr][sg] = uint16_t((cls ^ ((cls >> 1) | (rb << 15))) & 0xffffu);
         const int o = (sr + kPsG) * kPsRS + 8 * sg;
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
@@ -342,14 +342,22 @@ __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) 
     }
     __syncthreads();
     // results, transposed: tile row = column, word = pair of rows; boundaries of
-    // the runs along the rows
+    // the runs along the rows (class differs from the column before / after)
+    auto bounds = [&](int row, int pc, uint32_t sh, uint32_t &st, uint32_t &en) {
+        const uint32_t c = cls16[row][pc];
+        const uint32_t lb = pc > 0 ? (uint32_t(cls16[row][pc - 1]) >> 15) & 1u : c & 1u;
+        const uint32_t rb = pc < 7 ? uint32_t(cls16[row][pc + 1]) & 1u : (c >> 15) & 1u;
+        st = ((c ^ ((c << 1) | lb)) >> sh) & 3u;
+        en = ((c ^ ((c >> 1) | (rb << 15))) >> sh) & 3u;
+    };
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int pi = wv + kPsWaves * i, pr = pi >> 3, pc = pi & 7;
         const int q = 16 * pr + 2 * rho, c0 = 16 * pc + 2 * jw;
         const uint32_t sh = 2 * jw;
-        const uint32_t eA = (en16[q][pc] >> sh) & 3u, eB = (en16[q + 1][pc] >> sh) & 3u;
-        const uint32_t sA = (st16[q][pc] >> sh) & 3u, sB = (st16[q + 1][pc] >> sh) & 3u;
+        uint32_t sA, eA, sB, eB;
+        bounds(q, pc, sh, sA, eA);
+        bounds(q + 1, pc, sh, sB, eB);
         const uint32_t A = as_word(rA[i]), B = as_word(rB[i]);
         // column c0: (row q, row q+1) = low halves; column c0+1: high halves
         const uint32_t w0 = (A & 0xffffu) | (B << 16), w1 = (A >> 16) | (B & 0xffff0000u);
@@ -370,19 +378,33 @@ __global__ void __launch_bounds__(kPsThreads) k_plane_signed(PlaneSignedArgs a) 
         const int c = 16 * pr + 2 * rho;       // columns c, c + 1
         const int r0 = 16 * pc + 2 * jw;       // rows r0, r0 + 1
         ps_search<true>(tU, tW, c, 8 * pc + jw, fA, fB);
-        auto value = [&](int r, int cc, uint32_t h) {
-            const bool fg = (cls16[r][cc >> 4] >> (cc & 15)) & 1u;
-            uint32_t d2 = h;
-            if (h == 0xffffu)   // one class in the whole sample: the virtual element (-1, 0, 0)
-                d2 = (x0 + 1) * (x0 + 1) + uint32_t(r * r) + uint32_t(cc * cc);
-            const float dv = sqrt_rn_int(d2);
-            return fg ? dv : -dv;
-        };
         // fA = (row r0, row r0+1) at column c; fB the same at column c + 1
+        uint32_t d2[4] = {fA.x, fB.x, fA.y, fB.y};   // (r0, c), (r0, c+1), (r0+1, c), (r0+1, c+1)
+        const u16x2 mx = __builtin_elementwise_max(fA, fB);
+        if (__any(mx.x == 0xffffu || mx.y == 0xffffu)) {
+            // one class in the whole sample: the virtual element (-1, 0, 0)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t r = uint32_t(r0 + (k >> 1)), cc = uint32_t(c + (k & 1));
+                if (d2[k] == 0xffffu) d2[k] = (x0 + 1) * (x0 + 1) + r * r + cc * cc;
+            }
+        }
+        float dv[4];
+        if (__all(d2[0] < uint32_t(kPsSignedLut) && d2[1] < uint32_t(kPsSignedLut) &&
+                  d2[2] < uint32_t(kPsSignedLut) && d2[3] < uint32_t(kPsSignedLut))) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) dv[k] = __builtin_bit_cast(float, lut[d2[k]]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) dv[k] = sqrt_rn_int(d2[k]);
+        }
+        // classes of (r0, c..c+1) and (r0+1, c..c+1): bits c & 15 of the rows' entries
+        const uint32_t cb = uint32_t(c & 15);
+        const uint32_t k0 = (uint32_t(cls16[r0][c >> 4]) >> cb) & 3u, k1 = (uint32_t(cls16[r0 + 1][c >> 4]) >> cb) & 3u;
         *reinterpret_cast<float2 *>(outp + r0 * kPsN + c) =
-            float2{value(r0, c, fA.x), value(r0, c + 1, fB.x)};
+            float2{(k0 & 1u) ? dv[0] : -dv[0], (k0 & 2u) ? dv[1] : -dv[1]};
         *reinterpret_cast<float2 *>(outp + (r0 + 1) * kPsN + c) =
-            float2{value(r0 + 1, c, fA.y), value(r0 + 1, c + 1, fB.y)};
+            float2{(k1 & 1u) ? dv[2] : -dv[2], (k1 & 2u) ? dv[3] : -dv[3]};
     }
 }
 
