@@ -155,3 +155,31 @@ def test_scipy_wrapper_uses_the_workspace():
     assert "order" in names, names
     ora = edt_oracle.edt(mask[:, 0], 2, None, want_sq=False, want_dist=True, nthreads=16)
     assert np.array_equal(d.cpu().numpy()[:, 0], ora["dist"])
+
+
+def test_misaligned_buffers_run_unordered():
+    # the row scan that estimates the costs needs 16-byte aligned input and
+    # output; a misaligned input runs the other scans, without an order
+    import torch
+    from paper_2608_24738_amd import binding
+    dev = torch.device("cuda:0")
+    mask = workloads.make_mask(2, (512, 512), 16)[:, 0].copy()
+    announce("misaligned input shape=%s" % (mask.shape,))
+    big = torch.empty(mask.size + 16, dtype=torch.uint8, device=dev)
+    x = big[1:1 + mask.size].view(mask.shape)
+    x.copy_(torch.from_numpy(mask).to(dev))
+    assert x.data_ptr() % 16 == 1
+    need = binding.tm_edt_workspace_size(2, mask.shape[1:], mask.shape[0])
+    ws = torch.zeros(need // 4, dtype=torch.int32, device=dev)
+    d = torch.empty(mask.shape, dtype=torch.float32, device=dev)
+    binding.prof_enable(64)
+    try:
+        binding.tm_edt_ws(x, 2, None, d, None, ws)
+        torch.cuda.synchronize()
+        names = [n for n, _ in binding.prof_read()]
+    finally:
+        binding.prof_enable(0)
+    assert "order" not in names and "scan_word.cost" not in names, names
+    ora = edt_oracle.edt(mask, 2, None, want_sq=False, want_dist=True, nthreads=16)
+    check_against_oracle(mask, 2, None, {"dist": d.cpu().numpy()}, ora)
+    assert not ws.cpu().numpy().any()
