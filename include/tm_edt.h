@@ -100,17 +100,18 @@ int tm_edt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch,
  * distance (paper, Section 2.3.2), so on masks with large foreground
  * regions some groups of lines carry several times the mean work; run last,
  * they set the end of the pass.  With a workspace, a 2-D distance request
- * (unit sampling, no indices) whose column pass takes 16 columns per
- * workgroup has its row pass estimate each group's work, a one-workgroup kernel
- * order the groups heaviest first, and the column pass dispatch them in that
- * order.  Results are identical to tm_edt's, bit for bit: the order
+ * (unit sampling, no indices) whose column pass runs at least 1024
+ * workgroups of 16 columns (rows of at most 512) or of 8 columns (longer
+ * rows, ordered in units of four such workgroups) has its row pass estimate
+ * each group's work, a one-workgroup kernel order the groups heaviest first,
+ * and the column pass dispatch them in that order.  Results are identical to tm_edt's, bit for bit: the order
  * decides only when each group runs.
  *
  *   workspace        NULL, or a DEVICE pointer, 4-byte aligned, owned by the
  *                    caller and not overlapping the input or outputs.
  *   workspace_bytes  its size.  tm_edt_workspace_size() gives the bytes a
- *                    request uses (8 per group of 16 columns, 0 when it has
- *                    no ordered pass); with fewer, or a NULL workspace, the
+ *                    request uses (8 per ordered group of 16 or 32 columns,
+ *                    0 when it has no ordered pass); with fewer, or a NULL workspace, the
  *                    call runs exactly as tm_edt.
  * The workspace is read and written on `stream`.  A call that uses it leaves
  * its first half (per-group counters) at zero for the next call; whatever
@@ -127,8 +128,9 @@ int tm_edt_ws(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batc
 /*
  * tm_edt_workspace_size -- bytes of workspace tm_edt_ws uses for a request
  * with these shapes and sampling, with (with_indices != 0) or without index
- * output: 8 per group of 16 columns for the requests it orders (at most
- * 16384 groups), else 0 (also for arguments tm_edt would reject).  Host-only; no HIP call.  The actual
+ * output: 8 per ordered group of 16 or 32 columns for the requests it
+ * orders (at most 16384 groups), else 0 (also for arguments tm_edt would
+ * reject).  Host-only; no HIP call.  The actual
  * call also needs the input and output pointers 16-byte aligned to use it.
  */
 size_t tm_edt_workspace_size(int ndim, const int64_t *shape, int64_t batch, const double *sampling,
@@ -142,7 +144,7 @@ size_t tm_edt_workspace_size(int ndim, const int64_t *shape, int64_t batch, cons
  * device (each device the library runs on holds it until the process ends),
  * whose address is looked up on the first call on each device.  Requests
  * whose dispatch order needs more (tm_edt_workspace_size() above 65536
- * bytes: more than 8192 groups of 16 columns) are refused with
+ * bytes: more than 8192 ordered groups) are refused with
  * TM_ERR_WORKSPACE before anything is enqueued; requests that need none run
  * as tm_edt.  Every call on a device shares that device's array and leaves
  * its counters at zero: calls on one device that overlap in time (on

@@ -525,20 +525,37 @@ WordShape word_shape(uint32_t nlast, uint64_t lines) {
     return {w32, nw, uint32_t(kWave) / nw};
 }
 
-// Groups of 16 columns whose dispatch order the workspace carries, or 0: a
-// 2-D distance request whose row pass is the word scan with the unit field
-// and whose column pass is the packed line pass (k_line_pair16), with words
-// per line dividing 64, whole workgroups of the scan inside one sample, and
-// at most kOrderMax groups.  (On 3-D inputs the packed passes measured no
-// faster in cost order.)
-uint64_t order_groups(const Request &r, const FhPlan *fh, uint64_t total) {
-    if (r.ndim != 2 || !r.unit || r.big || r.idx || r.metric != kL2 || r.sgn || !fh[0].lp16) return 0;
+// Groups of columns below which a dispatch order is not kept: with one or
+// two workgroups per slot of the chip (two per CU) the heaviest groups start
+// early anyway, and the order's own kernel would cost more than it saves.
+constexpr uint64_t kOrderMinGroups = 1024;
+
+// The column pass whose dispatch order the workspace carries: a 2-D
+// distance request whose row pass is the word scan with the unit field and
+// whose column pass takes `width` adjacent columns per workgroup
+// (k_line_pair16: 16; k_line_search: 8 or 4), with words per line dividing
+// 64, whole workgroups of the scan inside one sample, at most 256 groups per
+// row and kOrderMinGroups to kOrderMax groups.  groups = 0: none.  (On 3-D
+// inputs the packed passes measured no faster in cost order.)
+struct OrderPlan {
+    uint64_t groups;
+    uint32_t width;
+};
+
+OrderPlan order_groups(const Request &r, const FhPlan *fh, uint64_t total) {
+    if (r.ndim != 2 || !r.unit || r.big || r.idx || r.metric != kL2 || r.sgn) return {0, 0};
+    // k_line_search orders units of four groups of 8 lines (32 columns)
+    const uint32_t width = fh[0].lp16 ? uint32_t(kLpLines)
+                           : (!fh[0].tiled16 && fh[0].ls_lpw == 8) ? 32u : 0u;
+    if (!width) return {0, 0};
     const uint32_t n0 = r.shape[0], nlast = r.shape[1];
-    if (nlast % kWave != 0 || nlast > uint32_t(kWave * kWave)) return 0;
+    if (nlast % kWave != 0 || nlast > uint32_t(kWave * kWave) || nlast / width > 256) return {0, 0};
     const WordShape wsh = word_shape(nlast, total / nlast);
-    if (kWave % wsh.nw != 0 || n0 % (4 * wsh.lpw) != 0) return 0;
-    const uint64_t groups = total / n0 / kLpLines;
-    return groups <= kOrderMax ? groups : 0;
+    if (kWave % wsh.nw != 0 || n0 % (4 * wsh.lpw) != 0) return {0, 0};
+    const uint64_t groups = total / n0 / width;
+    const uint64_t workgroups = total / n0 / (width == 32 ? 8 : width);
+    if (workgroups < kOrderMinGroups || workgroups % 32 != 0 || groups > kOrderMax) return {0, 0};
+    return {groups, width};
 }
 
 int run(Request &r) {
@@ -616,7 +633,8 @@ int run(Request &r) {
     const uint32_t nlast = r.shape[nd - 1];
 
     // Dispatch order of the column pass, kept in the workspace (edt_order.h).
-    uint64_t order_n = r.ws ? order_groups(r, fh, total) : 0;
+    const OrderPlan oplan = r.ws ? order_groups(r, fh, total) : OrderPlan{0, 0};
+    uint64_t order_n = oplan.groups;
     if (order_n && r.ws_bytes < order_workspace_bytes(order_n)) order_n = 0;
 
     int rc;
@@ -706,11 +724,15 @@ int run(Request &r) {
          : launch("scan_word", k_scan_word<M, 64>, grid, block, 0, r.stream, ws))
             switch (mode) {
                 case kScanFieldInt:
-                    if (order_n)
-                        rc = w32 ? launch("scan_word.cost", k_scan_word<kScanFieldInt, 32, true>, grid, block, 0, r.stream, ws)
-                                 : launch("scan_word.cost", k_scan_word<kScanFieldInt, 64, true>, grid, block, 0, r.stream, ws);
-                    else
+                    if (order_n) {
+#define TM_WORD_COST(CW)                                                                                 \
+    (w32 ? launch("scan_word.cost", k_scan_word<kScanFieldInt, 32, CW>, grid, block, 0, r.stream, ws)     \
+         : launch("scan_word.cost", k_scan_word<kScanFieldInt, 64, CW>, grid, block, 0, r.stream, ws))
+                        rc = oplan.width == 16 ? TM_WORD_COST(16) : TM_WORD_COST(32);
+#undef TM_WORD_COST
+                    } else {
                         rc = TM_WORD(kScanFieldInt);
+                    }
                     break;
                 case kScanFieldL1: rc = TM_WORD(kScanFieldL1); break;
                 case kScanFieldFlt: rc = TM_WORD(kScanFieldFlt); break;
@@ -886,6 +908,7 @@ int run(Request &r) {
                 la.shape[b] = r.shape[b];
                 la.wall[b] = r.w[b];
             }
+            if (order_n && a == 0 && p.ls_lpw == 8 && lines == 32 * order_n) la.order = r.ws + order_n;
             const dim3 lgrid(uint32_t((lines + p.ls_lpw - 1) / p.ls_lpw)), lblock(kWave * kLsWaves);
             const char *nm = r.metric == kL2 ? (fin ? "line_search_final" : "line_search")
                                              : (fin ? "cdt_line_final" : "cdt_line");
@@ -1094,7 +1117,7 @@ extern "C" size_t tm_edt_workspace_size(int ndim, const int64_t *shape, int64_t 
     if (r.shape[0] <= uint32_t(kSmallMax) && r.shape[1] <= uint32_t(kSmallMax)) return 0;
     FhPlan fh[kMaxDim];
     if (plan_passes(r, total, false, fh) != TM_OK) return 0;
-    const uint64_t g = order_groups(r, fh, total);
+    const uint64_t g = order_groups(r, fh, total).groups;
     return g ? size_t(order_workspace_bytes(g)) : 0;
 }
 

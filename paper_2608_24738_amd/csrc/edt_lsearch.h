@@ -54,6 +54,7 @@ struct LineSearchArgs {
     int32_t ndim;
     uint32_t shape[kMaxDim];
     double wall[kMaxDim];  // ones (virtual element of a final euclidean pass)
+    const uint32_t *order; // null, or the line group of each workgroup (a permutation, k_order)
 };
 
 // LDS bytes of the staged tile.
@@ -124,15 +125,22 @@ __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs
     const int wv = __builtin_amdgcn_readfirstlane(t / kWave);
     const int j = lane % LPW, sub = lane / LPW;
     const int n = int(a.n);
-    // Workgroups are dealt to the 8 XCDs in turn (workgroup b to XCD b % 8),
-    // and each XCD has its own L2.  Consecutive line groups are adjacent in
-    // memory (four groups of 8 lines fill a 128-byte cache line), so each run
-    // of four consecutive groups goes to the workgroups b, b + 8, b + 16,
-    // b + 24 of one XCD, which run at about the same time and share those
-    // cache lines in its L2.  The last partial set of 32 workgroups keeps the
-    // identity order.
+    // With a schedule (k_order), workgroup b takes line group order[b]:
+    // groups estimated heaviest are dispatched first.  Otherwise: workgroups
+    // are dealt to the 8 XCDs in turn (workgroup b to XCD b % 8), and each
+    // XCD has its own L2.  Consecutive line groups are adjacent in memory
+    // (four groups of 8 lines fill a 128-byte cache line), so each run of four
+    // consecutive groups goes to the workgroups b, b + 8, b + 16, b + 24 of one
+    // XCD, which run at about the same time and share those cache lines in its
+    // L2.  The last partial set of 32 workgroups keeps the identity order.
     uint32_t g = blockIdx.x;
-    if (g < (gridDim.x & ~31u)) {
+    if (a.order) {
+        // units of four consecutive groups (one 128-byte line of each row) in
+        // order; a unit's four groups on the workgroups b, b + 8, b + 16,
+        // b + 24 of one XCD (the grid is a multiple of 32)
+        const uint32_t x = g & 7u, i = g >> 3;
+        g = 4u * a.order[(i >> 2) * 8u + x] + (i & 3u);
+    } else if (g < (gridDim.x & ~31u)) {
         const uint32_t x = g & 7u, i = g >> 3;
         g = (i >> 2) * 32u + x * 4u + (i & 3u);
     }

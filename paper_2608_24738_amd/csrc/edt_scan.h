@@ -328,10 +328,11 @@ namespace tmedt {
 // to right (distance to the last zero) and right to left (distance to the
 // next zero), keeping the left zero on ties.
 //
-// COST (field output, when the next pass is the packed line pass over the
-// columns of a 2-D input, k_line_pair16): the scan also estimates that pass's
-// work per group of 16 adjacent columns, as the sum over every fourth element
-// of the group of min(d, 128), d the distance just found along the row.  The
+// COST = CW > 0 (field output, when the next pass is the final column pass
+// of a 2-D input taking CW adjacent columns per workgroup: k_line_pair16 with
+// 16, k_line_search with 8 or 4): the scan also estimates that pass's work
+// per group of CW columns, as the sum over every fourth element of the group
+// of min(d, 128), d the distance just found along the row.  The
 // column search from an element runs as far as its final distance, which d
 // bounds from above, so groups crossing large foreground regions sum high.
 // Words per line divide 64 and the four waves of a workgroup hold rows of one
@@ -356,13 +357,16 @@ struct WordScanArgs {
     uint64_t cstride;      // kScanIndex: carrier elements per sample
     float *dist;           // kScanFinal outputs (each may be null)
     int32_t *sq;
-    uint32_t *cost;        // COST: one counter per group of 16 columns, [sample][n / 16]
-    uint32_t rows;         // COST: rows per sample, a multiple of 4 lpw
+    uint32_t *cost;        // CW > 0: one counter per group of CW columns, [sample][n / CW]
+    uint32_t rows;         // CW > 0: rows per sample, a multiple of 4 lpw
 };
 
-template <int MODE, int WB, bool COST = false>
+template <int MODE, int WB, int CW = 0>
 __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
+    constexpr bool COST = CW > 0;
     static_assert(!COST || MODE == kScanFieldInt, "the cost estimate comes with the unit field");
+    static_assert(CW == 0 || CW == 16 || CW == 32, "groups of 16 or 32 columns");
+    constexpr int kCG = COST ? WB / CW : 1;     // groups per lane word
     static_assert(WB == 32 || WB == 64, "a word holds 32 or 64 positions");
     const int lane = threadIdx.x & (kWave - 1);
     const uint64_t wave = uint64_t(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
@@ -431,7 +435,7 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
         dl[p] = last;             // last zero at or before base + p
     }
     int32_t out[WB];
-    uint32_t csum[WB / 16] = {};      // COST: this lane's share of its groups' sums
+    uint32_t csum[kCG] = {};          // COST: this lane's share of its groups' sums
 #pragma unroll
     for (int p = WB - 1; p >= 0; --p) {
         if ((mask >> p) & 1ull) next = base + p;
@@ -439,7 +443,7 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
         const int l = x - dl[p], r = next - x;   // l, r >= 0
         const bool left = l <= r;
         const int dd = left ? l : r;
-        if (COST && p % 4 == 0) csum[p / 16] += uint32_t(min(dd, 128));
+        if (COST && p % 4 == 0) csum[p / (COST ? CW : 1)] += uint32_t(min(dd, 128));
         const int y = left ? dl[p] : next;        // line-relative zero, valid if dd < kFar / 2
         const bool none = dd >= kFar / 2;
         if (MODE == kScanFieldInt || MODE == kScanFieldL1) {
@@ -504,13 +508,13 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
             // workgroup's waves, all of one sample: one atomic per group
             __shared__ uint32_t cs[256 / kWave][kWave * 4];
 #pragma unroll
-            for (int k = 0; k < WB / 16; ++k) {
+            for (int k = 0; k < kCG; ++k) {
                 uint32_t v = live ? csum[k] : 0u;
                 for (int d = nw; d < kWave; d <<= 1) v += __shfl_xor(v, d, kWave);
-                if (lw == 0) cs[threadIdx.x / kWave][w * (WB / 16) + k] = v;
+                if (lw == 0) cs[threadIdx.x / kWave][w * kCG + k] = v;
             }
             __syncthreads();
-            const uint32_t ng = a.n / 16u, t = threadIdx.x;
+            const uint32_t ng = a.n / uint32_t(COST ? CW : 1), t = threadIdx.x;
             if (t < ng) {
                 const uint32_t smp_c = uint32_t(uint64_t(blockIdx.x) * (256 / kWave) * a.lpw / a.rows);
                 __hip_atomic_fetch_add(a.cost + uint64_t(smp_c) * ng + t, cs[0][t] + cs[1][t] + cs[2][t] + cs[3][t],

@@ -129,18 +129,21 @@ def test_workspace_entry_checks(lib):
 
 
 def test_workspace_size(lib):
-    # 8 bytes per group of 16 columns for 2-D distance requests whose column
-    # pass runs 16 columns per workgroup; nothing for other requests
+    # 8 bytes per group of columns (16 per workgroup of the packed pass, 32
+    # for four workgroups of 8 of the whole-line search) for 2-D distance
+    # requests with at least 1024 workgroups; nothing for other requests
     size = binding.tm_edt_workspace_size
     assert size(2, (512, 512), 32) == 8 * 32 * 512 // 16
     assert size(2, (512, 512), 32, (1.0, 1.0)) == 8 * 1024          # unit sampling spelled out
-    assert size(2, (256, 512), 16) == 8 * 16 * 512 // 16            # 32-position row words
+    assert size(2, (128, 512), 32) == 8 * 32 * 512 // 16            # 32-position row words
+    assert size(2, (1024, 1024), 8) == 8 * 8 * 1024 // 32           # whole-line search: units of 4 x 8 lines
     assert size(2, (512, 512), 512) == 8 * 16384                     # the most groups one order holds
+    assert size(2, (512, 512), 16) == 0                              # 512 groups: no order
     assert size(2, (512, 512), 32, None, True) == 0                  # indices: other passes
     assert size(2, (512, 512), 32, (1.0, 2.0)) == 0                  # sampled
     assert size(3, (128, 128, 128), 8) == 0                          # 3-D
     assert size(2, (64, 64), 100) == 0                               # one workgroup per sample
-    assert size(2, (1024, 1024), 8) == 0                             # lines past 512 rows
+    assert size(2, (2048, 2048), 2) == 0                             # rows past 256 groups
     assert size(2, (256, 256), 8) == 0                               # too few groups to order
     assert size(2, (512, 512), 513) == 0                             # more groups than one order holds
     assert size(2, (512, 512), 0) == 0                               # rejected arguments

@@ -1,7 +1,9 @@
 """GPU parity of tm_edt_ws, whose workspace carries a dispatch order for the
-column pass of 2-D distance requests: the row scan estimates each group of
-16 columns' work (k_scan_word with the cost estimate), k_order sorts the
-groups heaviest first, and k_line_pair16 takes them in that order.  The
+column pass of 2-D distance requests with at least 1024 groups of columns:
+the row scan estimates each group's work (k_scan_word with the cost
+estimate), k_order sorts the groups heaviest first, and the column pass
+(k_line_pair16, 16 columns per workgroup, or k_line_search, 8) takes them in
+that order.  The
 order decides only when each group runs, so every result must equal the
 oracle's bit for bit, and equal tm_edt's (no workspace), whatever the
 workspace held before the call.  Each case checks which kernels ran.
@@ -16,7 +18,7 @@ from paper_2608_24738_amd import workloads
 pytestmark = pytest.mark.gpu
 
 
-def run_ws(mask, ws_fill=None, ws_bytes=None, sq_too=False):
+def run_ws(mask, ws_fill=None, ws_bytes=None):
     """tm_edt_ws on (batch, n0, n1) ``mask`` with a fresh workspace (zeros,
     or ``ws_fill`` 32-bit words); returns (dist, kernel names, workspace)."""
     import torch
@@ -54,11 +56,11 @@ def run_plain(mask):
     return d.cpu().numpy()
 
 
-def check_ordered(mask, tag, ws_fill=None):
+def check_ordered(mask, tag, ws_fill=None, final="line_pair_final"):
     announce("ordered column pass %s shape=%s" % (tag, mask.shape))
     dist, names, ws, need = run_ws(mask, ws_fill)
     assert need > 0, "this request should take a workspace"
-    assert names == ["scan_word.cost", "order", "line_pair_final"], names
+    assert names == ["scan_word.cost", "order", final], names
     ora = edt_oracle.edt(mask, 2, None, want_sq=False, want_dist=True, nthreads=16)
     check_against_oracle(mask, 2, None, {"dist": dist}, ora)
     assert np.array_equal(dist, run_plain(mask)), "tm_edt_ws and tm_edt differ"
@@ -80,19 +82,33 @@ def test_full_workload_2():
 @pytest.mark.parametrize("p_bg", [0.3, 0.01, 0.0005])
 def test_densities(p_bg):
     rng = np.random.default_rng([41, int(p_bg * 1e4)])
-    mask = (rng.random((16, 512, 512)) >= p_bg).astype(np.uint8)
+    mask = (rng.random((32, 256, 512)) >= p_bg).astype(np.uint8)
     check_ordered(mask, "p_bg=%g" % p_bg)
 
 
 def test_short_batch_32_position_words():
-    # 16 x 256 x 512: few enough rows that the scan takes 32-position words
-    mask = workloads.make_mask(2, (256, 512), 16)[:, 0]
-    check_ordered(mask, "16x256x512")
+    # 32 x 128 x 512: few enough rows that the scan takes 32-position words
+    mask = workloads.make_mask(2, (128, 512), 32)[:, 0]
+    check_ordered(mask, "32x128x512")
+
+
+def test_whole_line_search_full_workload_9():
+    # 8 x 1024^2 discs: columns of 1024 rows, 8 per workgroup of k_line_search
+    mask = workloads.make_mask(9)[:, 0]
+    check_ordered(mask, "8x1024^2 discs", final="line_search_final")
+
+
+@pytest.mark.parametrize("p_bg", [0.01, 0.0002])
+def test_whole_line_search_densities(p_bg):
+    rng = np.random.default_rng([45, int(p_bg * 1e4)])
+    mask = (rng.random((8, 1024, 1024)) >= p_bg).astype(np.uint8)
+    mask[3] = 1                      # no background: the virtual element
+    check_ordered(mask, "1024^2 p_bg=%g" % p_bg, final="line_search_final")
 
 
 def test_samples_without_background_and_ties():
     rng = np.random.default_rng(43)
-    mask = (rng.random((16, 512, 512)) >= 0.002).astype(np.uint8)
+    mask = (rng.random((32, 256, 512)) >= 0.002).astype(np.uint8)
     mask[0] = 1                      # no background: the virtual element
     mask[5] = 0                      # all background
     mask[9] = 1
@@ -101,16 +117,16 @@ def test_samples_without_background_and_ties():
 
 
 def test_workspace_contents_do_not_matter():
-    mask = workloads.make_mask(2, (512, 512), 16)[:, 0]
+    mask = workloads.make_mask(2, (256, 512), 32)[:, 0]
     rng = np.random.default_rng(44)
-    junk = rng.integers(0, 2 ** 32, size=2 * 512, dtype=np.uint64).astype(np.uint32)
+    junk = rng.integers(0, 2 ** 32, size=2 * 1024, dtype=np.uint64).astype(np.uint32)
     check_ordered(mask, "junk workspace", ws_fill=junk)
-    ones = np.full(2 * 512, 0xffffffff, np.uint32)    # counters that wrap when added to
+    ones = np.full(2 * 1024, 0xffffffff, np.uint32)   # counters that wrap when added to
     check_ordered(mask, "all-ones workspace", ws_fill=ones)
 
 
 def test_small_or_missing_workspace_runs_unordered():
-    mask = workloads.make_mask(2, (512, 512), 16)[:, 0]
+    mask = workloads.make_mask(2, (256, 512), 32)[:, 0]
     announce("workspace too small shape=%s" % (mask.shape,))
     want = run_plain(mask)
     for nb in (0, 8):
@@ -125,7 +141,7 @@ def test_reuse_across_calls_and_shapes():
     from paper_2608_24738_amd import binding
     dev = torch.device("cuda:0")
     ws = torch.zeros(2 * 1024, dtype=torch.int32, device=dev)
-    for k, (batch, n0) in enumerate([(32, 512), (16, 256), (32, 512), (16, 512)]):
+    for k, (batch, n0) in enumerate([(32, 512), (32, 128), (32, 256), (32, 512)]):
         mask = workloads.make_mask(2, (n0, 512), batch)[:, 0].copy()
         mask[k % batch] = 1
         announce("reuse %d shape=%s" % (k, mask.shape))
@@ -142,7 +158,7 @@ def test_reuse_across_calls_and_shapes():
 def test_scipy_wrapper_uses_the_workspace():
     import torch
     from paper_2608_24738_amd import binding
-    mask = workloads.make_mask(2, (512, 512), 16)
+    mask = workloads.make_mask(2, (256, 512), 32)
     announce("wrapper shape=%s" % (mask.shape,))
     x = torch.from_numpy(mask).cuda()
     binding.prof_enable(64)
@@ -163,13 +179,14 @@ def test_misaligned_buffers_run_unordered():
     import torch
     from paper_2608_24738_amd import binding
     dev = torch.device("cuda:0")
-    mask = workloads.make_mask(2, (512, 512), 16)[:, 0].copy()
+    mask = workloads.make_mask(2, (256, 512), 32)[:, 0].copy()
     announce("misaligned input shape=%s" % (mask.shape,))
     big = torch.empty(mask.size + 16, dtype=torch.uint8, device=dev)
     x = big[1:1 + mask.size].view(mask.shape)
     x.copy_(torch.from_numpy(mask).to(dev))
     assert x.data_ptr() % 16 == 1
     need = binding.tm_edt_workspace_size(2, mask.shape[1:], mask.shape[0])
+    assert need > 0
     ws = torch.zeros(need // 4, dtype=torch.int32, device=dev)
     d = torch.empty(mask.shape, dtype=torch.float32, device=dev)
     binding.prof_enable(64)

@@ -27,7 +27,7 @@ def test_noalloc_matches_workspace_entry():
     lib = binding.load()
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream().cuda_stream
-    cases = [((512, 512), 32), ((256, 512), 16)]          # the second call smaller
+    cases = [((512, 512), 32), ((128, 512), 32)]          # the second call smaller
     outs = []
     for spatial, batch in cases:
         mask = workloads.make_mask(2, spatial, batch)[:, 0].copy()
