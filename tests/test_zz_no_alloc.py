@@ -59,3 +59,35 @@ def test_noalloc_matches_workspace_entry():
         check_against_oracle(mask, 2, None, {"dist": got}, ora)
         outs.append(got)
     assert len(outs) == 2
+
+
+def test_noalloc_whole_line_search_order():
+    """The order of the whole-line search (units of four 8-column workgroups)
+    in the static workspace: 8 x 1024^2 discs, then a smaller 4 x 768 x 2048
+    input, each equal to tm_edt_ws's result."""
+    import torch
+    from paper_2608_24738_amd import binding
+    lib = binding.load()
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream().cuda_stream
+    for spatial, batch in [((1024, 1024), 8), ((768, 2048), 4)]:
+        mask = workloads.make_mask(9, spatial, batch)[:, 0].copy()
+        x = torch.from_numpy(mask).to(dev)
+        announce("tm_edt_noalloc whole-line search shape=%s" % (mask.shape,))
+        out = torch.empty(mask.shape, dtype=torch.float32, device=dev)
+        binding.prof_enable(64)
+        try:
+            rc = call_noalloc(lib, x, out, stream)
+            torch.cuda.synchronize()
+            names = [n for n, _ in binding.prof_read()]
+        finally:
+            binding.prof_enable(0)
+        assert rc == 0, binding.tm_strerror(rc)
+        need = binding.tm_edt_workspace_size(2, spatial, batch)
+        assert need > 0
+        assert names == ["scan_word.cost", "order", "line_search_final"], names
+        ws = torch.zeros(max(1, need // 4), dtype=torch.int32, device=dev)
+        ref = torch.empty_like(out)
+        binding.tm_edt_ws(x, 2, None, ref, None, ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy(), ref.cpu().numpy())
