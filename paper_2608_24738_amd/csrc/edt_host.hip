@@ -525,18 +525,20 @@ WordShape word_shape(uint32_t nlast, uint64_t lines) {
     return {w32, nw, uint32_t(kWave) / nw};
 }
 
-// Groups of columns below which a dispatch order is not kept: with one or
-// two workgroups per slot of the chip (two per CU) the heaviest groups start
+// Workgroups of the column pass below which no dispatch order is kept: with
+// at most two per slot of the chip (two per CU) the heaviest groups start
 // early anyway, and the order's own kernel would cost more than it saves.
 constexpr uint64_t kOrderMinGroups = 1024;
 
 // The column pass whose dispatch order the workspace carries: a 2-D
 // distance request whose row pass is the word scan with the unit field and
-// whose column pass takes `width` adjacent columns per workgroup
-// (k_line_pair16: 16; k_line_search: 8 or 4), with words per line dividing
-// 64, whole workgroups of the scan inside one sample, at most 256 groups per
-// row and kOrderMinGroups to kOrderMax groups.  groups = 0: none.  (On 3-D
-// inputs the packed passes measured no faster in cost order.)
+// whose column pass is ordered in groups of `width` adjacent columns
+// (k_line_pair16: its workgroups' 16; k_line_search with 8 columns per
+// workgroup: units of four workgroups, 32), with words per line dividing 64,
+// whole workgroups of the scan inside one sample, at most 256 groups per row,
+// at least kOrderMinGroups workgroups and at most kOrderMax groups.  groups =
+// 0: none.  (On 3-D inputs the packed passes measured no faster in cost
+// order.)
 struct OrderPlan {
     uint64_t groups;
     uint32_t width;

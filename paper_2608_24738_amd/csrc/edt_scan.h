@@ -329,10 +329,11 @@ namespace tmedt {
 // next zero), keeping the left zero on ties.
 //
 // COST = CW > 0 (field output, when the next pass is the final column pass
-// of a 2-D input taking CW adjacent columns per workgroup: k_line_pair16 with
-// 16, k_line_search with 8 or 4): the scan also estimates that pass's work
-// per group of CW columns, as the sum over every fourth element of the group
-// of min(d, 128), d the distance just found along the row.  The
+// of a 2-D input, dispatched in an order kept in a workspace: k_line_pair16,
+// whose groups are 16 columns, or k_line_search, whose units are four
+// workgroups of 8 columns, 32): the scan also estimates that pass's work per
+// group of CW columns, as the sum over every fourth element of the group of
+// min(d, 128), d the distance just found along the row.  The
 // column search from an element runs as far as its final distance, which d
 // bounds from above, so groups crossing large foreground regions sum high.
 // Words per line divide 64 and the four waves of a workgroup hold rows of one
