@@ -251,9 +251,11 @@ def bench_cdt(args, dev, stream):
     x = torch.from_numpy(mask).to(dev)
     out = torch.empty(mask.shape, dtype=torch.int32, device=dev)
     code = binding.METRICS[metric]
+    ws_bytes = binding.tm_cdt_workspace_size(w.ndim, w.spatial, w.batch, code)
+    ws = torch.zeros(max(1, ws_bytes // 4), dtype=torch.int32, device=dev) if ws_bytes else None
 
     def step():
-        binding.tm_cdt(x, w.ndim, code, out, stream=stream)
+        binding.tm_cdt_ws(x, w.ndim, code, out, ws, stream=stream)
 
     ms, kernels = time_op(step, args, stream)
     total = int(mask.size)
@@ -265,6 +267,7 @@ def bench_cdt(args, dev, stream):
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "int32", "data": "synthetic",
         "config": {"workload": w.name, "metric": metric, "outputs": "int32 distances",
+                   "workspace_bytes": ws_bytes,
                    "mask_sha256": workloads.mask_digest(mask)[:16]},
         "voxels_per_s": total / (ms * 1e-3),
         "roofline": roofline,

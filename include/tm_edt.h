@@ -264,6 +264,19 @@ int tm_edt_signed(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t 
 int tm_cdt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, int metric,
            int32_t *out_dist, hipStream_t stream);
 
+/*
+ * tm_cdt_ws -- tm_cdt with a caller-owned device workspace in which a 2-D
+ * request's column pass (at least 1024 workgroups of 8 columns, ordered in
+ * units of four of them) keeps a heaviest-first dispatch order, as tm_edt_ws
+ * does for the exact transform; results are identical to tm_cdt's.
+ * workspace and workspace_bytes as for tm_edt_ws; tm_cdt_workspace_size()
+ * gives the bytes a request uses (8 per unit of 32 columns, or 0; host only).
+ * Errors: as tm_cdt, plus TM_ERR_WORKSPACE and TM_ERR_ALIAS as for tm_edt_ws.
+ */
+int tm_cdt_ws(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, int metric,
+              int32_t *out_dist, void *workspace, size_t workspace_bytes, hipStream_t stream);
+size_t tm_cdt_workspace_size(int ndim, const int64_t *shape, int64_t batch, int metric);
+
 /* Element types the foreground predicate reads. */
 typedef enum {
     TM_DTYPE_U8 = 0,     /* 1-byte integers: uint8, int8, bool */

@@ -6,7 +6,7 @@ and turns status codes into exceptions.  There is no fallback: if the library
 is missing, every call raises.
 
 Entry points with the C names (``tm_edt``, ``tm_edt_ws``, ``tm_edt_noalloc``,
-``tm_edt_workspace_size``,
+``tm_edt_workspace_size``, ``tm_cdt_ws``, ``tm_cdt_workspace_size``,
 ``tm_edt_sq``, ``tm_edt_signed``,
 ``tm_dt_bf``, ``tm_cdt``, ``tm_mask_nonzero``, ``tm_strerror``) plus ``scipy.ndimage``-style
 wrappers (``distance_transform_edt``, ``distance_transform_bf``,
@@ -50,6 +50,10 @@ def load() -> ctypes.CDLL:
             lib.tm_edt.argtypes = [vp, i32, vp, i64, vp, vp, vp, vp]
             lib.tm_edt_ws.restype = i32
             lib.tm_edt_ws.argtypes = [vp, i32, vp, i64, vp, vp, vp, vp, ctypes.c_size_t, vp]
+            lib.tm_cdt_ws.restype = i32
+            lib.tm_cdt_ws.argtypes = [vp, i32, vp, i64, i32, vp, vp, ctypes.c_size_t, vp]
+            lib.tm_cdt_workspace_size.restype = ctypes.c_size_t
+            lib.tm_cdt_workspace_size.argtypes = [i32, vp, i64, i32]
             lib.tm_edt_noalloc.restype = i32
             lib.tm_edt_noalloc.argtypes = [vp, i32, vp, i64, vp, vp, vp, vp]
             lib.tm_edt_workspace_size.restype = ctypes.c_size_t
@@ -284,6 +288,33 @@ def tm_cdt(in_u8: torch.Tensor, ndim: int, metric: int, out_dist, stream=None) -
         raise TMError(rc, "tm_cdt")
 
 
+def tm_cdt_workspace_size(ndim: int, spatial, batch: int, metric: int) -> int:
+    """Calls tm_cdt_workspace_size: bytes of workspace tm_cdt_ws uses (0: none)."""
+    shape = (ctypes.c_int64 * ndim)(*[int(v) for v in spatial])
+    return int(load().tm_cdt_workspace_size(ndim, shape, int(batch), int(metric)))
+
+
+def tm_cdt_ws(in_u8: torch.Tensor, ndim: int, metric: int, out_dist, workspace=None, stream=None) -> None:
+    """Calls tm_cdt_ws: tm_cdt with ``workspace`` (a device tensor or None) for
+    the dispatch order of its column pass."""
+    _check_mask(in_u8)
+    spatial, batch = _shape_args(in_u8, ndim)
+    vox = in_u8.numel() // max(batch, 1)
+    _check_out(out_dist, torch.int32, batch * vox, "out_dist", in_u8.device)
+    nbytes = 0
+    if workspace is not None:
+        if workspace.device != in_u8.device or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous tensor on %s" % in_u8.device)
+        nbytes = workspace.numel() * workspace.element_size()
+    shape = (ctypes.c_int64 * ndim)(*spatial)
+    with torch.cuda.device(in_u8.device):
+        st = _stream_handle(stream)
+        rc = load().tm_cdt_ws(_ptr(in_u8), ndim, shape, batch, int(metric), _ptr(out_dist), _ptr(workspace),
+                              nbytes, ctypes.c_void_p(st))
+    if rc != TM_OK:
+        raise TMError(rc, "tm_cdt_ws")
+
+
 def _normalise_sampling(sampling, ndim):
     if sampling is None:
         return None
@@ -446,7 +477,9 @@ def distance_transform_cdt(input: torch.Tensor, metric: str = "chessboard", dist
         raise ValueError("metric must be 'chessboard' or 'taxicab'")
     mask = _as_mask(input)
     out, back = _out_buffer(distances, mask.shape, torch.int32, mask.device, "distances")
-    tm_cdt(mask, ndim, METRICS[metric], out)
+    batch = int(mask.shape[0]) * int(mask.shape[1])
+    ws = _workspace(mask.device, tm_cdt_workspace_size(ndim, tuple(mask.shape[2:]), batch, METRICS[metric]))
+    tm_cdt_ws(mask, ndim, METRICS[metric], out, ws)
     if back is not None:
         back.copy_(out)
     return None if distances is not None else out

@@ -545,10 +545,10 @@ struct OrderPlan {
 };
 
 OrderPlan order_groups(const Request &r, const FhPlan *fh, uint64_t total) {
-    if (r.ndim != 2 || !r.unit || r.big || r.idx || r.metric != kL2 || r.sgn) return {0, 0};
+    if (r.ndim != 2 || !r.unit || r.big || r.idx || r.sgn) return {0, 0};
     // k_line_search orders units of four groups of 8 lines (32 columns)
-    const uint32_t width = fh[0].lp16 ? uint32_t(kLpLines)
-                           : (!fh[0].tiled16 && fh[0].ls_lpw == 8) ? 32u : 0u;
+    const uint32_t width = (fh[0].lp16 && r.metric == kL2) ? uint32_t(kLpLines)
+                           : (!fh[0].tiled16 && !fh[0].l1long && fh[0].ls_lpw == 8) ? 32u : 0u;
     if (!width) return {0, 0};
     const uint32_t n0 = r.shape[0], nlast = r.shape[1];
     if (nlast % kWave != 0 || nlast > uint32_t(kWave * kWave) || nlast / width > 256) return {0, 0};
@@ -697,7 +697,7 @@ int run(Request &r) {
         }
         const bool word_ok = nlast % kWave == 0 && nlast <= uint32_t(kWave * kWave) &&
                              uintptr_t(r.in) % 16 == 0 && uintptr_t(out) % 16 == 0;
-        if (!word_ok || mode != kScanFieldInt) order_n = 0;
+        if (!word_ok || (mode != kScanFieldInt && mode != kScanFieldL1)) order_n = 0;
         if (word_ok) {
             WordScanArgs ws{};
             ws.in = r.in;
@@ -736,7 +736,14 @@ int run(Request &r) {
                         rc = TM_WORD(kScanFieldInt);
                     }
                     break;
-                case kScanFieldL1: rc = TM_WORD(kScanFieldL1); break;
+                case kScanFieldL1:
+                    if (order_n) {
+                        rc = w32 ? launch("scan_word.cost", k_scan_word<kScanFieldL1, 32, 32>, grid, block, 0, r.stream, ws)
+                                 : launch("scan_word.cost", k_scan_word<kScanFieldL1, 64, 32>, grid, block, 0, r.stream, ws);
+                    } else {
+                        rc = TM_WORD(kScanFieldL1);
+                    }
+                    break;
                 case kScanFieldFlt: rc = TM_WORD(kScanFieldFlt); break;
                 case kScanIndex: rc = TM_WORD(kScanIndex); break;
                 default: rc = TM_WORD(kScanFinal); break;
@@ -1238,18 +1245,45 @@ extern "C" int tm_edt_signed(const uint8_t *in_u8, int ndim, const int64_t *shap
     return run(r);
 }
 
-extern "C" int tm_cdt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, int metric,
-                      int32_t *out_dist, hipStream_t stream) {
+extern "C" int tm_cdt_ws(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, int metric,
+                         int32_t *out_dist, void *workspace, size_t workspace_bytes, hipStream_t stream) {
     Request r{};
     int rc = validate(in_u8, ndim, shape, batch, nullptr, nullptr, out_dist, nullptr, r, false);
     if (rc != TM_OK) return rc;
     if (metric != TM_METRIC_TAXICAB && metric != TM_METRIC_CHESSBOARD) return TM_ERR_METRIC;
+    if (workspace && uintptr_t(workspace) % 4 != 0) return TM_ERR_WORKSPACE;
     r.dist = nullptr;
     r.sq = out_dist;
     r.idx = nullptr;
+    r.ws = workspace_bytes ? static_cast<uint32_t *>(workspace) : nullptr;
+    r.ws_bytes = workspace ? workspace_bytes : 0;
     r.stream = stream;
     r.metric = metric == TM_METRIC_TAXICAB ? kL1 : kLinf;
     return run(r);
+}
+
+extern "C" int tm_cdt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, int metric,
+                      int32_t *out_dist, hipStream_t stream) {
+    return tm_cdt_ws(in_u8, ndim, shape, batch, metric, out_dist, nullptr, 0, stream);
+}
+
+extern "C" size_t tm_cdt_workspace_size(int ndim, const int64_t *shape, int64_t batch, int metric) {
+    Request r{};
+    const void *dummy = reinterpret_cast<const void *>(uintptr_t(4096));
+    if (validate(static_cast<const uint8_t *>(dummy), ndim, shape, batch, nullptr, nullptr, dummy, nullptr, r,
+                 false) != TM_OK)
+        return 0;
+    if (metric != TM_METRIC_TAXICAB && metric != TM_METRIC_CHESSBOARD) return 0;
+    r.sq = reinterpret_cast<int32_t *>(uintptr_t(4096));
+    r.metric = metric == TM_METRIC_TAXICAB ? kL1 : kLinf;
+    if (r.ndim != 2) return 0;
+    uint64_t vox = 1;
+    for (int a = 0; a < r.ndim; ++a) vox *= r.shape[a];
+    const uint64_t total = r.batch * vox;
+    FhPlan fh[kMaxDim];
+    if (plan_passes(r, total, false, fh) != TM_OK) return 0;
+    const uint64_t g = order_groups(r, fh, total).groups;
+    return g ? size_t(order_workspace_bytes(g)) : 0;
 }
 
 extern "C" int tm_mask_nonzero(const void *in, int dtype, int ndim, const int64_t *shape,

@@ -328,10 +328,10 @@ namespace tmedt {
 // to right (distance to the last zero) and right to left (distance to the
 // next zero), keeping the left zero on ties.
 //
-// COST = CW > 0 (field output, when the next pass is the final column pass
-// of a 2-D input, dispatched in an order kept in a workspace: k_line_pair16,
-// whose groups are 16 columns, or k_line_search, whose units are four
-// workgroups of 8 columns, 32): the scan also estimates that pass's work per
+// COST = CW > 0 (unit or chamfer field output, when the next pass is the
+// final column pass of a 2-D input, dispatched in an order kept in a
+// workspace: k_line_pair16, whose groups are 16 columns, or k_line_search,
+// whose units are four workgroups of 8 columns, 32): the scan also estimates that pass's work per
 // group of CW columns, as the sum over every fourth element of the group of
 // min(d, 128), d the distance just found along the row.  The
 // column search from an element runs as far as its final distance, which d
@@ -365,7 +365,8 @@ struct WordScanArgs {
 template <int MODE, int WB, int CW = 0>
 __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
     constexpr bool COST = CW > 0;
-    static_assert(!COST || MODE == kScanFieldInt, "the cost estimate comes with the unit field");
+    static_assert(!COST || MODE == kScanFieldInt || MODE == kScanFieldL1,
+                  "the cost estimate comes with the unit field or the chamfer field");
     static_assert(CW == 0 || CW == 16 || CW == 32, "groups of 16 or 32 columns");
     constexpr int kCG = COST ? WB / CW : 1;     // groups per lane word
     static_assert(WB == 32 || WB == 64, "a word holds 32 or 64 positions");

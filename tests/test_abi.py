@@ -150,6 +150,22 @@ def test_workspace_size(lib):
     assert size(9, (1,) * 9, 1) == 0
 
 
+def test_chamfer_workspace(lib):
+    size = binding.tm_cdt_workspace_size
+    assert size(2, (1024, 1024), 8, 2) == 8 * 8 * 1024 // 32        # units of four 8-column workgroups
+    assert size(2, (1024, 1024), 8, 1) == 8 * 8 * 1024 // 32
+    assert size(2, (256, 256), 8, 2) == 0                            # 256 workgroups: no order
+    assert size(3, (64, 64, 64), 8, 2) == 0
+    assert size(2, (1024, 1024), 8, 0) == 0                          # not a chamfer metric
+    sh = (ctypes.c_int64 * 2)(1024, 1024)
+    def call(metric, ws):
+        return lib.tm_cdt_ws(ctypes.c_void_p(FAKE_IN), 2, sh, 8, metric, ctypes.c_void_p(FAKE_OUT),
+                             ctypes.c_void_p(ws), 4096, None)
+    assert call(0, FAKE_WS) == TM_ERR_METRIC
+    assert call(2, FAKE_WS + 2) == TM_ERR_WORKSPACE
+    assert call(2, FAKE_IN + 64) == TM_ERR_ALIAS
+
+
 def test_static_workspace_limit(lib):
     # tm_edt_noalloc refuses, on the host, requests whose dispatch order needs
     # more than its 64 KiB static workspace (8192 groups of 16 columns)

@@ -191,3 +191,47 @@ def test_rejects_euclidean_and_unknown_metrics():
     for code in (0, 3):
         with pytest.raises(binding.TMError):
             binding.tm_cdt(x, 2, code, out)
+
+
+@pytest.mark.parametrize("metric", CHAMFER)
+def test_ordered_column_pass(metric):
+    """tm_cdt_ws: the column pass of 8 x 1024^2 discs dispatched heaviest
+    first from the row scan's estimates (units of four 8-column workgroups):
+    equal to tm_cdt, the chamfer equations at every element and brute-force
+    values at seeded points (as the full-size test), counters cleared, the
+    order a permutation."""
+    import torch
+    from paper_2608_24738_amd import binding
+    dev = torch.device("cuda:0")
+    mask = workloads.make_mask(7)[:, 0].copy()
+    mask[5] = 1                                     # a sample without background: -1
+    announce("cdt ordered %s shape=%s" % (metric, mask.shape))
+    code = binding.METRICS[metric]
+    need = binding.tm_cdt_workspace_size(2, mask.shape[1:], mask.shape[0], code)
+    assert need > 0
+    x = torch.from_numpy(mask).to(dev)
+    ws = torch.zeros(need // 4, dtype=torch.int32, device=dev)
+    out = torch.empty(mask.shape, dtype=torch.int32, device=dev)
+    binding.prof_enable(64)
+    try:
+        binding.tm_cdt_ws(x, 2, code, out, ws)
+        torch.cuda.synchronize()
+        names = [n for n, _ in binding.prof_read()]
+    finally:
+        binding.prof_enable(0)
+    assert names == ["scan_word.cost", "order", "cdt_line_final"], names
+    got = out.cpu().numpy()
+    assert np.array_equal(got, run_cdt(mask, 2, metric))
+    assert (got[5] == -1).all()
+    rng = np.random.default_rng([7, 6])
+    for b in range(mask.shape[0]):
+        if b == 5:
+            continue
+        assert chamfer_fixed_point_violations(mask[b], got[b], metric) == 0, b
+        pts = np.stack([rng.integers(0, n, 64) for n in mask.shape[1:]], axis=1)
+        ref = edt_oracle.metric_dt_at(mask[b], metric, pts)
+        assert np.array_equal(got[b][tuple(pts.T)], ref.astype(np.int64)), b
+    w = ws.cpu().numpy()
+    units = need // 8
+    assert not w[:units].any()
+    assert np.array_equal(np.sort(w[units:2 * units]), np.arange(units))
