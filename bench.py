@@ -65,7 +65,7 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
     fin = 2 if "i16" in tags else 1 if "i8" in tags else 4     # field bytes read
     fout = 2 if "o16" in tags else 1 if "o8" in tags else 4    # field bytes written
     if base.startswith("scan"):
-        return total * (1 + 4)
+        return total * (1 + fout)
     if base in ("plane_pair", "cdt_plane", "col_scan"):  # reads the mask, writes the field
         return total * (1 + fout)
     if base in ("plane_pair_final", "cdt_plane_final"):

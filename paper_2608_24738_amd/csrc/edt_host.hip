@@ -640,6 +640,11 @@ int run(Request &r) {
     if (order_n && r.ws_bytes < order_workspace_bytes(order_n)) order_n = 0;
 
     int rc;
+    // The row scan writes its distances packed to 16 bits, in strips of pkw
+    // columns, for a first strided pass on k_line_pair16 (16) or on
+    // k_line_search with 8 lines per workgroup (8): half the field's bytes
+    // written and read.
+    int pkw = 0;
     // ---- pass over the last axis: nearest zero in each contiguous line ----
     // (computed by the next pass itself when that one reads the mask)
     if (r.sgn) {
@@ -719,35 +724,46 @@ int run(Request &r) {
             ws.sq = s.sq;
             ws.cost = r.ws;
             ws.rows = r.shape[0];
+            // packed field: the next pass takes it, and every wave's rows pair
+            // up inside one block of that axis's rows
+            if (nd >= 2 && wsh.lpw >= 2 && r.shape[nd - 2] % wsh.lpw == 0 && !fh[nd - 2].l1long &&
+                !fh[nd - 2].tiled16) {
+                const FhPlan &p1 = fh[nd - 2];
+                if (mode == kScanFieldInt && p1.lp16) pkw = 16;
+                else if ((mode == kScanFieldInt || mode == kScanFieldL1) && !p1.lp16 && p1.ls_lpw == 8) pkw = 8;
+            }
+            ws.n1 = nd >= 2 ? r.shape[nd - 2] : 1;
             const uint64_t waves = (ws.lines + ws.lpw - 1) / ws.lpw;
             const dim3 grid(uint32_t((waves + 3) / 4)), block(256);
 #define TM_WORD(M)                                                                            \
     (w32 ? launch("scan_word", k_scan_word<M, 32>, grid, block, 0, r.stream, ws)                  \
          : launch("scan_word", k_scan_word<M, 64>, grid, block, 0, r.stream, ws))
+#define TM_WORD_X(NM, M, CW, PKW)                                                                          \
+    (w32 ? launch(NM, k_scan_word<M, 32, CW, PKW>, grid, block, 0, r.stream, ws)                           \
+         : launch(NM, k_scan_word<M, 64, CW, PKW>, grid, block, 0, r.stream, ws))
+            // cost widths: 16 with k_line_pair16 (pkw 16 or none), 32 with
+            // k_line_search (pkw 8 or none)
             switch (mode) {
                 case kScanFieldInt:
-                    if (order_n) {
-#define TM_WORD_COST(CW)                                                                                 \
-    (w32 ? launch("scan_word.cost", k_scan_word<kScanFieldInt, 32, CW>, grid, block, 0, r.stream, ws)     \
-         : launch("scan_word.cost", k_scan_word<kScanFieldInt, 64, CW>, grid, block, 0, r.stream, ws))
-                        rc = oplan.width == 16 ? TM_WORD_COST(16) : TM_WORD_COST(32);
-#undef TM_WORD_COST
-                    } else {
-                        rc = TM_WORD(kScanFieldInt);
-                    }
+                    if (order_n && pkw == 16) rc = TM_WORD_X("scan_word.cost.o16", kScanFieldInt, 16, 16);
+                    else if (order_n && pkw == 8) rc = TM_WORD_X("scan_word.cost.o16", kScanFieldInt, 32, 8);
+                    else if (order_n && oplan.width == 16) rc = TM_WORD_X("scan_word.cost", kScanFieldInt, 16, 0);
+                    else if (order_n) rc = TM_WORD_X("scan_word.cost", kScanFieldInt, 32, 0);
+                    else if (pkw == 16) rc = TM_WORD_X("scan_word.o16", kScanFieldInt, 0, 16);
+                    else if (pkw == 8) rc = TM_WORD_X("scan_word.o16", kScanFieldInt, 0, 8);
+                    else rc = TM_WORD(kScanFieldInt);
                     break;
                 case kScanFieldL1:
-                    if (order_n) {
-                        rc = w32 ? launch("scan_word.cost", k_scan_word<kScanFieldL1, 32, 32>, grid, block, 0, r.stream, ws)
-                                 : launch("scan_word.cost", k_scan_word<kScanFieldL1, 64, 32>, grid, block, 0, r.stream, ws);
-                    } else {
-                        rc = TM_WORD(kScanFieldL1);
-                    }
+                    if (order_n && pkw) rc = TM_WORD_X("scan_word.cost.o16", kScanFieldL1, 32, 8);
+                    else if (order_n) rc = TM_WORD_X("scan_word.cost", kScanFieldL1, 32, 0);
+                    else if (pkw) rc = TM_WORD_X("scan_word.o16", kScanFieldL1, 0, 8);
+                    else rc = TM_WORD(kScanFieldL1);
                     break;
                 case kScanFieldFlt: rc = TM_WORD(kScanFieldFlt); break;
                 case kScanIndex: rc = TM_WORD(kScanIndex); break;
                 default: rc = TM_WORD(kScanFinal); break;
             }
+#undef TM_WORD_X
 #undef TM_WORD
             if (rc == TM_OK && order_n)
                 rc = launch("order", k_order, dim3(1), dim3(kOrderThreads), 0, r.stream,
@@ -901,8 +917,12 @@ int run(Request &r) {
             }
             const dim3 lgrid(uint32_t(lines / kLpLines)), lblock(kPsThreads);
             if (order_n && a == 0 && lgrid.x == order_n) lp.order = r.ws + order_n;
-            rc = fin ? launch("line_pair_final", k_line_pair16<true>, lgrid, lblock, p.lds, r.stream, lp)
-                     : launch("line_pair", k_line_pair16<false>, lgrid, lblock, p.lds, r.stream, lp);
+            if (pkw == 16 && a == nd - 2)
+                rc = fin ? launch("line_pair_final.i16", k_line_pair16<true, true>, lgrid, lblock, p.lds, r.stream, lp)
+                         : launch("line_pair.i16", k_line_pair16<false, true>, lgrid, lblock, p.lds, r.stream, lp);
+            else
+                rc = fin ? launch("line_pair_final", k_line_pair16<true>, lgrid, lblock, p.lds, r.stream, lp)
+                         : launch("line_pair", k_line_pair16<false>, lgrid, lblock, p.lds, r.stream, lp);
         } else if (p.ls_lpw) {
             LineSearchArgs la{};
             la.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;
@@ -935,7 +955,22 @@ int run(Request &r) {
                           : launch(nm, k_line_search<M, F, W, 4, false, true>, lgrid, lblock, p.lds, r.stream, la)) \
          : (p.ls_lpw == 8 ? launch(nm, k_line_search<M, F, W, 8>, lgrid, lblock, p.lds, r.stream, la)              \
                           : launch(nm, k_line_search<M, F, W, 4>, lgrid, lblock, p.lds, r.stream, la)))
-            if (r.sgn) {
+            if (pkw == 8 && a == nd - 2) {
+                // the row scan's packed field, in strips of 8 lines (ls_lpw 8)
+                nm = r.metric == kL2 ? (fin ? "line_search_final.i16" : "line_search.i16")
+                                     : (fin ? "cdt_line_final.i16" : "cdt_line.i16");
+#define TM_LSP(M, F, W, D) launch(nm, k_line_search<M, F, W, 8, false, D, true>, lgrid, lblock, p.lds, r.stream, la)
+                if (r.metric == kL2)
+                    rc = n >= kLsDirectMinRows ? (fin ? TM_LSP(kL2, true, false, true) : TM_LSP(kL2, false, false, true))
+                                               : (fin ? TM_LSP(kL2, true, false, false) : TM_LSP(kL2, false, false, false));
+                else if (r.metric == kL1)
+                    rc = p.ls_w16 ? (fin ? TM_LSP(kL1, true, true, false) : TM_LSP(kL1, false, true, false))
+                                  : (fin ? TM_LSP(kL1, true, false, false) : TM_LSP(kL1, false, false, false));
+                else
+                    rc = p.ls_w16 ? (fin ? TM_LSP(kLinf, true, true, false) : TM_LSP(kLinf, false, true, false))
+                                  : (fin ? TM_LSP(kLinf, true, false, false) : TM_LSP(kLinf, false, false, false));
+#undef TM_LSP
+            } else if (r.sgn) {
                 nm = fin ? "line_search_signed_final" : "line_search_signed";
                 rc = fin ? TM_LS4(kL2, true, false, true) : TM_LS4(kL2, false, false, true);
             } else if (r.metric == kL2) rc = fin ? TM_LS(kL2, true, false) : TM_LS(kL2, false, false);

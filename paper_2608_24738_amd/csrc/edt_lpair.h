@@ -139,7 +139,12 @@ __device__ __forceinline__ void lp_search32(const int32_t *exact, int n, int q, 
     }
 }
 
-template <bool FINAL>
+// PK: the field is the row scan's packed one (k_scan_word<..., PK>): row r
+// of the strip holds no int32 values, and the 16 distances d of row r (0xffff:
+// no site) are the 16-bit pairs in the 32 bytes at word 8 (r & 1) of row r / 2;
+// the exact copy takes d * d.  Only this workgroup reads or writes its strip,
+// and it writes only after staging all of it.
+template <bool FINAL, bool PK = false>
 __global__ void __launch_bounds__(kPsThreads, 8) k_line_pair16(LinePairArgs a) {
     extern __shared__ __attribute__((aligned(16))) uint32_t lp_lds[];
     const int n = int(a.n);
@@ -187,12 +192,25 @@ __global__ void __launch_bounds__(kPsThreads, 8) k_line_pair16(LinePairArgs a) {
     __syncthreads();
     for (int r = t >> 1; r < n; r += kPsThreads / 2) {
         const int h = t & 1;
-        const int32_t *src = a.buf + base + uint64_t(r) * a.inner + 8 * h;
-        const int4 v0 = *reinterpret_cast<const int4 *>(src);
-        const int4 v1 = *reinterpret_cast<const int4 *>(src + 4);
-        const int32_t v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-        *reinterpret_cast<int4 *>(exact + r * kLpLines + 8 * h) = v0;
-        *reinterpret_cast<int4 *>(exact + r * kLpLines + 8 * h + 4) = v1;
+        int32_t v[8];
+        if constexpr (PK) {
+            const int4 p = *reinterpret_cast<const int4 *>(a.buf + base + uint64_t(r >> 1) * a.inner + 8 * (r & 1) + 4 * h);
+            const uint32_t pw[4] = {uint32_t(p.x), uint32_t(p.y), uint32_t(p.z), uint32_t(p.w)};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t lo = pw[k] & 0xffffu, hi = pw[k] >> 16;
+                v[2 * k] = lo == 0xffffu ? kInfI : int32_t(lo * lo);
+                v[2 * k + 1] = hi == 0xffffu ? kInfI : int32_t(hi * hi);
+            }
+        } else {
+            const int32_t *src = a.buf + base + uint64_t(r) * a.inner + 8 * h;
+            const int4 v0 = *reinterpret_cast<const int4 *>(src);
+            const int4 v1 = *reinterpret_cast<const int4 *>(src + 4);
+            v[0] = v0.x; v[1] = v0.y; v[2] = v0.z; v[3] = v0.w;
+            v[4] = v1.x; v[5] = v1.y; v[6] = v1.z; v[7] = v1.w;
+        }
+        *reinterpret_cast<int4 *>(exact + r * kLpLines + 8 * h) = make_int4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<int4 *>(exact + r * kLpLines + 8 * h + 4) = make_int4(v[4], v[5], v[6], v[7]);
         bool any = false;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {

@@ -108,9 +108,15 @@ __device__ __attribute__((noinline)) uint32_t ls_direct_min(const T *row0, const
 // repeat the end rows of the line (a repeated row read at a larger distance
 // than its own only overestimates), since no single word reads as "no site"
 // for both classes.
-template <int METRIC, bool FINAL, bool W16, int LPW, bool SIGNED = false, bool DIRECT = false>
+// PK: the field is the row scan's packed one (k_scan_word<..., 8>): the
+// distance d along the row (0xffff: no site) of line l of row r of a strip of
+// 8 lines is the 16-bit value l of the 16 bytes at word 4 (r & 1) of row r / 2;
+// the staged value is d * d (euclidean) or d (chamfer).  Only this workgroup
+// reads or writes its strip, and it writes only after staging all of it.
+template <int METRIC, bool FINAL, bool W16, int LPW, bool SIGNED = false, bool DIRECT = false, bool PK = false>
 __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs a) {
     static_assert(!(SIGNED && DIRECT), "the signed field has no few-site lines");
+    static_assert(!PK || (LPW == 8 && !SIGNED), "packed strips hold 8 lines of a distance field");
     static_assert(!SIGNED || (METRIC == kL2 && !W16), "signed transform: euclidean, 32-bit tile");
     using T = typename std::conditional<W16, uint16_t, uint32_t>::type;
     constexpr uint32_t NONE = W16 ? 0xffffu : 0xffffffffu;
@@ -165,7 +171,55 @@ __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs
     const int qs = wv * RPW + sub;
     uint32_t seen = 0;
     constexpr int SB = 8;
-    for (int q0 = qs; q0 < n; q0 += STEP * SB) {
+    if constexpr (PK) {
+        // one packed word per lane and row: lines 2 jp and 2 jp + 1 (the
+        // grid covers whole strips: every line is live), 4 lanes per row
+        constexpr int RPW2 = 2 * RPW, STEP2 = kLsWaves * RPW2;
+        const int jp = lane % (LPW / 2), sub2 = lane / (LPW / 2);
+        const uint32_t *strip = reinterpret_cast<const uint32_t *>(a.buf + (base - uint32_t(j)));
+        uint32_t seen_hi = 0;
+        auto value = [](uint32_t d) { return d == 0xffffu ? kInfI : int32_t(METRIC == kL2 ? d * d : d); };
+        for (int q0 = wv * RPW2 + sub2; q0 < n; q0 += STEP2 * SB) {
+            uint32_t pw[SB];
+#pragma unroll
+            for (int s = 0; s < SB; ++s) {
+                const int q = q0 + s * STEP2;
+                pw[s] = q < n ? strip[uint64_t(q >> 1) * a.inner + 4 * (q & 1) + jp] : 0xffffffffu;
+            }
+#pragma unroll
+            for (int s = 0; s < SB; ++s) {
+                const int q = q0 + s * STEP2;
+                if (q < n) {
+                    const int32_t v0 = value(pw[s] & 0xffffu), v1 = value(pw[s] >> 16);
+                    row0[q * LPW + 2 * jp] = v0 == kInfI ? T(NONE) : T(v0);
+                    row0[q * LPW + 2 * jp + 1] = v1 == kInfI ? T(NONE) : T(v1);
+                    if (DIRECT) {
+                        seen += v0 != kInfI ? 1u : 0u;
+                        seen_hi += v1 != kInfI ? 1u : 0u;
+                    } else {
+                        seen |= v0 != kInfI ? 1u : 0u;
+                        seen_hi |= v1 != kInfI ? 1u : 0u;
+                    }
+                }
+            }
+        }
+        // per line pair: the lanes holding it (jp, jp + LPW / 2, ...) add up
+        if constexpr (DIRECT) {
+#pragma unroll
+            for (int m = LPW / 2; m < kWave; m <<= 1) {
+                seen += uint32_t(__shfl_xor(int(seen), m, kWave));
+                seen_hi += uint32_t(__shfl_xor(int(seen_hi), m, kWave));
+            }
+            if (lane < LPW / 2) {
+                if (seen) atomicAdd(&has_site[2 * jp], seen);
+                if (seen_hi) atomicAdd(&has_site[2 * jp + 1], seen_hi);
+            }
+        } else {
+            if (seen) atomicOr(&has_site[2 * jp], 1u);
+            if (seen_hi) atomicOr(&has_site[2 * jp + 1], 1u);
+        }
+    }
+    for (int q0 = qs; q0 < (PK ? 0 : n); q0 += STEP * SB) {
         int32_t v[SB];
 #pragma unroll
         for (int s = 0; s < SB; ++s) {
@@ -185,7 +239,8 @@ __global__ void __launch_bounds__(kWave * kLsWaves) k_line_search(LineSearchArgs
     }
     // sites per line: the lanes of a wave holding the same line (l, l + LPW,
     // ...) add up their counts, one LDS atomic per line and wave
-    if constexpr (DIRECT) {
+    if constexpr (PK) {
+    } else if constexpr (DIRECT) {
 #pragma unroll
         for (int m = LPW; m < kWave; m <<= 1) seen += uint32_t(__shfl_xor(int(seen), m, kWave));
         if (lane < LPW && seen) atomicAdd(&has_site[j], seen);

@@ -360,11 +360,16 @@ struct WordScanArgs {
     int32_t *sq;
     uint32_t *cost;        // CW > 0: one counter per group of CW columns, [sample][n / CW]
     uint32_t rows;         // CW > 0: rows per sample, a multiple of 4 lpw
+    uint32_t n1;           // PKW > 0: extent of the next axis (rows of a strip), a multiple of lpw
 };
 
-template <int MODE, int WB, int CW = 0>
+template <int MODE, int WB, int CW = 0, int PKW = 0>
 __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
     constexpr bool COST = CW > 0;
+    constexpr bool PK = PKW > 0;
+    static_assert(!PK || MODE == kScanFieldInt || MODE == kScanFieldL1,
+                  "the packed field holds distances along the row (unit or chamfer)");
+    static_assert(PKW == 0 || PKW == 8 || PKW == 16, "strips of 8 or 16 columns");
     static_assert(!COST || MODE == kScanFieldInt || MODE == kScanFieldL1,
                   "the cost estimate comes with the unit field or the chamfer field");
     static_assert(CW == 0 || CW == 16 || CW == 32, "groups of 16 or 32 columns");
@@ -448,7 +453,9 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
         if (COST && p % 4 == 0) csum[p / (COST ? CW : 1)] += uint32_t(min(dd, 128));
         const int y = left ? dl[p] : next;        // line-relative zero, valid if dd < kFar / 2
         const bool none = dd >= kFar / 2;
-        if (MODE == kScanFieldInt || MODE == kScanFieldL1) {
+        if (PK) {
+            out[p] = none ? 0xffff : dd;
+        } else if (MODE == kScanFieldInt || MODE == kScanFieldL1) {
             out[p] = none ? kInfI : (MODE == kScanFieldL1 ? dd : dd * dd);
         } else if (MODE == kScanFieldFlt) {
             const double df = double(dd);
@@ -483,10 +490,43 @@ __global__ void __launch_bounds__(256) k_scan_word(WordScanArgs a) {
             db = MODE == kScanFieldFlt ? reinterpret_cast<int32_t *>(a.field_f) : a.field_i;
             own = pos0;
         }
-        ds[lane] = live ? own : ~0ull;
+        if constexpr (PK) {
+            // Packed field: per strip of PKW columns, row R of the int32
+            // layout (4 PKW bytes) holds the distances of rows 2R and 2R + 1
+            // (0xffff: no zero in the line) as 16-bit pairs of adjacent
+            // columns, row 2R in its first half.  The wave's lpw rows (even,
+            // inside one block of n1 rows) fill lpw / 2 int32 rows, one
+            // contiguous run of 32 WB words; a lane's four-word pieces go to LDS
+            // at their place in the run (one pad piece per eight) and each
+            // store instruction then writes 1 KiB of it.
+            const uint32_t rb = uint32_t(lw >> 1) * a.n + uint32_t(w) * WB + uint32_t(PKW / 2) * uint32_t(lw & 1);
+#pragma unroll
+            for (int k = 0; k < (PK ? WB / PKW : 0); ++k) {
+#pragma unroll
+                for (int j = 0; j < PKW / 8; ++j) {
+                    const int p0 = PKW * k + 8 * j;
+                    auto pair = [&](int q) { return int32_t(uint32_t(out[q]) | (uint32_t(out[q + 1]) << 16)); };
+                    const int4 v = make_int4(pair(p0), pair(p0 + 2), pair(p0 + 4), pair(p0 + 6));
+                    const uint32_t c = (rb + uint32_t(PKW * k + 4 * j)) / 4u;  // strip k: PKW words
+                    st[c + c / 8] = v;
+                }
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            const uint64_t l0 = wave * a.lpw;
+            const uint64_t blk = l0 / a.n1;
+            int4 *dst = reinterpret_cast<int4 *>(a.field_i + (blk * a.n1 + (l0 - blk * a.n1) / 2) * a.n);
+#pragma unroll
+            for (int i = 0; i < WB / 8; ++i) {
+                const int c = lane + kWave * i;
+                dst[c] = st[c + c / 8];
+            }
+        }
+        if (!PK) ds[lane] = live ? own : ~0ull;
         const int src = lane >> 3, piece = lane & 7;
 #pragma unroll
-        for (int h = WB / 32 - 1; h >= 0; --h) {                // the later half is ready first
+        for (int h = PK ? -1 : WB / 32 - 1; h >= 0; --h) {      // the later half is ready first
 #pragma unroll
             for (int i = 0; i < 8; ++i)
                 st[lane * kPad + i] = make_int4(out[32 * h + 4 * i], out[32 * h + 4 * i + 1],

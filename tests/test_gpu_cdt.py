@@ -219,7 +219,7 @@ def test_ordered_column_pass(metric):
         names = [n for n, _ in binding.prof_read()]
     finally:
         binding.prof_enable(0)
-    assert names == ["scan_word.cost", "order", "cdt_line_final"], names
+    assert names == ["scan_word.cost.o16", "order", "cdt_line_final.i16"], names
     got = out.cpu().numpy()
     assert np.array_equal(got, run_cdt(mask, 2, metric))
     assert (got[5] == -1).all()

@@ -29,7 +29,13 @@ def run_named(mask, nd):
     return res, names
 
 
-def check(mask, nd, tag, expect=("line_pair_final",)):
+# kernel names: the row scan packs its distances to 16 bits (".o16") when the
+# column pass is this one and every wave's rows pair up inside one block of
+# rows; the first column pass then reads them (".i16")
+PACKED = ("scan_word.o16", "line_pair_final.i16")
+
+
+def check(mask, nd, tag, expect=PACKED):
     announce("line pair %s shape=%s" % (tag, mask.shape))
     res, names = run_named(mask, nd)
     for e in expect:
@@ -47,8 +53,17 @@ def test_densities(p_bg):
 def test_line_lengths():
     # 256-row columns (1024 wide, 8192 lines) and 64-row columns
     rng = np.random.default_rng(32)
-    check((rng.random((8, 256, 1024)) >= 0.002).astype(np.uint8), 2, "n=256")
-    check((rng.random((16, 64, 8192)) >= 0.01).astype(np.uint8), 2, "n=64")
+    check((rng.random((8, 256, 1024)) >= 0.002).astype(np.uint8), 2, "n=256")     # 32-position words
+    check((rng.random((16, 64, 8192)) >= 0.01).astype(np.uint8), 2, "n=64", expect=("line_pair_final",))
+
+
+def test_packed_field_row_blocks():
+    # rows of 64: a wave scans 32 rows of two 32-position words; blocks of 96
+    # rows hold whole waves (packed field), blocks of 80 do not (int32 field)
+    rng = np.random.default_rng(35)
+    check((rng.random((128, 96, 64)) >= 0.05).astype(np.uint8), 2, "96x64 blocks")
+    check((rng.random((128, 80, 64)) >= 0.05).astype(np.uint8), 2, "80x64 blocks",
+          expect=("scan_word", "line_pair_final"))
 
 
 def test_long_distances_many_sites():
@@ -74,7 +89,7 @@ def test_samples_without_background():
 def test_3d_intermediate_and_final():
     # workload 13 (2 x 256^3 balls): the axis-1 and axis-0 passes both take it
     mask = workloads.make_mask(13)[:, 0]
-    check(mask, 3, "2x256^3 balls", expect=("line_pair", "line_pair_final"))
+    check(mask, 3, "2x256^3 balls", expect=("scan_word.o16", "line_pair.i16", "line_pair_final"))
 
 
 def test_full_workload_2():

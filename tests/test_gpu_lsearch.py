@@ -35,3 +35,49 @@ def test_line_search_grids(spatial, batch):
     assert any(n.startswith("line_search") for n in names), names
     ora = edt_oracle.edt(mask, 2, None, nthreads=16)
     check_against_oracle(mask, 2, None, res, ora)
+
+
+# The row scan hands its distances to a whole-line pass of 8 lines per
+# workgroup packed to 16 bits (".o16" / ".i16") when every wave's rows pair up
+# inside one block of rows (the block's row count a multiple of the wave's
+# rows: 4 for 512-wide rows, 8 for 256-wide ones); otherwise as int32.
+PACKED_CASES = [((520, 512), 2, True),
+                ((514, 512), 1, False),
+                ((304, 256), 4, True),
+                ((300, 256), 4, False)]
+
+
+@pytest.mark.parametrize("metric", ["euclidean", "taxicab", "chessboard"])
+@pytest.mark.parametrize("spatial,batch,packed", PACKED_CASES,
+                         ids=["%dx%d_b%d" % (s[0], s[1], b) for s, b, _ in PACKED_CASES])
+def test_packed_row_field(spatial, batch, packed, metric):
+    import torch
+
+    from paper_2608_24738_amd import binding
+    rng = np.random.default_rng([36, spatial[0], spatial[1], batch])
+    mask = (rng.random((batch,) + spatial) >= 0.003).astype(np.uint8)
+    mask[0, :, 5] = 0                  # a background column: rows with a zero at 5
+    if batch > 1:
+        mask[1] = 1                    # one background element: the direct minimum
+        mask[1, 7, spatial[1] - 9] = 0
+    announce("packed row field %s shape=%s" % (metric, mask.shape))
+    binding.prof_enable(64)
+    try:
+        if metric == "euclidean":
+            res = run_gpu(mask, 2, None, dist=True, idx=False, sq=True)
+        else:
+            x = torch.from_numpy(mask).cuda()
+            out = torch.empty(mask.shape, dtype=torch.int32, device=x.device)
+            binding.tm_cdt(x, 2, binding.METRICS[metric], out)
+            torch.cuda.synchronize()
+            got = out.cpu().numpy()
+        names = [n for n, _ in binding.prof_read()]
+    finally:
+        binding.prof_enable(0)
+    final = "line_search_final" if metric == "euclidean" else "cdt_line_final"
+    want = ["scan_word.o16", final + ".i16"] if packed else ["scan_word", final]
+    assert list(dict.fromkeys(names)) == want, names     # run_gpu makes two calls
+    if metric == "euclidean":
+        check_against_oracle(mask, 2, None, res, edt_oracle.edt(mask, 2, None, nthreads=16))
+    else:
+        assert np.array_equal(got, edt_oracle.cdt(mask, 2, metric, nthreads=16))

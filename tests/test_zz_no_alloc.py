@@ -46,7 +46,7 @@ def test_noalloc_matches_workspace_entry():
             binding.prof_enable(0)
         assert rc == 0, binding.tm_strerror(rc)
         assert torch.cuda.memory_allocated(dev) == before
-        assert names == ["scan_word.cost", "order", "line_pair_final"], names
+        assert names == ["scan_word.cost.o16", "order", "line_pair_final.i16"], names
         # the entry point with a caller workspace, on the same input
         need = binding.tm_edt_workspace_size(2, spatial, batch)
         ws = torch.zeros(need // 4, dtype=torch.int32, device=dev)
@@ -85,7 +85,7 @@ def test_noalloc_whole_line_search_order():
         assert rc == 0, binding.tm_strerror(rc)
         need = binding.tm_edt_workspace_size(2, spatial, batch)
         assert need > 0
-        assert names == ["scan_word.cost", "order", "line_search_final"], names
+        assert names == ["scan_word.cost.o16", "order", "line_search_final.i16"], names
         ws = torch.zeros(max(1, need // 4), dtype=torch.int32, device=dev)
         ref = torch.empty_like(out)
         binding.tm_edt_ws(x, 2, None, ref, None, ws)
