@@ -81,3 +81,35 @@ def test_packed_row_field(spatial, batch, packed, metric):
         check_against_oracle(mask, 2, None, res, edt_oracle.edt(mask, 2, None, nthreads=16))
     else:
         assert np.array_equal(got, edt_oracle.cdt(mask, 2, metric, nthreads=16))
+
+
+@pytest.mark.parametrize("metric", ["euclidean", "taxicab", "chessboard"])
+def test_packed_row_field_3d(metric):
+    # 2 x 4 x 600 x 256: the row scan (32-position words, 8 rows per wave)
+    # packs for the axis-1 whole-line pass, which is not the last one
+    import torch
+
+    from paper_2608_24738_amd import binding
+    rng = np.random.default_rng(37)
+    mask = (rng.random((2, 4, 600, 256)) >= 0.002).astype(np.uint8)
+    mask[1, 2] = 1                     # a plane without background
+    announce("packed row field 3-D %s shape=%s" % (metric, mask.shape))
+    binding.prof_enable(64)
+    try:
+        if metric == "euclidean":
+            res = run_gpu(mask, 3, None, dist=True, idx=False, sq=True)
+        else:
+            x = torch.from_numpy(mask).cuda()
+            out = torch.empty(mask.shape, dtype=torch.int32, device=x.device)
+            binding.tm_cdt(x, 3, binding.METRICS[metric], out)
+            torch.cuda.synchronize()
+            got = out.cpu().numpy()
+        names = list(dict.fromkeys(n for n, _ in binding.prof_read()))
+    finally:
+        binding.prof_enable(0)
+    middle = "line_search.i16" if metric == "euclidean" else "cdt_line.i16"
+    assert names[:2] == ["scan_word.o16", middle], names
+    if metric == "euclidean":
+        check_against_oracle(mask, 3, None, res, edt_oracle.edt(mask, 3, None, nthreads=16))
+    else:
+        assert np.array_equal(got, edt_oracle.cdt(mask, 3, metric, nthreads=16))
