@@ -77,10 +77,11 @@ def algorithmic_bytes(name, total, ndim, want_idx, out_bytes=4):
     if base == "plane_signed_final":         # those bytes in, signed distances out
         return total * (1 + out_bytes)
     if base in ("fh_field", "tile_pair", "cdt_pair", "cdt_line", "cdt_none",
-                "line_search", "line_search_signed", "line_pair"):
+                "line_search", "line_search_signed", "line_pair", "cdt_l1_scan"):
         return total * (fin + fout)
     if base in ("fh_field_final", "tile_pair_final", "cdt_pair_final", "cdt_line_final",
-                "line_search_final", "plane_final", "line_search_signed_final", "line_pair_final"):
+                "line_search_final", "plane_final", "line_search_signed_final", "line_pair_final",
+                "cdt_l1_scan_final"):
         return total * (fin + out_bytes)
     if base == "small2d":                    # mask in; distances (and indices) out
         return total * (1 + out_bytes + (4 * ndim if want_idx else 0))

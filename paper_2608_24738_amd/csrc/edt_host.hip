@@ -30,6 +30,7 @@
 #include "edt_bf.h"
 #include "edt_cdt.h"
 #include "edt_lsearch.h"
+#include "edt_l1scan.h"
 #include "edt_fh.h"
 #include "edt_tidx.h"
 #include "edt_scan.h"
@@ -217,6 +218,7 @@ struct FhPlan {
     uint32_t rbits;  // tidx, unit sampling: bits of the row in a key
     bool lng;        // index carrier, envelope in the line's own storage (k_fh_long)
     bool l1long;     // taxicab, two running minima in place (k_cdt_l1_long)
+    bool l1scan;     // taxicab, whole lines in LDS, prefix and suffix minima (k_cdt_l1_scan)
     bool lp16;       // 16 lines per workgroup, two per packed 16-bit word (k_line_pair16)
 };
 
@@ -406,6 +408,16 @@ int plan_passes(const Request &r, uint64_t total, bool index_path, FhPlan *fh) {
                 continue;
             }
             const uint64_t cmax = r.metric == kL1 ? vmax + n + 4 : std::max<uint64_t>(vmax, n + 4);
+            // taxicab lines whose 8-line groups share rows: prefix and suffix
+            // minima, no search
+            const void *cfield = r.sq;
+            if (r.metric == kL1 && inner % kL1Lines == 0 && n <= kL1MaxN && cmax < (uint64_t(1) << 29) &&
+                l1scan_lds(n) + 1024 <= kLdsBytes && total / n / kL1Lines < (uint64_t(1) << 31) &&
+                uintptr_t(cfield) % 16 == 0) {
+                p.l1scan = true;
+                p.lds = l1scan_lds(n);
+                continue;
+            }
             if (plan_line_search(p, n, total, cmax < uint64_t(kNone16), 1)) continue;
             // taxicab lines of any length: two running minima in place
             if (r.metric == kL1) {
@@ -730,7 +742,8 @@ int run(Request &r) {
                 !fh[nd - 2].tiled16) {
                 const FhPlan &p1 = fh[nd - 2];
                 if (mode == kScanFieldInt && p1.lp16) pkw = 16;
-                else if ((mode == kScanFieldInt || mode == kScanFieldL1) && !p1.lp16 && p1.ls_lpw == 8) pkw = 8;
+                else if ((mode == kScanFieldInt || mode == kScanFieldL1) && !p1.lp16 && (p1.ls_lpw == 8 || p1.l1scan))
+                    pkw = 8;
             }
             ws.n1 = nd >= 2 ? r.shape[nd - 2] : 1;
             const uint64_t waves = (ws.lines + ws.lpw - 1) / ws.lpw;
@@ -923,6 +936,24 @@ int run(Request &r) {
             else
                 rc = fin ? launch("line_pair_final", k_line_pair16<true>, lgrid, lblock, p.lds, r.stream, lp)
                          : launch("line_pair", k_line_pair16<false>, lgrid, lblock, p.lds, r.stream, lp);
+        } else if (p.l1scan) {
+            LineSearchArgs la{};
+            la.buf = r.sq;
+            la.lines = uint32_t(lines);
+            la.n = n;
+            la.inner = uint32_t(inner);
+            la.div_inner = Div32::make(la.inner);
+            const dim3 lgrid(uint32_t(lines / kL1Lines)), lblock(kWave * kL1Lines);
+            const bool lpk = pkw == 8 && a == nd - 2;
+            const char *nm = fin ? (lpk ? "cdt_l1_scan_final.i16" : "cdt_l1_scan_final")
+                                 : (lpk ? "cdt_l1_scan.i16" : "cdt_l1_scan");
+            // 16 rows per lane up to 1024 rows, else 36
+            const bool r16 = n <= uint32_t(16 * kWave);
+#define TM_L1S(F, PK)                                                                                   \
+    (r16 ? launch(nm, k_cdt_l1_scan<F, PK, 16>, lgrid, lblock, p.lds, r.stream, la)                      \
+         : launch(nm, k_cdt_l1_scan<F, PK, 36>, lgrid, lblock, p.lds, r.stream, la))
+            rc = lpk ? (fin ? TM_L1S(true, true) : TM_L1S(false, true)) : (fin ? TM_L1S(true, false) : TM_L1S(false, false));
+#undef TM_L1S
         } else if (p.ls_lpw) {
             LineSearchArgs la{};
             la.buf = r.dist ? reinterpret_cast<int32_t *>(r.dist) : r.sq;

@@ -105,6 +105,8 @@ def test_paired_tile(metric, batch, spatial, p, kernels):
     finally:
         binding.prof_enable(0)
     for k in kernels:
+        if metric == "taxicab" and k == "cdt_line_final":
+            k = "cdt_l1_scan_final"          # taxicab lines: prefix and suffix minima
         assert k in names, (k, names)
 
 
@@ -193,9 +195,9 @@ def test_rejects_euclidean_and_unknown_metrics():
             binding.tm_cdt(x, 2, code, out)
 
 
-@pytest.mark.parametrize("metric", CHAMFER)
+@pytest.mark.parametrize("metric", ["chessboard"])
 def test_ordered_column_pass(metric):
-    """tm_cdt_ws: the column pass of 8 x 1024^2 discs dispatched heaviest
+    """tm_cdt_ws (chessboard): the column pass of 8 x 1024^2 discs dispatched heaviest
     first from the row scan's estimates (units of four 8-column workgroups):
     equal to tm_cdt, the chamfer equations at every element and brute-force
     values at seeded points (as the full-size test), counters cleared, the
@@ -235,3 +237,71 @@ def test_ordered_column_pass(metric):
     units = need // 8
     assert not w[:units].any()
     assert np.array_equal(np.sort(w[units:2 * units]), np.arange(units))
+
+
+def full_size_checks(mask, got, metric, key):
+    """The chamfer equations at every element and brute-force values at 64
+    seeded points per sample (the full-size pattern); -1 on samples without
+    background."""
+    rng = np.random.default_rng([key, 6])
+    for b in range(mask.shape[0]):
+        if not (mask[b] == 0).any():
+            assert (got[b] == -1).all(), b
+            continue
+        assert chamfer_fixed_point_violations(mask[b], got[b], metric) == 0, b
+        pts = np.stack([rng.integers(0, n, 64) for n in mask.shape[1:]], axis=1)
+        ref = edt_oracle.metric_dt_at(mask[b], metric, pts)
+        assert np.array_equal(got[b][tuple(pts.T)], ref.astype(np.int64)), b
+
+
+def test_taxicab_scan_full_workload():
+    """8 x 1024^2 discs, taxicab, through tm_cdt_ws: the row scan packs its
+    distances and the column pass is the prefix / suffix minimum (even work
+    per group: no workspace, no order)."""
+    import torch
+    from paper_2608_24738_amd import binding
+    mask = workloads.make_mask(7)[:, 0].copy()
+    mask[5] = 1
+    announce("taxicab scan shape=%s" % (mask.shape,))
+    code = binding.METRICS["taxicab"]
+    assert binding.tm_cdt_workspace_size(2, mask.shape[1:], mask.shape[0], code) == 0
+    x = torch.from_numpy(mask).cuda()
+    out = torch.empty(mask.shape, dtype=torch.int32, device=x.device)
+    binding.prof_enable(64)
+    try:
+        binding.tm_cdt_ws(x, 2, code, out, None)
+        torch.cuda.synchronize()
+        names = [n for n, _ in binding.prof_read()]
+    finally:
+        binding.prof_enable(0)
+    assert names == ["scan_word.o16", "cdt_l1_scan_final.i16"], names
+    full_size_checks(mask, out.cpu().numpy(), "taxicab", 7)
+
+
+# (batch, spatial, kernel of the last pass): whole taxicab lines of 300, 1000,
+# 2000 and 2304 rows (16 or 36 rows per lane, ragged last lanes, 8-line
+# groups of 64-, 24-, 8- and 16-wide rows), a 3-D case after the paired tile,
+# and 2400 rows (past 36 rows per lane: the whole-line search)
+L1_SCAN = [(2, (300, 64), "cdt_l1_scan_final"),
+           (1, (1000, 24), "cdt_l1_scan_final"),
+           (3, (2000, 8), "cdt_l1_scan_final"),
+           (2, (2304, 16), "cdt_l1_scan_final"),
+           (2, (300, 20, 16), "cdt_l1_scan_final"),
+           (2, (2400, 16), "cdt_line_final")]
+
+
+@pytest.mark.parametrize("batch,spatial,last", L1_SCAN,
+                         ids=["b%d-%s" % (b, "x".join(map(str, s))) for b, s, _ in L1_SCAN])
+def test_taxicab_scan_shapes(batch, spatial, last):
+    from paper_2608_24738_amd import binding
+    mask = rand_mask((batch, 1) + spatial, 0.003, 5000 + sum(spatial))
+    mask[(0, 0) + tuple(n // 2 for n in spatial)] = 0
+    if batch > 1:
+        mask[1] = 1                                # a sample without background
+    binding.prof_enable(64)
+    try:
+        check(mask, len(spatial), "taxicab", "l1 scan")
+        names = [n for n, _ in binding.prof_read()]
+    finally:
+        binding.prof_enable(0)
+    assert last in names, names

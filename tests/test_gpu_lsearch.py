@@ -74,7 +74,8 @@ def test_packed_row_field(spatial, batch, packed, metric):
         names = [n for n, _ in binding.prof_read()]
     finally:
         binding.prof_enable(0)
-    final = "line_search_final" if metric == "euclidean" else "cdt_line_final"
+    final = {"euclidean": "line_search_final", "taxicab": "cdt_l1_scan_final",
+             "chessboard": "cdt_line_final"}[metric]
     want = ["scan_word.o16", final + ".i16"] if packed else ["scan_word", final]
     assert list(dict.fromkeys(names)) == want, names     # run_gpu makes two calls
     if metric == "euclidean":
@@ -107,7 +108,7 @@ def test_packed_row_field_3d(metric):
         names = list(dict.fromkeys(n for n, _ in binding.prof_read()))
     finally:
         binding.prof_enable(0)
-    middle = "line_search.i16" if metric == "euclidean" else "cdt_line.i16"
+    middle = {"euclidean": "line_search.i16", "taxicab": "cdt_l1_scan.i16", "chessboard": "cdt_line.i16"}[metric]
     assert names[:2] == ["scan_word.o16", middle], names
     if metric == "euclidean":
         check_against_oracle(mask, 3, None, res, edt_oracle.edt(mask, 3, None, nthreads=16))
