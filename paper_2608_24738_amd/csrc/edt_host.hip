@@ -265,8 +265,13 @@ constexpr int kNotPlane = 1;
 
 // Wavefronts below which the last-axis word scan takes 32-position words
 // (one per SIMD).  Measured: 8 x 256^2 6.8 against 8.2 us; at 2048 wavefronts
-// (32 x 512^2, 8 x 1024^2) 64-position words stay faster (16.7 against 18.0 us).
+// (32 x 512^2, 8 x 1024^2) 64-position words stay faster with the int32 field
+// (16.7 against 18.0 us).  A unit or chamfer field (written packed to 16 bits
+// where the next pass takes it) of rows up to 512 wide takes 32-position
+// words below kWord32WavesField: 32 x 512^2 with the cost estimate 14.1 ->
+// 11.8 us (HIP events; 8 x 1024^2 unchanged, 15.5 against 15.8 us).
 constexpr uint64_t kWord32Waves = 1024;
+constexpr uint64_t kWord32WavesField = 4096;
 
 int run_plane(Request &r, uint64_t total, uint64_t vox) {
     const int nd = r.ndim;
@@ -530,9 +535,11 @@ struct WordShape {
     uint32_t lpw;    // whole lines per wavefront
 };
 
-WordShape word_shape(uint32_t nlast, uint64_t lines) {
+WordShape word_shape(uint32_t nlast, uint64_t lines, bool field) {
     const uint64_t lpw64 = kWave / (nlast / kWave);
-    const bool w32 = nlast <= uint32_t(32 * kWave) && (lines + lpw64 - 1) / lpw64 < kWord32Waves;
+    const uint64_t waves64 = (lines + lpw64 - 1) / lpw64;
+    const bool w32 = nlast <= uint32_t(32 * kWave) &&
+                     (waves64 < kWord32Waves || (field && nlast <= 512u && waves64 < kWord32WavesField));
     const uint32_t nw = nlast / (w32 ? 32 : 64);
     return {w32, nw, uint32_t(kWave) / nw};
 }
@@ -564,7 +571,7 @@ OrderPlan order_groups(const Request &r, const FhPlan *fh, uint64_t total) {
     if (!width) return {0, 0};
     const uint32_t n0 = r.shape[0], nlast = r.shape[1];
     if (nlast % kWave != 0 || nlast > uint32_t(kWave * kWave) || nlast / width > 256) return {0, 0};
-    const WordShape wsh = word_shape(nlast, total / nlast);
+    const WordShape wsh = word_shape(nlast, total / nlast, true);
     if (kWave % wsh.nw != 0 || n0 % (4 * wsh.lpw) != 0) return {0, 0};
     const uint64_t groups = total / n0 / width;
     const uint64_t workgroups = total / n0 / (width == 32 ? 8 : width);
@@ -720,7 +727,7 @@ int run(Request &r) {
             ws.in = r.in;
             ws.n = nlast;
             ws.lines = total / nlast;
-            const WordShape wsh = word_shape(nlast, ws.lines);
+            const WordShape wsh = word_shape(nlast, ws.lines, mode == kScanFieldInt || mode == kScanFieldL1);
             const bool w32 = wsh.w32;
             ws.nw = wsh.nw;
             ws.lpw = wsh.lpw;
