@@ -266,9 +266,11 @@ int tm_cdt(const uint8_t *in_u8, int ndim, const int64_t *shape, int64_t batch, 
 
 /*
  * tm_cdt_ws -- tm_cdt with a caller-owned device workspace in which a 2-D
- * request's column pass (at least 1024 workgroups of 8 columns, ordered in
- * units of four of them) keeps a heaviest-first dispatch order, as tm_edt_ws
- * does for the exact transform; results are identical to tm_cdt's.
+ * chessboard request's column pass (at least 1024 workgroups of 8 columns,
+ * ordered in units of four of them) keeps a heaviest-first dispatch order, as
+ * tm_edt_ws does for the exact transform; results are identical to tm_cdt's.
+ * Taxicab whole-line passes do the same work on every group and take no
+ * workspace (size 0).
  * workspace and workspace_bytes as for tm_edt_ws; tm_cdt_workspace_size()
  * gives the bytes a request uses (8 per unit of 32 columns, or 0; host only).
  * Errors: as tm_cdt, plus TM_ERR_WORKSPACE and TM_ERR_ALIAS as for tm_edt_ws.
