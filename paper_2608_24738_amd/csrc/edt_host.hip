@@ -18,6 +18,7 @@
 // and distances are recomputed from it.
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include <array>
 #include <atomic>
@@ -64,17 +65,16 @@ Prof &prof() {
     return p;
 }
 
-int prof_begin(const char *name, hipStream_t s) {
+// A slot for one timed launch (-1: not timing); the launch itself records
+// the slot's start and stop events around the kernel (hipExtLaunchKernelGGL),
+// so the interval is the kernel's own, without the queue's gaps.
+int prof_begin(const char *name) {
     Prof &p = prof();
     if (p.cap <= 0) return -1;
     int slot = p.next.fetch_add(1);
     if (slot >= p.cap) return -1;
     p.names[slot] = name;
-    (void)hipEventRecord(p.start[slot], s);
     return slot;
-}
-void prof_end(int slot, hipStream_t s) {
-    if (slot >= 0) (void)hipEventRecord(prof().stop[slot], s);
 }
 
 // ---------------------------------------------------------------------------
@@ -91,7 +91,7 @@ template <typename K, typename Args>
 int launch(const char *name, K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s,
            const Args &args) {
     if (allow_lds(kernel, lds) != hipSuccess) return TM_ERR_HIP;
-    int slot = prof_begin(name, s);
+    int slot = prof_begin(name);
     if (slot >= 0) {
         hipFuncAttributes fa{};
         const bool ok = hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(kernel)) == hipSuccess;
@@ -99,9 +99,11 @@ int launch(const char *name, K kernel, dim3 grid, dim3 block, size_t lds, hipStr
                              int64_t(lds), ok ? int64_t(fa.sharedSizeBytes) : -1,
                              ok ? int64_t(fa.numRegs) : -1, ok ? int64_t(fa.localSizeBytes) : -1};
     }
-    hipLaunchKernelGGL(kernel, grid, block, lds, s, args);
+    if (slot >= 0)
+        hipExtLaunchKernelGGL(kernel, grid, block, uint32_t(lds), s, prof().start[slot], prof().stop[slot], 0u, args);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, lds, s, args);
     hipError_t e = hipGetLastError();
-    prof_end(slot, s);
     return e == hipSuccess ? TM_OK : TM_ERR_HIP;
 }
 
